@@ -1,0 +1,121 @@
+/*
+ * gwtf_mcf.h -- C ABI of the batched min-cost max-flow solver for layered
+ * pipeline-stage graphs, on AMD Instinct MI355X (gfx950).
+ *
+ * The problem (paper Sec. III system model, Sec. IV Eq. 1 and Sec. V-A
+ * Eq. 2): a data node sends microbatches through S pipeline stages of n
+ * relay nodes each and receives them back.  Node i holds at most cap_i
+ * microbatches at a time (its memory, Sec. III) and costs c_i to run one;
+ * sending from node i of stage k to node j of stage k+1 costs the delay
+ * d(i, j).  One microbatch is one unit of flow (Sec. V-A).  The solver finds,
+ * per instance, the largest number of microbatches F the stages can carry
+ * (capped by the data node's supply) and, among flows of that value, one of
+ * minimum total cost sum f(i, j) * d(i, j) (Eq. 2).  Eq. 1's compute halves
+ * summed along a microbatch's closed route equal the sum of the compute costs
+ * of the nodes it visits, so each node's full compute cost is charged on the
+ * node itself; a bandwidth term of Eq. 1 can be folded into arc_cost by the
+ * caller.  The data node is both source and sink (Sec. V-A).
+ *
+ * All arrays passed to these calls are DEVICE pointers on the handle's GPU,
+ * owned by the caller, C-contiguous, batch-major.  Integers only: int32
+ * inputs, int64 flow value and cost.  All work is enqueued on the HIP stream
+ * given to gwtf_mcf_create; calls return after enqueueing and outputs are
+ * valid once the caller has synchronised that stream.  A handle serves one
+ * stream and is not thread-safe; distinct handles are independent.
+ */
+#ifndef GWTF_MCF_H
+#define GWTF_MCF_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct gwtf_mcf gwtf_mcf_t; /* opaque; owns its device workspace */
+
+typedef enum {
+    GWTF_OK = 0,
+    GWTF_ERR_INVALID_ARG = 1,   /* bad pointer, shape or range; nothing enqueued */
+    GWTF_ERR_OUT_OF_MEMORY = 2, /* workspace allocation failed */
+    GWTF_ERR_DEVICE = 3,        /* a HIP runtime call failed; see gwtf_mcf_last_error */
+    GWTF_ERR_NOT_SOLVED = 4,    /* gwtf_mcf_get_flows before any successful solve */
+    GWTF_ERR_RANGE = 5          /* instance range outside the last solved batch */
+} gwtf_status_t;
+
+/* Per-instance status written to gwtf_mcf_batch_t.status. */
+enum {
+    GWTF_INST_OK = 0,
+    GWTF_INST_BAD_INPUT = 1, /* a capacity, cost or supply < 0, or an arc cost < -1 */
+    GWTF_INST_OVERFLOW = 2   /* (2*S*n + 3) * max cost >= 2^29: labels could leave int32 */
+};
+
+/* arc_cost entry meaning "these two nodes share no link". */
+#define GWTF_NO_ARC (-1)
+
+typedef struct {
+    int32_t num_stages;      /* S >= 1 */
+    int32_t nodes_per_stage; /* n >= 1 (a stage with fewer nodes pads with cap 0) */
+    int32_t max_batch;       /* largest batch a solve may pass, >= 1 */
+    int32_t device;          /* HIP device ordinal the handle works on */
+} gwtf_mcf_shape_t;
+
+typedef struct {
+    int32_t batch;           /* B, 1 <= B <= max_batch */
+    const int32_t *node_cap; /* [B][S][n] >= 0; 0 = node absent (crashed / left) */
+    const int32_t *node_cost;/* [B][S][n] >= 0: compute cost c_i of one microbatch */
+    const int32_t *arc_cost; /* [B][S-1][n][n]: [b][k][i][j] = delay from node i of stage k
+                                to node j of stage k+1, >= 0 or GWTF_NO_ARC; NULL iff S == 1 */
+    const int32_t *src_cost; /* [B][n] data node -> stage-0 node delay, >= 0; NULL = all 0 */
+    const int32_t *snk_cost; /* [B][n] stage-(S-1) node -> data node delay, >= 0; NULL = all 0 */
+    const int32_t *supply;   /* [B] >= 0: microbatches the data node injects */
+    int64_t *flow_value;     /* [B] out: F */
+    int64_t *total_cost;     /* [B] out: sum over arcs of flow * cost (Eq. 2) */
+    int32_t *status;         /* [B] out: GWTF_INST_*; a bad instance reports F = cost = 0 */
+} gwtf_mcf_batch_t;
+
+/* Creates a solver for batches of `shape` on shape->device, enqueueing on
+ * `hip_stream` (a hipStream_t; NULL = the device's null stream).  Allocates
+ * the workspace (flows, potentials, fallback state) for shape->max_batch
+ * instances.  *out receives the handle, or NULL on failure. */
+gwtf_status_t gwtf_mcf_create(const gwtf_mcf_shape_t *shape, void *hip_stream, gwtf_mcf_t **out);
+
+/* Solves every instance of the batch (paper Eq. 2 optimum per instance).
+ * Argument errors return GWTF_ERR_INVALID_ARG with nothing enqueued; input
+ * values are checked on the device and reported per instance in status.
+ * Results are deterministic: the same inputs give the same flows. */
+gwtf_status_t gwtf_mcf_solve_batch(gwtf_mcf_t *h, const gwtf_mcf_batch_t *b);
+
+/* Copies the optimal flow of instances [first, first + count) of the last
+ * solved batch into caller device buffers (any may be NULL):
+ *   node_flow [count][S][n]        microbatches through each node
+ *   arc_flow  [count][S-1][n][n]   microbatches on each inter-stage link
+ *   src_flow  [count][n]           data node -> stage-0 node
+ *   snk_flow  [count][n]           stage-(S-1) node -> data node
+ *   potential [count][2*S*n + 3]   node potentials certifying optimality: every
+ *       arc with spare capacity has cost + pi(tail) - pi(head) >= 0.  Vertex
+ *       order: 0 = source root s0, 1 = data node as source s, 2 = data node as
+ *       sink t, 3 + 2*(k*n + i) = node (k, i) entry, 4 + 2*(k*n + i) = its exit
+ *       (the node's compute arc runs entry -> exit; the root s0 -> s arc holds
+ *       the supply). */
+gwtf_status_t gwtf_mcf_get_flows(gwtf_mcf_t *h, int32_t first, int32_t count,
+                                 int32_t *node_flow, int32_t *arc_flow,
+                                 int32_t *src_flow, int32_t *snk_flow, int32_t *potential);
+
+/* Per-instance work counters of the last solve, into a caller device buffer
+ * stats[count][4] (int64): augmenting paths, label-correcting rounds, cost
+ * rows streamed in the dense relaxation (each row is n arc relaxations), and
+ * flow-list (reverse-arc) relaxations. */
+gwtf_status_t gwtf_mcf_get_stats(gwtf_mcf_t *h, int32_t first, int32_t count, int64_t *stats);
+
+/* Frees the handle and its workspace after draining its stream; NULL-safe. */
+void gwtf_mcf_destroy(gwtf_mcf_t *h);
+
+/* Text of the last error on this handle ("" if none); NULL handle gives the
+ * last create error of the calling thread. */
+const char *gwtf_mcf_last_error(const gwtf_mcf_t *h);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* GWTF_MCF_H */

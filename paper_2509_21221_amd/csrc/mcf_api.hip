@@ -1,0 +1,255 @@
+// Host side of the C ABI declared in include/gwtf_mcf.h: argument checks,
+// workspace ownership, and the choice between the LDS-resident solver pass
+// (n <= 64, instance state in the workgroup's LDS) and the global-memory
+// fallback pass (any n, or instances whose flow lists outgrow LDS).
+#include "gwtf_mcf.h"
+#include "mcf_internal.h"
+
+#include <algorithm>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+
+using namespace gwtf;
+
+struct gwtf_mcf {
+    gwtf_mcf_shape_t shape;
+    hipStream_t stream;
+    std::string err;
+    size_t lds_max;
+    // workspace
+    int32_t *route = nullptr, *node_flow = nullptr, *arc_flow = nullptr, *pot = nullptr;
+    int64_t *stats = nullptr;
+    unsigned char *state = nullptr;
+    size_t state_stride = 0;
+    int64_t fallback_slots = 0;
+    int32_t solved = 0; // batch size of the last successful solve (0 = none)
+};
+
+namespace {
+
+thread_local std::string g_create_err;
+
+gwtf_status_t fail(gwtf_mcf_t *h, gwtf_status_t code, const std::string &msg)
+{
+    if (h) h->err = msg;
+    else g_create_err = msg;
+    return code;
+}
+
+gwtf_status_t hip_fail(gwtf_mcf_t *h, hipError_t e, const char *what)
+{
+    return fail(h, GWTF_ERR_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+// Narrow LDS state: flow-list capacity left once the node state and the
+// scratch buffers are placed (0 if the node state alone does not fit).
+int64_t lds_slots(int S, int n, int waves, size_t lds_max)
+{
+    if (n > 64) return 0;
+    size_t fixed = make_layout(S, n, 0, true).total + scratch_bytes(waves, n) + 64;
+    if (fixed >= lds_max) return 0;
+    int64_t slots = int64_t((lds_max - fixed) / 9) - 16;
+    int64_t worst = int64_t(std::max(S - 1, 0)) * n * n;
+    slots = std::min<int64_t>(std::min<int64_t>(slots, worst), 65535);
+    return std::max<int64_t>(slots, 0);
+}
+
+int lds_waves(int n) { return n <= 16 ? 1 : 4; }
+
+void free_ws(gwtf_mcf_t *h)
+{
+    (void)hipFree(h->route);
+    (void)hipFree(h->node_flow);
+    (void)hipFree(h->arc_flow);
+    (void)hipFree(h->pot);
+    (void)hipFree(h->stats);
+    (void)hipFree(h->state);
+    h->route = h->node_flow = h->arc_flow = h->pot = nullptr;
+    h->stats = nullptr;
+    h->state = nullptr;
+}
+
+} // namespace
+
+extern "C" gwtf_status_t gwtf_mcf_create(const gwtf_mcf_shape_t *shape, void *hip_stream, gwtf_mcf_t **out)
+{
+    if (!out) return fail(nullptr, GWTF_ERR_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    if (!shape) return fail(nullptr, GWTF_ERR_INVALID_ARG, "shape is NULL");
+    const int S = shape->num_stages, n = shape->nodes_per_stage, B = shape->max_batch;
+    if (S < 1 || n < 1 || B < 1) return fail(nullptr, GWTF_ERR_INVALID_ARG, "shape values must be >= 1");
+    if (n > 32767) return fail(nullptr, GWTF_ERR_INVALID_ARG, "nodes_per_stage must be <= 32767");
+    const int64_t SN = int64_t(S) * n, V = 2 * SN + 3;
+    if (V > (int64_t(1) << 30) / 4) return fail(nullptr, GWTF_ERR_INVALID_ARG, "shape too large");
+    int ndev = 0;
+    hipError_t e = hipGetDeviceCount(&ndev);
+    if (e != hipSuccess) return fail(nullptr, GWTF_ERR_DEVICE, std::string("hipGetDeviceCount: ") + hipGetErrorString(e));
+    if (shape->device < 0 || shape->device >= ndev) return fail(nullptr, GWTF_ERR_INVALID_ARG, "bad device ordinal");
+    if ((e = hipSetDevice(shape->device)) != hipSuccess)
+        return fail(nullptr, GWTF_ERR_DEVICE, std::string("hipSetDevice: ") + hipGetErrorString(e));
+
+    gwtf_mcf_t *h = new (std::nothrow) gwtf_mcf_t();
+    if (!h) return fail(nullptr, GWTF_ERR_OUT_OF_MEMORY, "host allocation failed");
+    h->shape = *shape;
+    h->stream = static_cast<hipStream_t>(hip_stream);
+    int lds = 0;
+    if ((e = hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerBlock, shape->device)) != hipSuccess) {
+        g_create_err = std::string("hipDeviceGetAttribute: ") + hipGetErrorString(e);
+        delete h;
+        return GWTF_ERR_DEVICE;
+    }
+    h->lds_max = size_t(lds);
+    // Raising the per-kernel dynamic-LDS ceiling is not needed on every
+    // runtime (some reject the attribute); failure is harmless, but its error
+    // must not linger where a later launch check would read it.
+    if (set_lds_limits(h->lds_max) != hipSuccess) (void)hipGetLastError();
+
+    // Fallback state sized for the worst case: every exit vertex may need
+    // min(cap, n, supply) <= n flow-list entries.
+    h->fallback_slots = int64_t(std::max(S - 1, 0)) * n * n;
+    h->state_stride = align16(make_layout(S, n, h->fallback_slots, false).total);
+    const size_t na = size_t(std::max(S - 1, 0)) * n * n;
+    struct {
+        void **p;
+        size_t bytes;
+    } allocs[] = {
+        {(void **)&h->route, sizeof(int32_t) * B},
+        {(void **)&h->node_flow, sizeof(int32_t) * SN * B},
+        {(void **)&h->arc_flow, sizeof(int32_t) * std::max<size_t>(na, 1) * B},
+        {(void **)&h->pot, sizeof(int32_t) * V * B},
+        {(void **)&h->stats, sizeof(int64_t) * 4 * B},
+        {(void **)&h->state, h->state_stride * B},
+    };
+    for (auto &a : allocs) {
+        if ((e = hipMalloc(a.p, a.bytes)) != hipSuccess) {
+            g_create_err = std::string("hipMalloc workspace: ") + hipGetErrorString(e);
+            free_ws(h);
+            delete h;
+            return GWTF_ERR_OUT_OF_MEMORY;
+        }
+    }
+    *out = h;
+    return GWTF_OK;
+}
+
+extern "C" gwtf_status_t gwtf_mcf_solve_batch(gwtf_mcf_t *h, const gwtf_mcf_batch_t *b)
+{
+    if (!h) return fail(nullptr, GWTF_ERR_INVALID_ARG, "handle is NULL");
+    if (!b) return fail(h, GWTF_ERR_INVALID_ARG, "batch is NULL");
+    const int S = h->shape.num_stages, n = h->shape.nodes_per_stage;
+    if (b->batch < 1 || b->batch > h->shape.max_batch)
+        return fail(h, GWTF_ERR_INVALID_ARG, "batch outside [1, max_batch]");
+    if (!b->node_cap || !b->node_cost || !b->supply || !b->flow_value || !b->total_cost || !b->status)
+        return fail(h, GWTF_ERR_INVALID_ARG, "required pointer is NULL");
+    if ((S > 1) != (b->arc_cost != nullptr))
+        return fail(h, GWTF_ERR_INVALID_ARG, "arc_cost must be non-NULL exactly when S > 1");
+    hipError_t e = hipSetDevice(h->shape.device);
+    if (e != hipSuccess) return hip_fail(h, e, "hipSetDevice");
+
+    SolveParams p{};
+    p.B = b->batch;
+    p.S = S;
+    p.n = n;
+    p.cap = b->node_cap;
+    p.ncost = b->node_cost;
+    p.acost = b->arc_cost;
+    p.src = b->src_cost;
+    p.snk = b->snk_cost;
+    p.supply = b->supply;
+    p.F_out = b->flow_value;
+    p.cost_out = b->total_cost;
+    p.status_out = b->status;
+    p.route = h->route;
+    p.node_flow = h->node_flow;
+    p.arc_flow = h->arc_flow;
+    p.pot = h->pot;
+    p.stats = h->stats;
+    p.state = h->state;
+    p.state_stride = h->state_stride;
+
+    h->solved = 0;
+    const int waves = lds_waves(n);
+    const int64_t slots = lds_slots(S, n, waves, h->lds_max);
+    bool need_fallback = true;
+    if (slots > 0) {
+        p.list_slots = slots;
+        p.route_all = 0;
+        size_t lds = make_layout(S, n, slots, true).total + scratch_bytes(waves, n);
+        if ((e = launch_lds_pass(p, waves, lds, h->stream)) != hipSuccess) return hip_fail(h, e, "LDS solver launch");
+        // Worst-case list demand of an instance: (S-1) * n * min(n, cap, supply).
+        need_fallback = slots < int64_t(std::max(S - 1, 0)) * n * n;
+    } else {
+        p.route_all = 1;
+    }
+    if (need_fallback) {
+        p.list_slots = h->fallback_slots;
+        size_t lds = scratch_bytes(fallback_waves(), n);
+        if (lds > h->lds_max) return fail(h, GWTF_ERR_INVALID_ARG, "nodes_per_stage too large for LDS scratch");
+        if ((e = launch_fallback_pass(p, lds, h->stream)) != hipSuccess)
+            return hip_fail(h, e, "fallback solver launch");
+    }
+    h->solved = b->batch;
+    h->err.clear();
+    return GWTF_OK;
+}
+
+extern "C" gwtf_status_t gwtf_mcf_get_flows(gwtf_mcf_t *h, int32_t first, int32_t count, int32_t *node_flow,
+                                            int32_t *arc_flow, int32_t *src_flow, int32_t *snk_flow,
+                                            int32_t *potential)
+{
+    if (!h) return fail(nullptr, GWTF_ERR_INVALID_ARG, "handle is NULL");
+    if (h->solved == 0) return fail(h, GWTF_ERR_NOT_SOLVED, "no successful solve on this handle");
+    if (first < 0 || count < 0 || int64_t(first) + count > h->solved)
+        return fail(h, GWTF_ERR_RANGE, "instance range outside the last solved batch");
+    if (count == 0) return GWTF_OK;
+    hipError_t e = hipSetDevice(h->shape.device);
+    if (e != hipSuccess) return hip_fail(h, e, "hipSetDevice");
+    const int S = h->shape.num_stages, n = h->shape.nodes_per_stage;
+    const size_t SN = size_t(S) * n, V = 2 * SN + 3, na = size_t(std::max(S - 1, 0)) * n * n;
+    auto copy = [&](void *dst, const void *src, size_t bytes) -> hipError_t {
+        if (!dst || bytes == 0) return hipSuccess;
+        return hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, h->stream);
+    };
+    if ((e = copy(node_flow, h->node_flow + size_t(first) * SN, sizeof(int32_t) * SN * count)) != hipSuccess)
+        return hip_fail(h, e, "copy node_flow");
+    if ((e = copy(arc_flow, h->arc_flow + size_t(first) * na, sizeof(int32_t) * na * count)) != hipSuccess)
+        return hip_fail(h, e, "copy arc_flow");
+    if ((e = copy(potential, h->pot + size_t(first) * V, sizeof(int32_t) * V * count)) != hipSuccess)
+        return hip_fail(h, e, "copy potential");
+    if (src_flow || snk_flow) {
+        if ((e = launch_export(h->node_flow, S, n, first, count, src_flow, snk_flow, h->stream)) != hipSuccess)
+            return hip_fail(h, e, "export launch");
+    }
+    return GWTF_OK;
+}
+
+extern "C" gwtf_status_t gwtf_mcf_get_stats(gwtf_mcf_t *h, int32_t first, int32_t count, int64_t *stats)
+{
+    if (!h) return fail(nullptr, GWTF_ERR_INVALID_ARG, "handle is NULL");
+    if (!stats) return fail(h, GWTF_ERR_INVALID_ARG, "stats is NULL");
+    if (h->solved == 0) return fail(h, GWTF_ERR_NOT_SOLVED, "no successful solve on this handle");
+    if (first < 0 || count < 0 || int64_t(first) + count > h->solved)
+        return fail(h, GWTF_ERR_RANGE, "instance range outside the last solved batch");
+    if (count == 0) return GWTF_OK;
+    hipError_t e = hipSetDevice(h->shape.device);
+    if (e != hipSuccess) return hip_fail(h, e, "hipSetDevice");
+    e = hipMemcpyAsync(stats, h->stats + size_t(first) * 4, sizeof(int64_t) * 4 * count, hipMemcpyDeviceToDevice,
+                       h->stream);
+    if (e != hipSuccess) return hip_fail(h, e, "copy stats");
+    return GWTF_OK;
+}
+
+extern "C" void gwtf_mcf_destroy(gwtf_mcf_t *h)
+{
+    if (!h) return;
+    if (hipSetDevice(h->shape.device) == hipSuccess) (void)hipStreamSynchronize(h->stream);
+    free_ws(h);
+    delete h;
+}
+
+extern "C" const char *gwtf_mcf_last_error(const gwtf_mcf_t *h)
+{
+    return h ? h->err.c_str() : g_create_err.c_str();
+}

@@ -1,0 +1,87 @@
+// Internal interface between the host API (mcf_api.hip) and the solver
+// kernels (mcf_solver.hip).  Not part of the public C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace gwtf {
+
+// Sentinel label for "not reached"; every finite label stays below 2^29 in
+// magnitude (the per-instance overflow check guarantees it), so sums of a
+// finite label and a cost never reach kInf.
+constexpr int32_t kInf = 0x3fffffff;
+constexpr int64_t kLabelBound = int64_t(1) << 29;
+
+// Route codes in the workspace: which solver pass finished an instance.
+enum : int32_t { kRouteDone = 0, kRouteFallback = 1, kRouteFallbackDone = 2 };
+
+// Kernel arguments shared by both solver passes.
+struct SolveParams {
+    int32_t B, S, n;
+    const int32_t *cap, *ncost, *acost, *src, *snk, *supply; // caller inputs
+    int64_t *F_out, *cost_out;                                 // caller outputs [B]
+    int32_t *status_out;                                       // [B]
+    int32_t *route;       // [B] kRoute*
+    int32_t *node_flow;   // [B][S][n]
+    int32_t *arc_flow;    // [B][S-1][n][n]
+    int32_t *pot;         // [B][2Sn+3]; entry potentials live here during the solve
+    int64_t *stats;       // [B][4]
+    unsigned char *state; // fallback pass: per-instance state, state_stride bytes each
+    size_t state_stride;
+    int64_t list_slots;   // flow-list capacity of one instance
+    int32_t route_all;    // fallback pass: solve every instance, ignoring route[]
+};
+
+// Byte offsets of the per-instance solver state.  The LDS-resident pass uses
+// narrow index types (n <= 64); the fallback pass keeps the state in global
+// memory with wider ones.
+struct StateLayout {
+    size_t din, dout, pout, flow, cap, cost, pend, srcc, snkc;
+    size_t prin, prout, loff, llen, lcost, lamt, lpart;
+    size_t total;
+};
+
+__host__ __device__ inline size_t align16(size_t x) { return (x + 15) & ~size_t(15); }
+
+__host__ __device__ inline StateLayout make_layout(int S, int n, int64_t slots, bool narrow)
+{
+    StateLayout L;
+    size_t SN = size_t(S) * n, nw = (size_t(n) + 63) / 64, o = 0;
+    auto take = [&](size_t bytes) { size_t at = o; o = align16(o + bytes); return at; };
+    L.din = take(4 * SN);
+    L.dout = take(4 * SN);
+    L.pout = take(4 * SN);
+    L.flow = take(4 * SN);
+    L.cap = take(4 * SN);
+    L.cost = take(4 * SN);
+    L.pend = take(8 * size_t(S) * nw);
+    L.srcc = take(4 * size_t(n));
+    L.snkc = take(4 * size_t(n));
+    L.prin = take((narrow ? 1 : 2) * SN);
+    L.prout = take((narrow ? 1 : 2) * SN);
+    L.loff = take((narrow ? 2 : 4) * SN);
+    L.llen = take((narrow ? 1 : 2) * SN);
+    L.lcost = take(4 * size_t(slots));
+    L.lamt = take(4 * size_t(slots));
+    L.lpart = take((narrow ? 1 : 2) * size_t(slots));
+    L.total = o;
+    return L;
+}
+
+// LDS needed besides the state: per-wave partial minima and a scan buffer.
+__host__ __device__ inline size_t scratch_bytes(int waves, int n)
+{
+    return align16(size_t(8) * waves * n) + align16(size_t(4) * waves * 64);
+}
+
+// Launchers (mcf_solver.hip).  Return the HIP launch status.
+hipError_t launch_lds_pass(const SolveParams &p, int waves, size_t lds_bytes, hipStream_t s);
+hipError_t launch_fallback_pass(const SolveParams &p, size_t lds_bytes, hipStream_t s);
+hipError_t launch_export(const int32_t *node_flow_ws, int32_t S, int32_t n, int32_t first, int32_t count,
+                         int32_t *src_flow, int32_t *snk_flow, hipStream_t s);
+int fallback_waves();
+hipError_t set_lds_limits(size_t max_bytes);
+
+} // namespace gwtf

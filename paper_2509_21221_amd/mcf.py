@@ -1,0 +1,224 @@
+"""Python binding of the C ABI in include/gwtf_mcf.h (ctypes; argument
+marshalling only -- every step of the solve runs in the HIP library).
+
+The functions carry the C names (``gwtf_mcf_create``, ``gwtf_mcf_solve_batch``,
+``gwtf_mcf_get_flows``, ``gwtf_mcf_get_stats``, ``gwtf_mcf_destroy``,
+``gwtf_mcf_last_error``); ``Solver`` wraps them for torch device tensors.
+PyTorch only provides device memory and the HIP stream.
+
+There is no fallback: if ``libgwtf_mcf.so`` is missing or cannot be loaded,
+every entry point raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libgwtf_mcf.so")
+
+GWTF_OK = 0
+GWTF_ERR_INVALID_ARG = 1
+GWTF_ERR_OUT_OF_MEMORY = 2
+GWTF_ERR_DEVICE = 3
+GWTF_ERR_NOT_SOLVED = 4
+GWTF_ERR_RANGE = 5
+GWTF_INST_OK = 0
+GWTF_INST_BAD_INPUT = 1
+GWTF_INST_OVERFLOW = 2
+GWTF_NO_ARC = -1
+
+STATUS_NAMES = {0: "GWTF_OK", 1: "GWTF_ERR_INVALID_ARG", 2: "GWTF_ERR_OUT_OF_MEMORY",
+                3: "GWTF_ERR_DEVICE", 4: "GWTF_ERR_NOT_SOLVED", 5: "GWTF_ERR_RANGE"}
+
+
+class gwtf_mcf_shape_t(ctypes.Structure):
+    _fields_ = [("num_stages", ctypes.c_int32), ("nodes_per_stage", ctypes.c_int32),
+                ("max_batch", ctypes.c_int32), ("device", ctypes.c_int32)]
+
+
+class gwtf_mcf_batch_t(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32),
+                ("node_cap", ctypes.c_void_p), ("node_cost", ctypes.c_void_p),
+                ("arc_cost", ctypes.c_void_p), ("src_cost", ctypes.c_void_p),
+                ("snk_cost", ctypes.c_void_p), ("supply", ctypes.c_void_p),
+                ("flow_value", ctypes.c_void_p), ("total_cost", ctypes.c_void_p),
+                ("status", ctypes.c_void_p)]
+
+
+class GwtfError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"{STATUS_NAMES.get(code, code)}: {msg}")
+        self.code = code
+
+
+_lib = None
+_lock = threading.Lock()
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libgwtf_mcf.so and declare its prototypes (raises if absent)."""
+    global _lib
+    with _lock:
+        if _lib is not None:
+            return _lib
+        if not os.path.exists(path):
+            raise RuntimeError(
+                f"{path} is missing: build the HIP library first "
+                "(python -m paper_2509_21221_amd.build_native or __graft_entry__.build())")
+        lib = ctypes.CDLL(path)
+        vp, i32, i64p = ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p
+        lib.gwtf_mcf_create.argtypes = [ctypes.POINTER(gwtf_mcf_shape_t), vp, ctypes.POINTER(vp)]
+        lib.gwtf_mcf_create.restype = ctypes.c_int
+        lib.gwtf_mcf_solve_batch.argtypes = [vp, ctypes.POINTER(gwtf_mcf_batch_t)]
+        lib.gwtf_mcf_solve_batch.restype = ctypes.c_int
+        lib.gwtf_mcf_get_flows.argtypes = [vp, i32, i32, vp, vp, vp, vp, vp]
+        lib.gwtf_mcf_get_flows.restype = ctypes.c_int
+        lib.gwtf_mcf_get_stats.argtypes = [vp, i32, i32, i64p]
+        lib.gwtf_mcf_get_stats.restype = ctypes.c_int
+        lib.gwtf_mcf_destroy.argtypes = [vp]
+        lib.gwtf_mcf_destroy.restype = None
+        lib.gwtf_mcf_last_error.argtypes = [vp]
+        lib.gwtf_mcf_last_error.restype = ctypes.c_char_p
+        _lib = lib
+        return lib
+
+
+def gwtf_mcf_last_error(handle=None) -> str:
+    return load_library().gwtf_mcf_last_error(handle).decode()
+
+
+def _check(code, handle=None):
+    if code != GWTF_OK:
+        raise GwtfError(code, gwtf_mcf_last_error(handle))
+
+
+def gwtf_mcf_create(num_stages: int, nodes_per_stage: int, max_batch: int, device: int = 0,
+                    hip_stream: int = 0):
+    """Returns an opaque handle (int) for solves of this shape on ``device``."""
+    lib = load_library()
+    shape = gwtf_mcf_shape_t(num_stages, nodes_per_stage, max_batch, device)
+    out = ctypes.c_void_p()
+    _check(lib.gwtf_mcf_create(ctypes.byref(shape), ctypes.c_void_p(hip_stream or None),
+                               ctypes.byref(out)))
+    return out.value
+
+
+def gwtf_mcf_solve_batch(handle, batch: int, node_cap: int, node_cost: int, arc_cost: int,
+                         src_cost: int, snk_cost: int, supply: int, flow_value: int,
+                         total_cost: int, status: int) -> None:
+    """All arguments after ``batch`` are device addresses (0 = NULL)."""
+    b = gwtf_mcf_batch_t(batch, node_cap or None, node_cost or None, arc_cost or None,
+                         src_cost or None, snk_cost or None, supply or None, flow_value or None,
+                         total_cost or None, status or None)
+    _check(load_library().gwtf_mcf_solve_batch(ctypes.c_void_p(handle), ctypes.byref(b)), handle)
+
+
+def gwtf_mcf_get_flows(handle, first: int, count: int, node_flow: int = 0, arc_flow: int = 0,
+                       src_flow: int = 0, snk_flow: int = 0, potential: int = 0) -> None:
+    _check(load_library().gwtf_mcf_get_flows(
+        ctypes.c_void_p(handle), first, count, node_flow or None, arc_flow or None,
+        src_flow or None, snk_flow or None, potential or None), handle)
+
+
+def gwtf_mcf_get_stats(handle, first: int, count: int, stats: int) -> None:
+    _check(load_library().gwtf_mcf_get_stats(ctypes.c_void_p(handle), first, count,
+                                             stats or None), handle)
+
+
+def gwtf_mcf_destroy(handle) -> None:
+    load_library().gwtf_mcf_destroy(ctypes.c_void_p(handle))
+
+
+class Solver:
+    """A solver handle bound to torch's current HIP stream on ``device``.
+
+    ``solve`` takes int32 device tensors in the canonical layout
+    ([B][S][n] caps and compute costs, [B][S-1][n][n] link delays or None
+    when S == 1, optional [B][n] data-node delays, [B] supply) and returns
+    int64 flow value, int64 cost and int32 status tensors on the device.
+    """
+
+    def __init__(self, num_stages: int, nodes_per_stage: int, max_batch: int, device: int = 0,
+                 stream=None):
+        import torch
+
+        self.torch = torch
+        self.S, self.n, self.max_batch, self.device = num_stages, nodes_per_stage, max_batch, device
+        self.stream = stream if stream is not None else torch.cuda.current_stream(device)
+        self.handle = gwtf_mcf_create(num_stages, nodes_per_stage, max_batch, device,
+                                      self.stream.cuda_stream)
+        self.last_batch = 0
+
+    def _arg(self, t, shape, name):
+        torch = self.torch
+        if t is None:
+            return 0
+        if not isinstance(t, torch.Tensor):
+            raise TypeError(f"{name}: expected a torch tensor")
+        if t.dtype != torch.int32 or not t.is_contiguous() or t.device.type != "cuda" \
+                or t.device.index != self.device:
+            raise ValueError(f"{name}: need a contiguous int32 tensor on cuda:{self.device}")
+        if tuple(t.shape) != tuple(shape):
+            raise ValueError(f"{name}: shape {tuple(t.shape)} != {tuple(shape)}")
+        return t.data_ptr()
+
+    def solve(self, node_cap, node_cost, arc_cost, supply, src_cost=None, snk_cost=None,
+              out=None):
+        torch = self.torch
+        S, n = self.S, self.n
+        B = int(supply.shape[0])
+        args = [self._arg(node_cap, (B, S, n), "node_cap"), self._arg(node_cost, (B, S, n), "node_cost"),
+                self._arg(arc_cost, (B, S - 1, n, n), "arc_cost") if S > 1 else 0,
+                self._arg(src_cost, (B, n), "src_cost"), self._arg(snk_cost, (B, n), "snk_cost"),
+                self._arg(supply, (B,), "supply")]
+        if S > 1 and arc_cost is None:
+            raise ValueError("arc_cost is required when S > 1")
+        dev = torch.device("cuda", self.device)
+        if out is None:
+            out = (torch.empty(B, dtype=torch.int64, device=dev),
+                   torch.empty(B, dtype=torch.int64, device=dev),
+                   torch.empty(B, dtype=torch.int32, device=dev))
+        F, cost, status = out
+        gwtf_mcf_solve_batch(self.handle, B, *args, F.data_ptr(), cost.data_ptr(), status.data_ptr())
+        self.last_batch = B
+        return F, cost, status
+
+    def flows(self, first: int = 0, count: int | None = None):
+        torch = self.torch
+        count = self.last_batch - first if count is None else count
+        S, n = self.S, self.n
+        dev = torch.device("cuda", self.device)
+        nf = torch.empty((count, S, n), dtype=torch.int32, device=dev)
+        af = torch.empty((count, max(S - 1, 0), n, n), dtype=torch.int32, device=dev)
+        sf = torch.empty((count, n), dtype=torch.int32, device=dev)
+        tf = torch.empty((count, n), dtype=torch.int32, device=dev)
+        pot = torch.empty((count, 2 * S * n + 3), dtype=torch.int32, device=dev)
+        gwtf_mcf_get_flows(self.handle, first, count, nf.data_ptr(), af.data_ptr() if S > 1 else 0,
+                           sf.data_ptr(), tf.data_ptr(), pot.data_ptr())
+        return {"node_flow": nf, "arc_flow": af, "src_flow": sf, "snk_flow": tf, "potential": pot}
+
+    def stats(self, first: int = 0, count: int | None = None):
+        torch = self.torch
+        count = self.last_batch - first if count is None else count
+        st = torch.empty((count, 4), dtype=torch.int64, device=torch.device("cuda", self.device))
+        gwtf_mcf_get_stats(self.handle, first, count, st.data_ptr())
+        return st
+
+    def close(self):
+        if self.handle:
+            gwtf_mcf_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()

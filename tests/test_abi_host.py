@@ -1,0 +1,73 @@
+"""Host-only checks of the C-ABI library: it loads without a GPU and exports
+every function include/gwtf_mcf.h declares (no compute call is made)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2509_21221_amd import mcf
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gwtf_mcf.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gwtf_mcf_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for required in ("gwtf_mcf_create", "gwtf_mcf_solve_batch", "gwtf_mcf_get_flows",
+                     "gwtf_mcf_destroy"):
+        assert required in names
+
+
+def test_library_exports_every_declared_symbol():
+    if not os.path.exists(mcf.LIB_PATH):
+        pytest.fail("libgwtf_mcf.so not built: run __graft_entry__.build()")
+    lib = ctypes.CDLL(mcf.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_binding_names_match_header():
+    for name in declared_functions():
+        assert callable(getattr(mcf, name)), name
+
+
+def test_header_constants_match_binding():
+    text = open(HEADER).read()
+    assert "GWTF_NO_ARC (-1)" in text and mcf.GWTF_NO_ARC == -1
+    for name, value in [("GWTF_OK", 0), ("GWTF_ERR_INVALID_ARG", 1), ("GWTF_ERR_OUT_OF_MEMORY", 2),
+                        ("GWTF_ERR_DEVICE", 3), ("GWTF_ERR_NOT_SOLVED", 4), ("GWTF_ERR_RANGE", 5),
+                        ("GWTF_INST_OK", 0), ("GWTF_INST_BAD_INPUT", 1), ("GWTF_INST_OVERFLOW", 2)]:
+        assert re.search(rf"\b{name}\s*=\s*{value}\b", text), name
+        assert getattr(mcf, name) == value
+
+
+def test_null_handle_calls_fail_cleanly():
+    """Calls that reject their arguments before touching a device."""
+    lib = mcf.load_library()
+    assert lib.gwtf_mcf_solve_batch(None, None) == mcf.GWTF_ERR_INVALID_ARG
+    assert lib.gwtf_mcf_get_flows(None, 0, 1, None, None, None, None, None) == mcf.GWTF_ERR_INVALID_ARG
+    assert lib.gwtf_mcf_get_stats(None, 0, 1, None) == mcf.GWTF_ERR_INVALID_ARG
+    lib.gwtf_mcf_destroy(None)
+    out = ctypes.c_void_p(1)
+    assert lib.gwtf_mcf_create(None, None, ctypes.byref(out)) == mcf.GWTF_ERR_INVALID_ARG
+    assert out.value is None
+    assert "shape" in mcf.gwtf_mcf_last_error(None)
+    bad = mcf.gwtf_mcf_shape_t(0, 4, 1, 0)
+    assert lib.gwtf_mcf_create(ctypes.byref(bad), None, ctypes.byref(out)) == mcf.GWTF_ERR_INVALID_ARG
+
+
+def test_product_path_fails_loudly_without_library(tmp_path):
+    saved = mcf._lib
+    mcf._lib = None
+    try:
+        with pytest.raises(RuntimeError, match="missing"):
+            mcf.load_library(str(tmp_path / "nope.so"))
+    finally:
+        mcf._lib = saved

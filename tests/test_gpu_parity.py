@@ -1,0 +1,200 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+(F, cost) must match the oracle bit for bit on every instance; flows may
+differ where several are optimal, so every returned flow is checked for
+feasibility, maximality and the complementary-slackness certificate with the
+potentials the GPU returns.
+"""
+import hashlib
+import json
+import os
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2509_21221_amd import workloads as W
+import mcf_checks as C
+from gpu_util import gpu_solve
+
+pytestmark = pytest.mark.gpu
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def compare(batch, g, ref, certify=None):
+    assert (g["status"] == ref["status"]).all(), "status mismatch"
+    bad = np.flatnonzero((g["F"] != ref["F"]) | (g["cost"] != ref["cost"]))
+    assert bad.size == 0, (f"{bad.size} mismatches, first {bad[:5]}: gpu "
+                           f"{g['F'][bad[:5]]}/{g['cost'][bad[:5]]} oracle "
+                           f"{ref['F'][bad[:5]]}/{ref['cost'][bad[:5]]}")
+    idx = range(batch.B) if certify is None else certify
+    for b in idx:
+        if g["status"][b] != 0:
+            continue
+        C.certify(batch, b, int(g["F"][b]), int(g["cost"][b]), g["node_flow"][b], g["arc_flow"][b],
+                  g["src_flow"][b], g["snk_flow"][b], g["potential"][b])
+
+
+def test_paper_examples():
+    from test_oracle_pins import batch_from_json
+    for name in sorted(os.listdir(GOLDEN)):
+        if not (name.startswith("paper_") and name.endswith(".json")):
+            continue
+        batch, d = batch_from_json(os.path.join(GOLDEN, name))
+        say("example", name)
+        g = gpu_solve(batch)
+        assert g["status"][0] == 0 and g["F"][0] == d["expect_F"]
+        if "expect_cost" in d:
+            assert g["cost"][0] == d["expect_cost"]
+        compare(batch, g, oracle.solve(batch))
+
+
+def test_config1_full():
+    batch = W.config1()
+    say("c1", batch.B)
+    compare(batch, gpu_solve(batch), oracle.solve(batch, flows=False, potentials=False))
+
+
+@pytest.mark.parametrize("cfg", [2, 3])
+def test_config2_3_full(cfg):
+    batch = W.CONFIGS[cfg]()
+    say(f"c{cfg}", batch.B)
+    g = gpu_solve(batch)
+    ref = oracle.solve(batch, flows=False, potentials=False)
+    compare(batch, g, ref, certify=range(0, batch.B, 16))
+
+
+def _digest(batch):
+    h = hashlib.sha256()
+    for key in ("node_cap", "node_cost", "arc_cost", "src_cost", "snk_cost", "supply"):
+        h.update(getattr(batch, key).tobytes())
+    return h.hexdigest()
+
+
+def test_config4_full_against_stored_oracle():
+    gold = json.load(open(os.path.join(GOLDEN, "c4_oracle.json")))
+    batch = W.config4()
+    assert _digest(batch) == gold["input_sha256"], "generator no longer reproduces the stored inputs"
+    say("c4", batch.B)
+    g = gpu_solve(batch)
+    assert (g["status"] == 0).all()
+    assert (g["F"] == np.array(gold["F"])).all()
+    assert (g["cost"] == np.array(gold["cost"])).all()
+    for b in range(0, batch.B, 32):
+        C.certify(batch, b, int(g["F"][b]), int(g["cost"][b]), g["node_flow"][b], g["arc_flow"][b],
+                  g["src_flow"][b], g["snk_flow"][b], g["potential"][b])
+        assert g["F"][b] == C.closed_form_value(batch, b)
+
+
+def test_config4_sample_against_live_oracle():
+    batch = W.config4(8)
+    say("c4 sample", batch.B)
+    compare(batch, gpu_solve(batch), oracle.solve(batch))
+
+
+@pytest.mark.parametrize("S,n,holes,zero", [
+    (1, 1, 0.0, 0.0), (1, 9, 0.0, 0.3), (2, 3, 0.3, 0.1), (3, 5, 0.2, 0.2), (4, 4, 0.5, 0.0),
+    (6, 13, 0.1, 0.1), (9, 17, 0.0, 0.05), (5, 64, 0.05, 0.1), (12, 33, 0.2, 0.0), (40, 3, 0.0, 0.1),
+])
+def test_random_shapes(S, n, holes, zero):
+    batch = W.random_small(48, S, n, seed=7, cap_hi=5, cost_hi=90, supply_hi=3 * n + 4,
+                           holes=holes, zero_cap=zero)
+    say("random", S, n)
+    compare(batch, gpu_solve(batch), oracle.solve(batch))
+
+
+@pytest.mark.parametrize("S,n", [(3, 65), (4, 100), (2, 130)])
+def test_wide_stages_use_fallback(S, n):
+    batch = W.random_small(6, S, n, seed=3, cap_hi=4, cost_hi=300, supply_hi=2 * n, holes=0.1,
+                           zero_cap=0.1)
+    say("wide", S, n)
+    compare(batch, gpu_solve(batch), oracle.solve(batch))
+
+
+def test_lists_outgrow_lds_use_fallback():
+    """Capacities of 64 make every exit vertex reserve 64 flow-list slots,
+    more than LDS holds at this shape, so the global-memory pass runs."""
+    batch = W.config4(3)
+    batch.node_cap[:] = 64
+    batch.supply[:] = 150
+    say("fallback c4-shape")
+    g = gpu_solve(batch, stats=True)
+    compare(batch, g, oracle.solve(batch))
+
+
+def test_paper_flow_test_shapes():
+    for setting in (1, 2, 3, 4):
+        batch = W.paper_flow_test(setting, B=32)
+        say("paper setting", setting)
+        compare(batch, gpu_solve(batch), oracle.solve(batch))
+
+
+def test_edge_cases():
+    batch = W.config1(8)
+    batch.supply[0] = 0
+    batch.node_cap[1, 2] = 0              # stage 2 deleted -> F = 0
+    batch.node_cap[2] = 0                 # everything deleted
+    batch.supply[3] = 1
+    batch.supply[4] = 2_000_000_000       # huge supply: stage capacity binds
+    batch.node_cost[5] = 0
+    batch.arc_cost[5] = 0                 # all-zero costs: ties everywhere
+    g = gpu_solve(batch)
+    compare(batch, g, oracle.solve(batch))
+    assert g["F"][0] == 0 and g["F"][1] == 0 and g["F"][2] == 0
+
+
+def test_bad_input_and_overflow_status():
+    batch = W.config1(6)
+    batch.node_cap[0, 0, 0] = -1
+    batch.arc_cost[1, 0, 0, 0] = -2
+    batch.supply[2] = -5
+    batch.src_cost[3, 0] = -1
+    batch.node_cost[4, 1, 1] = 2 ** 28    # (2Sn+3) * max cost >= 2^29
+    g = gpu_solve(batch)
+    assert g["status"].tolist() == [1, 1, 1, 1, 2, 0]
+    assert (g["F"][:5] == 0).all() and (g["cost"][:5] == 0).all()
+    ref = oracle.solve(batch.subset([5]))
+    assert g["F"][5] == ref["F"][0] and g["cost"][5] == ref["cost"][0]
+
+
+def test_deterministic_flows():
+    batch = W.config2(512)
+    a = gpu_solve(batch)
+    b = gpu_solve(batch)
+    for key in ("F", "cost", "node_flow", "arc_flow", "potential"):
+        assert (a[key] == b[key]).all(), key
+
+
+def test_api_errors():
+    import torch
+    from paper_2509_21221_amd import mcf
+
+    s = mcf.Solver(4, 4, 8)
+    with pytest.raises(mcf.GwtfError) as e:
+        s.flows(0, 1)
+    assert e.value.code == mcf.GWTF_ERR_NOT_SOLVED
+    batch = W.config1(4)
+    gpu_solve(batch, flows=False, solver=s)
+    with pytest.raises(mcf.GwtfError) as e:
+        s.flows(2, 3)
+    assert e.value.code == mcf.GWTF_ERR_RANGE
+    dev = torch.device("cuda", 0)
+    z = lambda *shape: torch.zeros(shape, dtype=torch.int32, device=dev)
+    out = [torch.zeros(9, dtype=torch.int64, device=dev)] * 2 + [z(9)]
+    with pytest.raises(mcf.GwtfError) as e:
+        mcf.gwtf_mcf_solve_batch(s.handle, 9, z(9, 4, 4).data_ptr(), z(9, 4, 4).data_ptr(),
+                                 z(9, 3, 4, 4).data_ptr(), 0, 0, z(9).data_ptr(), out[0].data_ptr(),
+                                 out[1].data_ptr(), out[2].data_ptr())
+    assert e.value.code == mcf.GWTF_ERR_INVALID_ARG
+    with pytest.raises(mcf.GwtfError) as e:
+        mcf.gwtf_mcf_solve_batch(s.handle, 2, z(2, 4, 4).data_ptr(), z(2, 4, 4).data_ptr(), 0, 0, 0,
+                                 z(2).data_ptr(), out[0].data_ptr(), out[1].data_ptr(),
+                                 out[2].data_ptr())
+    assert e.value.code == mcf.GWTF_ERR_INVALID_ARG
+    s.close()

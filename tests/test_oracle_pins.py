@@ -31,7 +31,7 @@ def certify_all(batch, r):
                   r["src_flow"][b], r["snk_flow"][b], r["potential"][b])
 
 
-@pytest.mark.parametrize("path", sorted(glob.glob(os.path.join(GOLDEN, "*.json"))),
+@pytest.mark.parametrize("path", sorted(glob.glob(os.path.join(GOLDEN, "paper_*.json"))),
                          ids=lambda p: os.path.basename(p))
 def test_paper_worked_examples(path):
     batch, d = batch_from_json(path)
@@ -45,7 +45,7 @@ def test_paper_worked_examples(path):
 
 def test_request_change_is_sum_not_bottleneck():
     """Eq. 2 (sum) keeps 3 + 8 = 11; the max-objective swap would cost 12."""
-    batch, _ = batch_from_json(os.path.join(GOLDEN, "request_change.json"))
+    batch, _ = batch_from_json(os.path.join(GOLDEN, "paper_request_change.json"))
     r = oracle.solve(batch)
     assert (r["F"][0], r["cost"][0]) == (2, 11)
     # the optimal flow keeps links 1->2 and 3->4
