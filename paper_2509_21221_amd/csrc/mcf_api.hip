@@ -18,6 +18,7 @@ struct gwtf_mcf {
     hipStream_t stream;
     std::string err;
     size_t lds_max;
+    int clock_khz = 0;
     // workspace
     int32_t *route = nullptr, *node_flow = nullptr, *arc_flow = nullptr, *pot = nullptr;
     int64_t *stats = nullptr;
@@ -101,6 +102,8 @@ extern "C" gwtf_status_t gwtf_mcf_create(const gwtf_mcf_shape_t *shape, void *hi
         return GWTF_ERR_DEVICE;
     }
     h->lds_max = size_t(lds);
+    if (hipDeviceGetAttribute(&h->clock_khz, hipDeviceAttributeWallClockRate, shape->device) != hipSuccess)
+        h->clock_khz = 0;
     // Raising the per-kernel dynamic-LDS ceiling is not needed on every
     // runtime (some reject the attribute); failure is harmless, but its error
     // must not linger where a later launch check would read it.
@@ -119,7 +122,7 @@ extern "C" gwtf_status_t gwtf_mcf_create(const gwtf_mcf_shape_t *shape, void *hi
         {(void **)&h->node_flow, sizeof(int32_t) * SN * B},
         {(void **)&h->arc_flow, sizeof(int32_t) * std::max<size_t>(na, 1) * B},
         {(void **)&h->pot, sizeof(int32_t) * V * B},
-        {(void **)&h->stats, sizeof(int64_t) * 4 * B},
+        {(void **)&h->stats, sizeof(int64_t) * kStatsPerInstance * B},
         {(void **)&h->state, h->state_stride * B},
     };
     for (auto &a : allocs) {
@@ -168,6 +171,7 @@ extern "C" gwtf_status_t gwtf_mcf_solve_batch(gwtf_mcf_t *h, const gwtf_mcf_batc
     p.stats = h->stats;
     p.state = h->state;
     p.state_stride = h->state_stride;
+    p.clock_khz = h->clock_khz;
 
     h->solved = 0;
     const int waves = lds_waves(n);
@@ -235,8 +239,8 @@ extern "C" gwtf_status_t gwtf_mcf_get_stats(gwtf_mcf_t *h, int32_t first, int32_
     if (count == 0) return GWTF_OK;
     hipError_t e = hipSetDevice(h->shape.device);
     if (e != hipSuccess) return hip_fail(h, e, "hipSetDevice");
-    e = hipMemcpyAsync(stats, h->stats + size_t(first) * 4, sizeof(int64_t) * 4 * count, hipMemcpyDeviceToDevice,
-                       h->stream);
+    e = hipMemcpyAsync(stats, h->stats + size_t(first) * kStatsPerInstance,
+                       sizeof(int64_t) * kStatsPerInstance * count, hipMemcpyDeviceToDevice, h->stream);
     if (e != hipSuccess) return hip_fail(h, e, "copy stats");
     return GWTF_OK;
 }

@@ -27,12 +27,19 @@ struct SolveParams {
     int32_t *node_flow;   // [B][S][n]
     int32_t *arc_flow;    // [B][S-1][n][n]
     int32_t *pot;         // [B][2Sn+3]; entry potentials live here during the solve
-    int64_t *stats;       // [B][4]
+    int64_t *stats;       // [B][kStatsPerInstance]
     unsigned char *state; // fallback pass: per-instance state, state_stride bytes each
     size_t state_stride;
     int64_t list_slots;   // flow-list capacity of one instance
     int32_t route_all;    // fallback pass: solve every instance, ignoring route[]
+    int32_t clock_khz;    // device wall-clock rate, for the phase timers
 };
+
+// Per-instance counters written to SolveParams::stats: augmentations,
+// label-correcting rounds, dense cost rows relaxed, flow-list relaxations,
+// then nanoseconds spent in forward sweeps, backward sweeps, augmentation
+// with the potential update, and the remainder (label reset, sink update).
+constexpr int kStatsPerInstance = 8;
 
 // Byte offsets of the per-instance solver state.  The LDS-resident pass uses
 // narrow index types (n <= 64); the fallback pass keeps the state in global

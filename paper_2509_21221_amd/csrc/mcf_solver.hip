@@ -102,6 +102,13 @@ struct Shared {
     long long slots;
 };
 
+__device__ __forceinline__ uint64_t lap(uint64_t &tick)
+{
+    uint64_t now = wall_clock64(), d = now - tick;
+    tick = now;
+    return d;
+}
+
 __device__ __forceinline__ void wave_sync()
 {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -357,10 +364,14 @@ __global__ __launch_bounds__(WAVES * 64) void solve_kernel(SolveParams p)
 
     const uint64_t myrows = wave_rows<WAVES>(wave);
     long long my_rows = 0, my_pulls = 0;
+    // Phase clocks (thread 0, wall-clock ticks): forward sweeps, backward
+    // sweeps, augmentation + potentials, and the rest (label reset, sink).
+    uint64_t tick = 0, clk_fwd = 0, clk_bwd = 0, clk_aug = 0, clk_other = 0;
 
     // ---- successive shortest paths ----
     if (sh.status == 0) {
         while (sh.F < supply) {
+            if (tid == 0) tick = wall_clock64();
             for (int q = tid; q < SN; q += NT) {
                 st.din[q] = kInf;
                 st.dout[q] = kInf;
@@ -383,6 +394,7 @@ __global__ __launch_bounds__(WAVES * 64) void solve_kernel(SolveParams p)
             int round_count = 0;
             for (;;) {
                 // -------- forward sweep --------
+                if (tid == 0) clk_other += lap(tick);
                 for (int k = 0; k < S; ++k) {
                     if (k > 0) {
                         bool has = false;
@@ -494,6 +506,7 @@ __global__ __launch_bounds__(WAVES * 64) void solve_kernel(SolveParams p)
                     }
                 }
                 // -------- sink --------
+                if (tid == 0) clk_fwd += lap(tick);
                 if (tid == 0) sh.tbest = ~0ull;
                 __syncthreads();
                 for (int j = tid; j < n; j += NT) {
@@ -522,6 +535,7 @@ __global__ __launch_bounds__(WAVES * 64) void solve_kernel(SolveParams p)
                 __syncthreads();
 
                 // -------- backward sweep --------
+                if (tid == 0) clk_other += lap(tick);
                 auto back_node = [&](int k, int i, long long &pulls) {
                     int q = k * n + i;
                     bool chg = false;
@@ -585,7 +599,10 @@ __global__ __launch_bounds__(WAVES * 64) void solve_kernel(SolveParams p)
                     if (lane == 0 && anyc) atomicOr(&sh.any, 1);
                 }
                 __syncthreads();
-                if (tid == 0) sh.rounds++;
+                if (tid == 0) {
+                    sh.rounds++;
+                    clk_bwd += lap(tick);
+                }
                 first = false;
                 if (!sh.any) break;
                 // Bellman-Ford settles within |V| passes when the residual
@@ -618,7 +635,10 @@ __global__ __launch_bounds__(WAVES * 64) void solve_kernel(SolveParams p)
                 *pi = min(st.din[q], *pi + dred);
             }
             __syncthreads();
-            if (tid == 0) sh.pit = sh.Dt;
+            if (tid == 0) {
+                sh.pit = sh.Dt;
+                clk_aug += lap(tick);
+            }
             __syncthreads();
             if (sh.status != 0) break;
         }
@@ -652,11 +672,16 @@ __global__ __launch_bounds__(WAVES * 64) void solve_kernel(SolveParams p)
         p.F_out[b] = ok ? sh.F : 0;
         p.cost_out[b] = ok ? sh.cost : 0;
         p.status_out[b] = sh.status;
-        int64_t *s = p.stats + size_t(b) * 4;
+        int64_t *s = p.stats + size_t(b) * kStatsPerInstance;
         s[0] = sh.augs;
         s[1] = sh.rounds;
         s[2] = sh.rows;
         s[3] = sh.pulls;
+        const double ns_per_tick = 1e6 / double(p.clock_khz > 0 ? p.clock_khz : 100000);
+        s[4] = int64_t(double(clk_fwd) * ns_per_tick);
+        s[5] = int64_t(double(clk_bwd) * ns_per_tick);
+        s[6] = int64_t(double(clk_aug) * ns_per_tick);
+        s[7] = int64_t(double(clk_other) * ns_per_tick);
     }
 }
 

@@ -28,6 +28,7 @@ GWTF_INST_OK = 0
 GWTF_INST_BAD_INPUT = 1
 GWTF_INST_OVERFLOW = 2
 GWTF_NO_ARC = -1
+STATS_PER_INSTANCE = 8
 
 STATUS_NAMES = {0: "GWTF_OK", 1: "GWTF_ERR_INVALID_ARG", 2: "GWTF_ERR_OUT_OF_MEMORY",
                 3: "GWTF_ERR_DEVICE", 4: "GWTF_ERR_NOT_SOLVED", 5: "GWTF_ERR_RANGE"}
@@ -202,7 +203,7 @@ class Solver:
     def stats(self, first: int = 0, count: int | None = None):
         torch = self.torch
         count = self.last_batch - first if count is None else count
-        st = torch.empty((count, 4), dtype=torch.int64, device=torch.device("cuda", self.device))
+        st = torch.empty((count, STATS_PER_INSTANCE), dtype=torch.int64, device=torch.device("cuda", self.device))
         gwtf_mcf_get_stats(self.handle, first, count, st.data_ptr())
         return st
 
