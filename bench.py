@@ -135,6 +135,9 @@ def main():
         "rounds_per_augmentation": float(stats[:, 1].sum() / max(1, stats[:, 0].sum())),
         "phase_ms_per_instance": {name: float(stats[:, col].mean()) / 1e6 for name, col in
                                   (("forward", 4), ("backward", 5), ("augment", 6), ("other", 7))},
+        "layer_steps_per_augmentation": {
+            "forward": float(stats[:, 8].sum() / max(1, stats[:, 0].sum())),
+            "backward": float(stats[:, 9].sum() / max(1, stats[:, 0].sum()))},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": None,
                      "kernel": "solve_kernel (one launch per step)",

@@ -103,11 +103,12 @@ gwtf_status_t gwtf_mcf_get_flows(gwtf_mcf_t *h, int32_t first, int32_t count,
                                  int32_t *src_flow, int32_t *snk_flow, int32_t *potential);
 
 /* Per-instance work counters of the last solve, into a caller device buffer
- * stats[count][8] (int64): augmenting paths, label-correcting rounds, cost
- * rows streamed in the dense relaxation (each row is n arc relaxations),
- * flow-list (reverse-arc) relaxations, then the nanoseconds the instance's
+ * stats[count][10] (int64): augmenting paths, label-correcting rounds, cost
+ * rows relaxed in the dense relaxation (each row is n arc relaxations),
+ * flow-list (reverse-arc) relaxations, the nanoseconds the instance's
  * workgroup spent in forward sweeps, backward sweeps, augmentation with the
- * potential update, and the rest (label reset, sink update). */
+ * potential update, and the rest (label reset, sink update), then the
+ * executed forward and backward layer steps (0 where not tracked). */
 gwtf_status_t gwtf_mcf_get_stats(gwtf_mcf_t *h, int32_t first, int32_t count, int64_t *stats);
 
 /* Frees the handle and its workspace after draining its stream; NULL-safe. */

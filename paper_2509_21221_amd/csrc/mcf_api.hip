@@ -59,6 +59,19 @@ int64_t lds_slots(int S, int n, int waves, size_t lds_max)
 
 int lds_waves(int n) { return n <= 16 ? 1 : 4; }
 
+// Flow-list capacity left in LDS beside a narrow state layout and `extra`
+// bytes of other LDS use.
+int64_t lds_slots_with(int S, int n, size_t extra, size_t lds_max)
+{
+    if (n > 64) return 0;
+    size_t fixed = make_layout(S, n, 0, true).total + extra + 64;
+    if (fixed >= lds_max) return 0;
+    int64_t slots = int64_t((lds_max - fixed) / 9) - 16;
+    int64_t worst = int64_t(std::max(S - 1, 0)) * n * n;
+    slots = std::min<int64_t>(std::min<int64_t>(slots, worst), 65535);
+    return std::max<int64_t>(slots, 0);
+}
+
 void free_ws(gwtf_mcf_t *h)
 {
     (void)hipFree(h->route);
@@ -174,16 +187,27 @@ extern "C" gwtf_status_t gwtf_mcf_solve_batch(gwtf_mcf_t *h, const gwtf_mcf_batc
     p.clock_khz = h->clock_khz;
 
     h->solved = 0;
-    const int waves = lds_waves(n);
-    const int64_t slots = lds_slots(S, n, waves, h->lds_max);
+    const int64_t worst = int64_t(std::max(S - 1, 0)) * n * n;
     bool need_fallback = true;
-    if (slots > 0) {
+    const int64_t reg_slots = (n > 16 && reg_pass_fits(S, n))
+        ? lds_slots_with(S, n, reg_pass_scratch_bytes() + kRegStaticLds, h->lds_max) : 0;
+    const int waves = lds_waves(n);
+    const int64_t slots = reg_slots > 0 ? 0 : lds_slots(S, n, waves, h->lds_max);
+    if (reg_slots > 0) {
+        // Register-resident pass; instances whose link costs need more than
+        // 16 bits or whose flow lists outgrow LDS go to the fallback pass.
+        p.list_slots = reg_slots;
+        p.route_all = 0;
+        size_t lds = make_layout(S, n, reg_slots, true).total + reg_pass_scratch_bytes();
+        if ((e = launch_reg_pass(p, lds, h->stream)) != hipSuccess) return hip_fail(h, e, "register solver launch");
+        need_fallback = true;
+    } else if (slots > 0) {
         p.list_slots = slots;
         p.route_all = 0;
         size_t lds = make_layout(S, n, slots, true).total + scratch_bytes(waves, n);
         if ((e = launch_lds_pass(p, waves, lds, h->stream)) != hipSuccess) return hip_fail(h, e, "LDS solver launch");
         // Worst-case list demand of an instance: (S-1) * n * min(n, cap, supply).
-        need_fallback = slots < int64_t(std::max(S - 1, 0)) * n * n;
+        need_fallback = slots < worst;
     } else {
         p.route_all = 1;
     }

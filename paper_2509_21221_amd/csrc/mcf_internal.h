@@ -38,8 +38,9 @@ struct SolveParams {
 // Per-instance counters written to SolveParams::stats: augmentations,
 // label-correcting rounds, dense cost rows relaxed, flow-list relaxations,
 // then nanoseconds spent in forward sweeps, backward sweeps, augmentation
-// with the potential update, and the remainder (label reset, sink update).
-constexpr int kStatsPerInstance = 8;
+// with the potential update, and the remainder (label reset, sink update),
+// then executed forward and backward layer steps (register pass only).
+constexpr int kStatsPerInstance = 10;
 
 // Byte offsets of the per-instance solver state.  The LDS-resident pass uses
 // narrow index types (n <= 64); the fallback pass keeps the state in global
@@ -70,9 +71,12 @@ __host__ __device__ inline StateLayout make_layout(int S, int n, int64_t slots, 
     L.prout = take((narrow ? 1 : 2) * SN);
     L.loff = take((narrow ? 2 : 4) * SN);
     L.llen = take((narrow ? 1 : 2) * SN);
-    L.lcost = take(4 * size_t(slots));
-    L.lamt = take(4 * size_t(slots));
-    L.lpart = take((narrow ? 1 : 2) * size_t(slots));
+    // Lists carry 64 slots of slack so batched reads past the last list
+    // stay inside the allocation.
+    const size_t lslots = size_t(slots) + 64;
+    L.lcost = take(4 * lslots);
+    L.lamt = take(4 * lslots);
+    L.lpart = take((narrow ? 1 : 2) * lslots);
     L.total = o;
     return L;
 }
@@ -89,6 +93,12 @@ hipError_t launch_fallback_pass(const SolveParams &p, size_t lds_bytes, hipStrea
 hipError_t launch_export(const int32_t *node_flow_ws, int32_t S, int32_t n, int32_t first, int32_t count,
                          int32_t *src_flow, int32_t *snk_flow, hipStream_t s);
 int fallback_waves();
+// Register-resident pass (mcf_solver_reg.hip): S <= 32, n <= 64, link costs
+// below 65535; instances outside that route to the fallback pass.
+hipError_t launch_reg_pass(const SolveParams &p, size_t lds_bytes, hipStream_t s);
+size_t reg_pass_scratch_bytes();
+bool reg_pass_fits(int S, int n);
+constexpr size_t kRegStaticLds = 4096; // static LDS of the register-resident kernel (upper bound)
 hipError_t set_lds_limits(size_t max_bytes);
 
 } // namespace gwtf

@@ -28,7 +28,7 @@ GWTF_INST_OK = 0
 GWTF_INST_BAD_INPUT = 1
 GWTF_INST_OVERFLOW = 2
 GWTF_NO_ARC = -1
-STATS_PER_INSTANCE = 8
+STATS_PER_INSTANCE = 10
 
 STATUS_NAMES = {0: "GWTF_OK", 1: "GWTF_ERR_INVALID_ARG", 2: "GWTF_ERR_OUT_OF_MEMORY",
                 3: "GWTF_ERR_DEVICE", 4: "GWTF_ERR_NOT_SOLVED", 5: "GWTF_ERR_RANGE"}

@@ -198,3 +198,25 @@ def test_api_errors():
                                  out[2].data_ptr())
     assert e.value.code == mcf.GWTF_ERR_INVALID_ARG
     s.close()
+
+
+@pytest.mark.parametrize("S,n,holes,zero", [
+    (1, 40, 0.0, 0.1), (2, 20, 0.2, 0.0), (31, 50, 0.1, 0.05), (32, 64, 0.0, 0.0), (7, 64, 0.3, 0.2),
+])
+def test_register_pass_shapes(S, n, holes, zero):
+    """Shapes served by the register-resident pass (S <= 32, 16 < n <= 64)."""
+    batch = W.random_small(12, S, n, seed=19, cap_hi=6, cost_hi=250, supply_hi=4 * n,
+                           holes=holes, zero_cap=zero)
+    say("register pass", S, n)
+    compare(batch, gpu_solve(batch), oracle.solve(batch))
+
+
+def test_register_pass_routes_wide_costs():
+    """Link costs above 16 bits send an instance to the fallback pass; the
+    others in the same batch stay on the register pass."""
+    batch = W.config4(4)
+    batch.arc_cost[1, 3, 5, 7] = 70000
+    batch.arc_cost[2, 0, 0, :] = 65535
+    say("register pass routing")
+    g = gpu_solve(batch)
+    compare(batch, g, oracle.solve(batch))
