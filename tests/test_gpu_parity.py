@@ -220,3 +220,18 @@ def test_register_pass_routes_wide_costs():
     say("register pass routing")
     g = gpu_solve(batch)
     compare(batch, g, oracle.solve(batch))
+
+
+def test_config5_full_against_stored_oracle():
+    """The single 64 x 512 instance: (F, cost) equal to the stored oracle
+    optimum, the closed-form flow value, and the returned flow certified."""
+    gold = json.load(open(os.path.join(GOLDEN, "c5_oracle.json")))
+    batch = W.config5()
+    assert _digest(batch) == gold["input_sha256"], "generator no longer reproduces the stored inputs"
+    say("c5 (about a minute)")
+    g = gpu_solve(batch)
+    assert g["status"][0] == 0
+    assert int(g["F"][0]) == gold["F"][0] == C.closed_form_value(batch, 0)
+    assert int(g["cost"][0]) == gold["cost"][0]
+    C.certify(batch, 0, int(g["F"][0]), int(g["cost"][0]), g["node_flow"][0], g["arc_flow"][0],
+              g["src_flow"][0], g["snk_flow"][0], g["potential"][0])
