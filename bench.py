@@ -37,6 +37,31 @@ WORKLOADS = {
 }
 
 
+def measured_traffic(config: int, kernel_s: float):
+    """HBM bytes per launch from the committed rocprofv3 counter summary,
+    as GB/s over the measured launch time; None when the summary does not
+    cover this workload or the kernel sources changed since it was taken."""
+    import glob
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", "solve_reg_kernel_c4_traffic.json")
+    if config != 4 or not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    h = hashlib.sha256()
+    for f in rec["sources"]:
+        full = os.path.join(ROOT, f)
+        if not os.path.exists(full):
+            return None
+        h.update(open(full, "rb").read())
+    now = sorted(glob.glob(os.path.join(ROOT, "paper_2509_21221_amd", "csrc", "*.hip")) +
+                 glob.glob(os.path.join(ROOT, "paper_2509_21221_amd", "csrc", "*.h")))
+    if h.hexdigest() != rec["kernel_sources_sha256"] or \
+            sorted(os.path.relpath(f, ROOT) for f in now) != sorted(f for f in rec["sources"] if "csrc" in f):
+        return None
+    return rec["traffic_bytes_per_launch"] / kernel_s / 1e9
+
+
 def cpu_baseline(batch, budget_s: float, threads: int):
     """The oracle on the host cores, on a bounded prefix of the workload."""
     import numpy as np
@@ -68,7 +93,20 @@ def main():
     ap.add_argument("--config", type=int, default=4, choices=sorted(WORKLOADS))
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle time for the CPU baseline (0 = skip)")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only run one device-to-device copy of MIB MiB (counter calibration)")
     args = ap.parse_args()
+    if args.calibrate_copy:
+        import torch
+
+        nbytes = args.calibrate_copy << 20
+        src = torch.ones(nbytes // 4, dtype=torch.int32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": nbytes, "copy_bytes_written": nbytes}), flush=True)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: this solver has no multi-GPU path "
               f"(--gpus {args.gpus} requested)", file=sys.stderr)
@@ -139,7 +177,7 @@ def main():
             "forward": float(stats[:, 8].sum() / max(1, stats[:, 0].sum())),
             "backward": float(stats[:, 9].sum() / max(1, stats[:, 0].sum()))},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(args.config, kernel_s),
                      "kernel": "solve_kernel (one launch per step)",
                      "kernel_ms": kernel_s * 1e3},
     }
