@@ -46,25 +46,12 @@ constexpr int kPathMax = 512;
 enum : int { kArcSplitFwd = 0, kArcSplitRev = 1, kArcLinkFwd = 2, kArcLinkRev = 3 };
 
 
-// Register arrays must be indexed by constants to stay in registers; the
-// stage pair is uniform, so a switch turns it into a scalar jump.
-#define GWTF_LAYER_CASES(X)                                                                           \
-    X(0) X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(9) X(10) X(11) X(12) X(13) X(14) X(15) X(16) X(17)  \
-    X(18) X(19) X(20) X(21) X(22) X(23) X(24) X(25) X(26) X(27) X(28) X(29) X(30)
-static_assert(kRegMaxStages - 1 == 31, "layer cases cover 31 stage pairs");
-
-// The 31 stage pairs' costs are 31 named uint4 values (not an array, which
-// the compiler may demote to scratch memory once indexed at run time); these
-// macros declare them and map a uniform stage-pair index to one of them.
-#define GWTF_DECL(K) uint4 lay##K = make_uint4(0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu);
-#define GWTF_GET(K)                                                                                   \
-    case K:                                                                                           \
-        w = lay##K;                                                                                   \
-        break;
-#define GWTF_SET(K)                                                                                   \
-    case K:                                                                                           \
-        lay##K = w;                                                                                   \
-        break;
+// The link costs of stage pair k sit in element k of four 32-element vector
+// values (one per register word).  The pair index is wave-uniform, so
+// reading or writing element k lowers to indirect register addressing
+// rather than to memory or branches.
+typedef uint32_t u32x32 __attribute__((ext_vector_type(32)));
+static_assert(kRegMaxStages <= 32, "one vector element per stage pair");
 
 __device__ __forceinline__ uint64_t pack_key(int label, int idx)
 {
@@ -177,7 +164,9 @@ __global__ __launch_bounds__(kRegThreads) void solve_reg_kernel(SolveParams p)
     for (int q = tid; q < V; q += NT) gpot[q] = 0;
 
     // link costs -> registers (each link read exactly once by one thread)
-    GWTF_LAYER_CASES(GWTF_DECL)
+    u32x32 lw0, lw1, lw2, lw3;
+#pragma unroll
+    for (int e = 0; e < 32; ++e) lw0[e] = lw1[e] = lw2[e] = lw3[e] = 0xffffffffu;
     for (int k = 0; k < S - 1; ++k) {
         uint32_t wv[kWordsPerLayer];
 #pragma unroll
@@ -195,8 +184,10 @@ __global__ __launch_bounds__(kRegThreads) void solve_reg_kernel(SolveParams p)
                 wv[m] |= c16 << (16 * h);
             }
         }
-        const uint4 w = make_uint4(wv[0], wv[1], wv[2], wv[3]);
-        switch (k) { GWTF_LAYER_CASES(GWTF_SET) default: break; }
+        lw0[k] = wv[0];
+        lw1[k] = wv[1];
+        lw2[k] = wv[2];
+        lw3[k] = wv[3];
     }
     if (bad) atomicOr(&sh.bad, 1);
     atomicMax(&sh.maxc, max(mx, mxlink));
@@ -303,20 +294,39 @@ __global__ __launch_bounds__(kRegThreads) void solve_reg_kernel(SolveParams p)
                     const uint64_t mine = __ballot(live) & myrows;
                     int best = kInf, arg = -1;
                     if (mine) {
-                        uint4 w = make_uint4(0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu);
-                        switch (k - 1) { GWTF_LAYER_CASES(GWTF_GET) default: break; }
-                        const uint32_t wl[kWordsPerLayer] = {w.x, w.y, w.z, w.w};
+                        const int kk = __builtin_amdgcn_readfirstlane(k - 1);
+                        const uint32_t wl[kWordsPerLayer] = {lw0[kk], lw1[kk], lw2[kk], lw3[kk]};
+                        if (__popcll(mine) > 3) {
+                            // many live rows: all of this wave's rows, no branches
 #pragma unroll
-                        for (int r = 0; r < kRowsPerWave; ++r) {
-                            const int i = wave + kRegWaves * r;
-                            const int d = __builtin_amdgcn_readlane(rowlab, i);
-                            const uint32_t cw = wl[r / 2];
-                            const uint32_t c = (r & 1) ? (cw >> 16) : (cw & 0xffffu);
-                            int cand = d + int(c); // kInf + c stays below 2^31
-                            if (holes && c == kNoArc16) cand = kInf;
-                            const bool lt = cand < best;
-                            best = lt ? cand : best;
-                            arg = lt ? i : arg;
+                            for (int r = 0; r < kRowsPerWave; ++r) {
+                                const int i = wave + kRegWaves * r;
+                                const int d = __builtin_amdgcn_readlane(rowlab, i);
+                                const uint32_t cw = wl[r / 2];
+                                const uint32_t c = (r & 1) ? (cw >> 16) : (cw & 0xffffu);
+                                int cand = d + int(c); // kInf + c stays below 2^31
+                                if (holes && c == kNoArc16) cand = kInf;
+                                const bool lt = cand < best;
+                                best = lt ? cand : best;
+                                arg = lt ? i : arg;
+                            }
+                        } else {
+                            // few live rows: visit only those
+                            uint64_t mm = mine;
+                            while (mm) {
+                                const int i = __builtin_ctzll(mm);
+                                mm &= mm - 1;
+                                const int r = i >> 3;
+                                const int d = __builtin_amdgcn_readlane(rowlab, i);
+                                const uint32_t cw = (r >> 1) == 0 ? wl[0] : (r >> 1) == 1 ? wl[1]
+                                                  : (r >> 1) == 2 ? wl[2] : wl[3];
+                                const uint32_t c = (cw >> (16 * (r & 1))) & 0xffffu;
+                                int cand = d + int(c);
+                                if (holes && c == kNoArc16) cand = kInf;
+                                const bool lt = cand < best;
+                                best = lt ? cand : best;
+                                arg = lt ? i : arg;
+                            }
                         }
                         wave_rows += __popcll(mine);
                     }
@@ -410,9 +420,10 @@ __global__ __launch_bounds__(kRegThreads) void solve_reg_kernel(SolveParams p)
                             for (int u = 0; u < 8; ++u) dj[u] = __shfl(dnext, part[u]);
 #pragma unroll
                             for (int u = 0; u < 8; ++u) {
+                                // branch-free (bitwise & instead of &&); ties keep the
+                                // earlier list entry, deterministic for given inputs
                                 const int cand = dj[u] - lc[u];
-                                const bool take = e0 + u < len && dj[u] < kInf &&
-                                                  (cand < best || (cand == best && part[u] < arg));
+                                const bool take = (e0 + u < len) & (dj[u] < kInf) & (cand < best);
                                 best = take ? cand : best;
                                 arg = take ? part[u] : arg;
                             }
