@@ -275,16 +275,30 @@ __global__ __launch_bounds__(kRegThreads) void solve_reg_kernel(SolveParams p)
                     pend_prev = st.pend[0];
                 }
                 pprev = st.pout[lq];
-                for (int k = 1; k < S; ++k) {
-                    const int qs = k * n + lq;
+                // stages whose exits were seeded by the last backward sweep
+                const uint64_t seeded_stages = __ballot(lane > 0 && lane < S && st.pend[lane] != 0);
+                for (int k = 1; k < S;) {
                     if (pend_prev == 0) {
-                        // nothing reaches stage k in this sweep
-                        const int d = st.dout[qs];
+                        // Nothing reaches stage k, so its pending exits are the
+                        // seeded ones: jump to the next seeded stage m and
+                        // continue with step m + 1 (or stop).
+                        const uint64_t rest = seeded_stages & (~uint64_t(0) << k);
+                        if (rest == 0) break;
+                        const int m = __builtin_ctzll(rest);
+                        const int qm = m * n + lq;
+                        const int d = st.dout[qm];
                         dprev = jv ? d : kInf;
-                        pprev = st.pout[qs];
-                        pend_prev = st.pend[k];
+                        pprev = st.pout[qm];
+                        pend_prev = st.pend[m];
+                        k = m + 1;
                         continue;
                     }
+                    const int qs = k * n + lq;
+                    // stage-k state first: its LDS latency overlaps the relaxation
+                    int din_k = st.din[qs], dout_k = st.dout[qs];
+                    const int pout_k = st.pout[qs];
+                    const int fl = st.flow[qs], cp = st.cap[qs], nc = st.cost[qs];
+                    const uint64_t seeded = st.pend[k];
                     fwd_steps++;
                     // Row labels of stage k-1: kInf unless the exit is pending
                     // and below the pruning bound, so the row loop needs no
@@ -334,10 +348,6 @@ __global__ __launch_bounds__(kRegThreads) void solve_reg_kernel(SolveParams p)
                     if (jv && best < kInf)
                         atomicMin(reinterpret_cast<unsigned long long *>(buf + lane),
                                   (unsigned long long)pack_key(best, arg));
-                    int din_k = st.din[qs], dout_k = st.dout[qs];
-                    const int pout_k = st.pout[qs];
-                    const int fl = st.flow[qs], cp = st.cap[qs], nc = st.cost[qs];
-                    const uint64_t seeded = st.pend[k];
                     __syncthreads();
                     const uint64_t key = buf[lane];
                     const int v = key_label(key);
@@ -366,8 +376,10 @@ __global__ __launch_bounds__(kRegThreads) void solve_reg_kernel(SolveParams p)
                     pend_prev = seeded | m;
                     dprev = jv ? dout_k : kInf;
                     pprev = pout_k;
+                    ++k;
                 }
                 // ------------- sink (every wave, from registers) -------------
+                // (pend_prev refers to the last stage here, or is 0 after an early stop)
                 if (pend_prev) {
                     int cand = kInf;
                     if (jv && ((pend_prev >> lane) & 1) && dprev < kInf) cand = dprev + st.snkc[lq];
@@ -451,7 +463,10 @@ __global__ __launch_bounds__(kRegThreads) void solve_reg_kernel(SolveParams p)
                         if (__ballot(ichg)) in_dirty |= 1u << k;
                         dnext = jv ? din_k : kInf;
                         have = k;
-                        wave_sync();
+                        // LDS operations of one wave complete in issue order, so the
+                        // next step's cross-lane reads only need the compiler to
+                        // keep them after these writes.
+                        asm volatile("" ::: "memory");
                     }
                     if (lane == 0) sh.any = anyc;
                 }
