@@ -50,6 +50,14 @@ enum {
     GWTF_INST_OVERFLOW = 2   /* (2*S*n + 3) * max cost >= 2^29: labels could leave int32 */
 };
 
+/* Solver pass that produced an instance's result (gwtf_mcf_get_passes). */
+enum {
+    GWTF_PASS_REGISTER = 1, /* one workgroup, link costs in registers: 16 < n <= 64, S <= 32 */
+    GWTF_PASS_LDS = 2,      /* one workgroup, instance state in LDS: n <= 64 */
+    GWTF_PASS_GRID = 3,     /* one instance over S * ceil(n/128) co-resident workgroups: 64 < n <= 512 */
+    GWTF_PASS_GLOBAL = 4    /* one workgroup, instance state in device memory: any shape */
+};
+
 /* arc_cost entry meaning "these two nodes share no link". */
 #define GWTF_NO_ARC (-1)
 
@@ -110,6 +118,13 @@ gwtf_status_t gwtf_mcf_get_flows(gwtf_mcf_t *h, int32_t first, int32_t count,
  * potential update, and the rest (label reset, sink update), then the
  * executed forward and backward layer steps (0 where not tracked). */
 gwtf_status_t gwtf_mcf_get_stats(gwtf_mcf_t *h, int32_t first, int32_t count, int64_t *stats);
+
+/* Which solver pass produced each instance of the last solve, into a caller
+ * device buffer pass[count] (int32, GWTF_PASS_*).  The pass follows from the
+ * handle's shape, except that an instance whose link costs exceed 65534 or
+ * whose flow lists outgrow LDS moves to GWTF_PASS_GLOBAL.  Enqueued on the
+ * handle's stream; errors as for gwtf_mcf_get_stats. */
+gwtf_status_t gwtf_mcf_get_passes(gwtf_mcf_t *h, int32_t first, int32_t count, int32_t *pass);
 
 /* Frees the handle and its workspace after draining its stream; NULL-safe. */
 void gwtf_mcf_destroy(gwtf_mcf_t *h);

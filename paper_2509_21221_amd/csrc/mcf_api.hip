@@ -1,7 +1,9 @@
 // Host side of the C ABI declared in include/gwtf_mcf.h: argument checks,
-// workspace ownership, and the choice between the LDS-resident solver pass
-// (n <= 64, instance state in the workgroup's LDS) and the global-memory
-// fallback pass (any n, or instances whose flow lists outgrow LDS).
+// workspace ownership, and the choice of solver pass: register-resident
+// (16 < n <= 64, S <= 32), LDS-resident (n <= 64, one workgroup per
+// instance), grid-cooperative (64 < n <= 512, one instance over many
+// workgroups), and the global-memory fallback pass (any n, or instances
+// whose link costs or flow lists do not fit the faster passes).
 #include "gwtf_mcf.h"
 #include "mcf_internal.h"
 
@@ -25,6 +27,12 @@ struct gwtf_mcf {
     unsigned char *state = nullptr;
     size_t state_stride = 0;
     int64_t fallback_slots = 0;
+    // grid-cooperative pass (64 < n <= 512), when the device can hold its grid
+    bool grid = false;
+    int64_t grid_slots = 0;
+    size_t grid_lds = 0;
+    int32_t *g_ex = nullptr, *g_en = nullptr, *g_path = nullptr, *g_path_j = nullptr, *g_ctrl = nullptr;
+    int16_t *g_pred = nullptr;
     int32_t solved = 0; // batch size of the last successful solve (0 = none)
 };
 
@@ -80,9 +88,17 @@ void free_ws(gwtf_mcf_t *h)
     (void)hipFree(h->pot);
     (void)hipFree(h->stats);
     (void)hipFree(h->state);
+    (void)hipFree(h->g_ex);
+    (void)hipFree(h->g_en);
+    (void)hipFree(h->g_pred);
+    (void)hipFree(h->g_path);
+    (void)hipFree(h->g_path_j);
+    (void)hipFree(h->g_ctrl);
     h->route = h->node_flow = h->arc_flow = h->pot = nullptr;
     h->stats = nullptr;
     h->state = nullptr;
+    h->g_ex = h->g_en = h->g_path = h->g_path_j = h->g_ctrl = nullptr;
+    h->g_pred = nullptr;
 }
 
 } // namespace
@@ -127,6 +143,26 @@ extern "C" gwtf_status_t gwtf_mcf_create(const gwtf_mcf_shape_t *shape, void *hi
     h->fallback_slots = int64_t(std::max(S - 1, 0)) * n * n;
     h->state_stride = align16(make_layout(S, n, h->fallback_slots, false).total);
     const size_t na = size_t(std::max(S - 1, 0)) * n * n;
+
+    // Grid-cooperative pass: S * ceil(n / 128) workgroups must all be
+    // resident at once (cooperative launch), one per CU given their LDS.
+    if (n > 64 && n <= kGridMaxNodes && S <= 1024) {
+        int coop = 0, cus = 0;
+        if (hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, shape->device) != hipSuccess) coop = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, shape->device) != hipSuccess) cus = 0;
+        (void)hipGetLastError();
+        const int64_t slots = grid_pass_list_slots(S, n, h->lds_max);
+        if (coop && cus > 0 && slots >= 64) {
+            const size_t lds = grid_pass_lds_bytes(S, n, slots);
+            const int per_cu = grid_pass_blocks_per_cu(lds);
+            if (per_cu >= 1 && int64_t(S) * grid_pass_slices(n) <= int64_t(per_cu) * cus) {
+                h->grid = true;
+                h->grid_slots = slots;
+                h->grid_lds = lds;
+            }
+        }
+    }
+    const size_t gsn = h->grid ? size_t(SN) : 0;
     struct {
         void **p;
         size_t bytes;
@@ -137,8 +173,15 @@ extern "C" gwtf_status_t gwtf_mcf_create(const gwtf_mcf_shape_t *shape, void *hi
         {(void **)&h->pot, sizeof(int32_t) * V * B},
         {(void **)&h->stats, sizeof(int64_t) * kStatsPerInstance * B},
         {(void **)&h->state, h->state_stride * B},
+        {(void **)&h->g_ex, sizeof(int32_t) * 2 * gsn},
+        {(void **)&h->g_en, sizeof(int32_t) * 2 * gsn},
+        {(void **)&h->g_pred, 16 * ((2 * gsn + 7) / 8)},
+        {(void **)&h->g_path, sizeof(int32_t) * (2 * gsn + 8)},
+        {(void **)&h->g_path_j, sizeof(int32_t) * (2 * gsn + 8)},
+        {(void **)&h->g_ctrl, sizeof(int32_t) * kGridCtrlInts},
     };
     for (auto &a : allocs) {
+        if (a.bytes == 0) continue;
         if ((e = hipMalloc(a.p, a.bytes)) != hipSuccess) {
             g_create_err = std::string("hipMalloc workspace: ") + hipGetErrorString(e);
             free_ws(h);
@@ -193,7 +236,30 @@ extern "C" gwtf_status_t gwtf_mcf_solve_batch(gwtf_mcf_t *h, const gwtf_mcf_batc
         ? lds_slots_with(S, n, reg_pass_scratch_bytes() + kRegStaticLds, h->lds_max) : 0;
     const int waves = lds_waves(n);
     const int64_t slots = reg_slots > 0 ? 0 : lds_slots(S, n, waves, h->lds_max);
-    if (reg_slots > 0) {
+    if (h->grid) {
+        // One cooperative launch per instance; instances whose link costs
+        // need more than 16 bits or whose flow lists outgrow LDS go to the
+        // fallback pass.
+        GridParams gp{};
+        gp.base = p;
+        gp.base.list_slots = h->grid_slots;
+        gp.base.route_all = 0;
+        gp.slices = grid_pass_slices(n);
+        gp.list_slots = h->grid_slots;
+        gp.big_bytes = grid_pass_big_bytes(S, n);
+        gp.ex = h->g_ex;
+        gp.en = h->g_en;
+        gp.pred = h->g_pred;
+        gp.path = h->g_path;
+        gp.path_j = h->g_path_j;
+        gp.ctrl = h->g_ctrl;
+        for (int i = 0; i < b->batch; ++i) {
+            gp.instance = i;
+            if ((e = launch_grid_pass(gp, h->grid_lds, h->stream)) != hipSuccess)
+                return hip_fail(h, e, "grid solver launch");
+        }
+        need_fallback = true;
+    } else if (reg_slots > 0) {
         // Register-resident pass; instances whose link costs need more than
         // 16 bits or whose flow lists outgrow LDS go to the fallback pass.
         p.list_slots = reg_slots;
@@ -266,6 +332,21 @@ extern "C" gwtf_status_t gwtf_mcf_get_stats(gwtf_mcf_t *h, int32_t first, int32_
     e = hipMemcpyAsync(stats, h->stats + size_t(first) * kStatsPerInstance,
                        sizeof(int64_t) * kStatsPerInstance * count, hipMemcpyDeviceToDevice, h->stream);
     if (e != hipSuccess) return hip_fail(h, e, "copy stats");
+    return GWTF_OK;
+}
+
+extern "C" gwtf_status_t gwtf_mcf_get_passes(gwtf_mcf_t *h, int32_t first, int32_t count, int32_t *pass)
+{
+    if (!h) return fail(nullptr, GWTF_ERR_INVALID_ARG, "handle is NULL");
+    if (!pass) return fail(h, GWTF_ERR_INVALID_ARG, "pass is NULL");
+    if (h->solved == 0) return fail(h, GWTF_ERR_NOT_SOLVED, "no successful solve on this handle");
+    if (first < 0 || count < 0 || int64_t(first) + count > h->solved)
+        return fail(h, GWTF_ERR_RANGE, "instance range outside the last solved batch");
+    if (count == 0) return GWTF_OK;
+    hipError_t e = hipSetDevice(h->shape.device);
+    if (e != hipSuccess) return hip_fail(h, e, "hipSetDevice");
+    e = hipMemcpyAsync(pass, h->route + first, sizeof(int32_t) * count, hipMemcpyDeviceToDevice, h->stream);
+    if (e != hipSuccess) return hip_fail(h, e, "copy pass");
     return GWTF_OK;
 }
 

@@ -14,8 +14,9 @@ namespace gwtf {
 constexpr int32_t kInf = 0x3fffffff;
 constexpr int64_t kLabelBound = int64_t(1) << 29;
 
-// Route codes in the workspace: which solver pass finished an instance.
-enum : int32_t { kRouteDone = 0, kRouteFallback = 1, kRouteFallbackDone = 2 };
+// Route codes in the workspace: an instance waiting for the fallback pass,
+// or the pass that finished it (the public GWTF_PASS_* values).
+enum : int32_t { kRouteFallback = -1, kRouteReg = 1, kRouteLds = 2, kRouteGrid = 3, kRouteGlobal = 4 };
 
 // Kernel arguments shared by both solver passes.
 struct SolveParams {
@@ -100,5 +101,29 @@ size_t reg_pass_scratch_bytes();
 bool reg_pass_fits(int S, int n);
 constexpr size_t kRegStaticLds = 4096; // static LDS of the register-resident kernel (upper bound)
 hipError_t set_lds_limits(size_t max_bytes);
+
+// Grid-cooperative pass (mcf_solver_grid.hip): one instance at a time over
+// S * ceil(n / 128) co-resident workgroups, for 64 < n <= 512.
+constexpr int kGridCtrlInts = 32;      // control block: flags, barrier, per-iteration words
+constexpr int kGridMaxNodes = 512;     // a stage's labels are staged with one thread per node
+constexpr size_t kGridStaticLds = 512; // static LDS of the grid kernel (upper bound)
+struct GridParams {
+    SolveParams base;
+    int32_t instance;   // instance solved by this launch
+    int32_t slices;     // workgroups per stage
+    int64_t list_slots; // flow-list capacity of one workgroup
+    size_t big_bytes;   // leading LDS area: link-cost block or staged predecessors
+    int32_t *ex, *en;   // [2][S*n] exit / entry labels, double-buffered by iteration
+    int16_t *pred;      // [2*S*n rounded up to 8]: entry predecessors, then exit ones
+    int32_t *path;      // [2*S*n + 8] arc codes of the augmenting path
+    int32_t *path_j;    // [2*S*n + 8] head node of each link arc on the path
+    int32_t *ctrl;      // [kGridCtrlInts], cleared before each launch
+};
+size_t grid_pass_big_bytes(int S, int n);
+size_t grid_pass_lds_bytes(int S, int n, int64_t list_slots);
+int64_t grid_pass_list_slots(int S, int n, size_t lds_max);
+int grid_pass_slices(int n);
+int grid_pass_blocks_per_cu(size_t lds_bytes);
+hipError_t launch_grid_pass(const GridParams &gp, size_t lds_bytes, hipStream_t s);
 
 } // namespace gwtf

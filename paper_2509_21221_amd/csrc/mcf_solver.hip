@@ -148,7 +148,7 @@ __global__ __launch_bounds__(WAVES * 64) void solve_kernel(SolveParams p)
         if (tid == 0) p.route[b] = kRouteFallback;
         return;
     }
-    if (tid == 0) p.route[b] = NARROW ? kRouteDone : kRouteFallbackDone;
+    if (tid == 0) p.route[b] = NARROW ? kRouteLds : kRouteGlobal;
 
     const uint64_t myrows = wave_rows<WAVES>(wave);
     long long my_rows = 0, my_pulls = 0;

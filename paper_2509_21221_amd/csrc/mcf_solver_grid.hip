@@ -1,0 +1,678 @@
+// Grid-cooperative solver pass for one large instance (64 < n <= 512).
+//
+// Same objective and method as the other passes -- successive shortest paths
+// with Johnson potentials on the node-split stage graph (paper Sec. V-A,
+// Eq. 2) -- spread over the whole GPU instead of one workgroup:
+//
+//  * Workgroup g owns a block of NB = 128 nodes of one stage k (g = k *
+//    slices + s covers nodes s*NB ...): their entry/exit labels, predecessors,
+//    exit potentials, compute arcs and the flow lists of their exits, plus the
+//    column block of the link layer that feeds them (all n exits of stage k-1
+//    by its NB entries) as 16-bit costs in LDS.  The launch is cooperative,
+//    one workgroup per CU, so every workgroup is resident.
+//  * Shortest paths come from a Jacobi label-correcting iteration.  In one
+//    iteration each workgroup relaxes the links into its entries from the
+//    exit labels of stage k-1 published by the previous iteration (only the
+//    rows whose label dropped since it last saw them), applies its nodes'
+//    compute arcs in both directions, pulls its exits' reverse links from the
+//    previous iteration's entry labels of stage k+1, and publishes its labels
+//    into the other half of a double buffer.  One grid barrier separates
+//    iterations; the iteration stops when no label changed anywhere.
+//  * Workgroup 0 (stage 0, which holds no link costs) stages all
+//    predecessors in its LDS, walks the augmenting path and finds its
+//    bottleneck; each owner then applies the path to its nodes and lists.
+//
+// The grid barrier is an arrival counter plus a generation word updated with
+// device-scope atomics.  Its wait is bounded: a barrier that does not complete
+// within the bound ends the solve with the internal-error status instead of
+// hanging the device.
+#include "mcf_device.h"
+
+namespace gwtf {
+namespace {
+
+using namespace dev;
+
+constexpr int kGridThreads = 512;
+constexpr int kGridWaves = kGridThreads / 64;
+constexpr int kGridNB = 128;                           // nodes per workgroup
+constexpr int kGridRowGroups = kGridThreads / kGridNB; // rows split over 4 groups
+constexpr uint16_t kNoArc16 = 0xffff;
+constexpr int kBias = 1 << 30;
+constexpr int kSpinLimit = 1 << 20;
+
+enum : int { kArcSplitFwd = 0, kArcSplitRev = 1, kArcLinkFwd = 2, kArcLinkRev = 3 };
+// grid-wide status bits
+enum : int { kFlagBad = 1, kFlagWide = 2, kFlagLists = 4, kFlagFault = 8 };
+// control words (int32 indices into GridParams::ctrl)
+enum : int {
+    kCtlFlags = 0,
+    kCtlMaxCost = 1,
+    kCtlBarCount = 2,
+    kCtlBarGen = 3,
+    kCtlChanged = 4, // [3]
+    kCtlDtKey = 8,   // 3 x uint64
+    kCtlDelta = 16,
+    kCtlLen = 17,
+    kCtlRelax = 20, // uint64
+    kCtlPulls = 22, // uint64
+};
+static_assert(kCtlPulls + 2 <= kGridCtrlInts, "control block too small");
+
+__device__ __forceinline__ uint64_t pack_key(int label, int idx)
+{
+    return (uint64_t(uint32_t(label + kBias)) << 32) | uint32_t(idx);
+}
+__device__ __forceinline__ int key_label(uint64_t key) { return int(uint32_t(key >> 32)) - kBias; }
+
+__device__ __forceinline__ int load_acq(const int *p)
+{
+    return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ unsigned long long load_acq_u64(const unsigned long long *p)
+{
+    return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Grid barrier; the call returns the same value in every thread of a block.
+struct GridBarrier {
+    unsigned *count, *gen;
+    unsigned nblocks, local_gen;
+
+    __device__ bool sync(int *ok_lds)
+    {
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            __threadfence();
+            const unsigned g = local_gen;
+            bool good = true;
+            if (atomicAdd(count, 1u) + 1u == nblocks) {
+                __hip_atomic_store(count, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_fetch_add(gen, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+            } else {
+                int spins = 0;
+                while (__hip_atomic_load(gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == g) {
+                    if (++spins > kSpinLimit) {
+                        good = false;
+                        break;
+                    }
+                    __builtin_amdgcn_s_sleep(1);
+                }
+            }
+            __threadfence();
+            local_gen = g + 1u;
+            *ok_lds = good;
+        }
+        __syncthreads();
+        return *ok_lds != 0;
+    }
+};
+
+__global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams gp)
+{
+    const SolveParams &p = gp.base;
+    const int b = gp.instance;
+    const int S = p.S, n = p.n, SN = S * n, V = 2 * SN + 3;
+    const int g = blockIdx.x, k = g / gp.slices, s = g % gp.slices;
+    const int j0 = s * kGridNB, nown = min(kGridNB, n - j0);
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int col = tid % kGridNB, rgrp = tid / kGridNB;
+    const bool has_prev = k >= 1, has_next = k + 1 < S;
+
+    extern __shared__ __align__(16) unsigned char smem[];
+    __shared__ int sh_ok, sh_bad, sh_maxc, sh_changed, sh_len, sh_delta, sh_fault;
+    __shared__ unsigned long long sh_key;
+    __shared__ int wcnt[kGridWaves];
+
+    // ---- LDS layout (same offsets in every workgroup) ----
+    // The leading area holds the link-cost block; workgroup 0 (no incoming
+    // links) uses it for the staged predecessors instead.
+    uint16_t *cost16 = reinterpret_cast<uint16_t *>(smem);
+    int16_t *all_pred = reinterpret_cast<int16_t *>(smem); // [2*SN]: entries, then exits
+    size_t o = align16(gp.big_bytes);
+    auto take = [&](size_t bytes) {
+        unsigned char *at = smem + o;
+        o = align16(o + bytes);
+        return at;
+    };
+    int *exrow = reinterpret_cast<int *>(take(4 * size_t(n)));   // last seen exit labels of stage k-1
+    int *enrow = reinterpret_cast<int *>(take(4 * size_t(n)));   // entry labels of stage k+1
+    int *rowlist = reinterpret_cast<int *>(take(4 * size_t(n))); // rows of stage k-1 that dropped
+    int *din = reinterpret_cast<int *>(take(4 * kGridNB));
+    int *dout = reinterpret_cast<int *>(take(4 * kGridNB));
+    int *pout = reinterpret_cast<int *>(take(4 * kGridNB));
+    int *flow = reinterpret_cast<int *>(take(4 * kGridNB));
+    int *cap = reinterpret_cast<int *>(take(4 * kGridNB));
+    int *ncost = reinterpret_cast<int *>(take(4 * kGridNB));
+    int *srcc = reinterpret_cast<int *>(take(4 * kGridNB));
+    int *snkc = reinterpret_cast<int *>(take(4 * kGridNB));
+    int *prin = reinterpret_cast<int *>(take(4 * kGridNB));
+    int *prout = reinterpret_cast<int *>(take(4 * kGridNB));
+    int *loff = reinterpret_cast<int *>(take(4 * kGridNB));
+    int *llen = reinterpret_cast<int *>(take(4 * kGridNB));
+    uint64_t *red = reinterpret_cast<uint64_t *>(take(8 * kGridRowGroups * kGridNB));
+    int *lcost = reinterpret_cast<int *>(take(4 * size_t(gp.list_slots)));
+    int *lamt = reinterpret_cast<int *>(take(4 * size_t(gp.list_slots)));
+    int16_t *lpart = reinterpret_cast<int16_t *>(take(2 * size_t(gp.list_slots)));
+    int *scanbuf = reinterpret_cast<int *>(red); // ingest only; red holds >= kGridThreads ints
+
+    int *ctrl = gp.ctrl;
+    int *changed = ctrl + kCtlChanged;
+    unsigned long long *dtkey = reinterpret_cast<unsigned long long *>(ctrl + kCtlDtKey);
+    GridBarrier bar{reinterpret_cast<unsigned *>(ctrl + kCtlBarCount), reinterpret_cast<unsigned *>(ctrl + kCtlBarGen),
+                    gridDim.x, 0u};
+    if (tid == 0) bar.local_gen = __hip_atomic_load(bar.gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+
+    const int32_t *gcap = p.cap + size_t(b) * SN;
+    const int32_t *gnc = p.ncost + size_t(b) * SN;
+    const int32_t *gac = p.acost ? p.acost + size_t(b) * (S - 1) * n * n : nullptr;
+    const int supply = p.supply[b];
+    int32_t *gpot = p.pot + size_t(b) * V;
+    int32_t *gnf = p.node_flow + size_t(b) * SN;
+    int32_t *gaf = p.arc_flow + size_t(b) * (S - 1) * n * n;
+
+    // ---------------- ingest ----------------
+    if (tid == 0) {
+        sh_bad = supply < 0;
+        sh_maxc = 0;
+        sh_fault = 0;
+        sh_key = ~0ull;
+    }
+    __syncthreads();
+    int bad = 0, wide = 0, mx = 0;
+    if (tid < kGridNB) {
+        const int c = tid;
+        const bool own = c < nown;
+        const int q = k * n + j0 + c;
+        const int cp = own ? gcap[q] : 0, w = own ? gnc[q] : 0;
+        const int a = (own && k == 0 && p.src) ? p.src[size_t(b) * n + j0 + c] : 0;
+        const int z = (own && k == S - 1 && p.snk) ? p.snk[size_t(b) * n + j0 + c] : 0;
+        bad |= (cp < 0) | (w < 0) | (a < 0) | (z < 0);
+        mx = max(max(mx, w), max(a, z));
+        cap[c] = cp;
+        ncost[c] = w;
+        srcc[c] = a;
+        snkc[c] = z;
+        flow[c] = 0;
+        pout[c] = 0;
+        if (own) {
+            gnf[q] = 0;
+            gpot[3 + 2 * q] = 0;
+            gpot[4 + 2 * q] = 0;
+        }
+    }
+    if (has_prev) {
+        const int32_t *layer = gac + size_t(k - 1) * n * n;
+        for (int e = tid; e < n * kGridNB; e += kGridThreads) {
+            const int i = e / kGridNB, c = e % kGridNB;
+            const int a = c < nown ? layer[size_t(i) * n + j0 + c] : -1;
+            bad |= a < -1;
+            wide |= a > 65534;
+            mx = max(mx, a);
+            cost16[e] = (a < 0 || a > 65534) ? kNoArc16 : uint16_t(a);
+        }
+    }
+    if (has_next) {
+        int32_t *rows = gaf + size_t(k) * n * n + size_t(j0) * n;
+        for (int e = tid; e < nown * n; e += kGridThreads) rows[e] = 0;
+    }
+    if (g == 0 && tid < 3) gpot[tid] = 0;
+    if (bad) atomicOr(&sh_bad, 1);
+    if (wide) atomicOr(&sh_bad, 2);
+    atomicMax(&sh_maxc, mx);
+    // flow-list capacity of each owned exit: min(cap, n, supply)
+    int mine = 0;
+    if (tid < nown && has_next && supply > 0 && cap[tid] > 0) mine = min(min(cap[tid], n), supply);
+    int total_slots;
+    const int off0 = block_exclusive_scan<kGridThreads>(mine, scanbuf, total_slots);
+    if (tid < kGridNB) {
+        loff[tid] = off0;
+        llen[tid] = 0;
+    }
+    if (tid == 0) {
+        int f = 0;
+        if (sh_bad & 1) f |= kFlagBad;
+        if (sh_bad & 2) f |= kFlagWide;
+        if (total_slots > gp.list_slots) f |= kFlagLists;
+        if (f) atomicOr(&ctrl[kCtlFlags], f);
+        atomicMax(&ctrl[kCtlMaxCost], sh_maxc);
+    }
+    bool timed_out = !bar.sync(&sh_ok);
+    int status = 0;
+    if (!timed_out) {
+        const int fl0 = load_acq(&ctrl[kCtlFlags]), maxc = load_acq(&ctrl[kCtlMaxCost]);
+        if (fl0 & kFlagBad) status = 1;
+        else if (int64_t(V) * maxc >= kLabelBound) status = 2;
+        if (status == 0 && (fl0 & (kFlagWide | kFlagLists))) {
+            // 16-bit link costs or LDS lists do not fit: the fallback pass
+            // solves this instance (every workgroup leaves here).
+            if (g == 0 && tid == 0) p.route[b] = kRouteFallback;
+            return;
+        }
+    }
+
+    long long F = 0, cost = 0, rounds = 0, augs = 0, my_relax = 0, my_pulls = 0;
+    int pit = 0;
+
+    // Labels of a fresh shortest-path search; buffer 0 holds its inputs.
+    auto reset_labels = [&]() {
+        if (tid < kGridNB) {
+            const int c = tid, q = k * n + j0 + c;
+            const int d0 = k == 0 ? srcc[c] : kInf;
+            din[c] = d0;
+            dout[c] = kInf;
+            prin[c] = k == 0 ? kPredSrc : kPredNone;
+            prout[c] = kPredNone;
+            if (c < nown) {
+                gp.ex[q] = kInf;
+                gp.en[q] = d0;
+            }
+        }
+        for (int i = tid; i < n; i += kGridThreads) exrow[i] = kInf;
+        if (g == 0 && tid < 3) {
+            changed[tid] = 0;
+            dtkey[tid] = ~0ull;
+        }
+    };
+
+    if (!timed_out && status == 0 && supply > 0) {
+        reset_labels();
+        timed_out = !bar.sync(&sh_ok);
+        while (!timed_out) {
+            // ---- (1) Jacobi label-correcting iteration ----
+            uint64_t final_key = ~0ull;
+            bool converged = false;
+            for (int t = 0; t < 4 * V + 8; ++t) {
+                const int *ex_in = gp.ex + size_t(t & 1) * SN;
+                const int *en_in = gp.en + size_t(t & 1) * SN;
+                int *ex_out = gp.ex + size_t((t + 1) & 1) * SN;
+                int *en_out = gp.en + size_t((t + 1) & 1) * SN;
+                int dropped = 0;
+                if (tid < n) {
+                    if (has_prev) {
+                        const int d = ex_in[(k - 1) * n + tid];
+                        dropped = d < exrow[tid];
+                        if (dropped) exrow[tid] = d;
+                    }
+                    if (has_next) enrow[tid] = en_in[(k + 1) * n + tid];
+                }
+                const uint64_t m = __ballot(dropped);
+                if (lane == 0) wcnt[wave] = __popcll(m);
+                if (tid == 0) sh_changed = 0;
+                __syncthreads();
+                int base = 0, nrows = 0;
+                for (int w = 0; w < kGridWaves; ++w) {
+                    const int cnt = wcnt[w];
+                    base += w < wave ? cnt : 0;
+                    nrows += cnt;
+                }
+                if (dropped) rowlist[base + __popcll(m & ((1ull << lane) - 1ull))] = tid;
+                __syncthreads();
+
+                // links into this block's entries, from the rows that dropped
+                uint64_t key = ~0ull;
+                if (col < nown) {
+                    int best = kInf, arg = -1;
+                    for (int e = rgrp; e < nrows; e += kGridRowGroups) {
+                        const int i = rowlist[e];
+                        const uint16_t c = cost16[i * kGridNB + col];
+                        const int cand = exrow[i] + int(c);
+                        const bool take_it = (c != kNoArc16) & (cand < best);
+                        best = take_it ? cand : best;
+                        arg = take_it ? i : arg;
+                    }
+                    if (best < kInf) key = pack_key(best, arg);
+                }
+                red[rgrp * kGridNB + col] = key;
+                __syncthreads();
+
+                // compute arcs and reverse links of the owned nodes
+                if (tid < nown) {
+                    const int c = tid, q = k * n + j0 + c;
+                    uint64_t kb = red[c];
+#pragma unroll
+                    for (int r = 1; r < kGridRowGroups; ++r) kb = min(kb, (uint64_t)red[r * kGridNB + c]);
+                    int di = din[c], dq = dout[c], pi = prin[c], po = prout[c];
+                    const int di0 = di, dq0 = dq;
+                    const int fl = flow[c], cp = cap[c], nc = ncost[c];
+                    if (kb != ~0ull && key_label(kb) < di) {
+                        di = key_label(kb);
+                        pi = int(uint32_t(kb));
+                    }
+                    if (fl > 0 && dq < kInf && dq - nc < di) {
+                        di = dq - nc;
+                        pi = kPredSplit;
+                    }
+                    if (di < kInf && fl < cp && di + nc < dq) {
+                        dq = di + nc;
+                        po = kPredSplit;
+                    }
+                    if (has_next) {
+                        const int lo = loff[c], hi = lo + llen[c];
+                        for (int e = lo; e < hi; ++e) {
+                            const int j = lpart[e];
+                            const int dj = enrow[j];
+                            if (dj < kInf && dj - lcost[e] < dq) {
+                                dq = dj - lcost[e];
+                                po = j;
+                            }
+                        }
+                        my_pulls += hi - lo;
+                    }
+                    if (fl > 0 && dq < kInf && dq - nc < di) {
+                        di = dq - nc;
+                        pi = kPredSplit;
+                    }
+                    din[c] = di;
+                    dout[c] = dq;
+                    prin[c] = pi;
+                    prout[c] = po;
+                    ex_out[q] = dq;
+                    en_out[q] = di;
+                    if ((di != di0) | (dq != dq0)) sh_changed = 1;
+                    if (k == S - 1 && dq < kInf) atomicMin(&sh_key, (unsigned long long)pack_key(dq + snkc[c], j0 + c));
+                }
+                __syncthreads();
+                if (tid == 0) {
+                    if (sh_changed) atomicAdd(&changed[t % 3], 1);
+                    if (sh_key != ~0ull) atomicMin(&dtkey[t % 3], sh_key);
+                    sh_key = ~0ull;
+                    my_relax += (long long)nrows * nown;
+                }
+                rounds++;
+                if (!bar.sync(&sh_ok)) {
+                    timed_out = true;
+                    break;
+                }
+                if (g == 0 && tid == 0) {
+                    changed[(t + 2) % 3] = 0;
+                    dtkey[(t + 2) % 3] = ~0ull;
+                }
+                if (load_acq(&changed[t % 3]) == 0) {
+                    final_key = load_acq_u64(&dtkey[t % 3]);
+                    converged = true;
+                    break;
+                }
+            }
+            if (timed_out) break;
+            if (!converged) {
+                if (tid == 0) sh_fault = 1;
+                break;
+            }
+            if (final_key == ~0ull) break; // sink unreachable: the flow is maximum
+
+            // ---- (2) potentials; publish predecessors ----
+            const int Dt = key_label(final_key), predt = int(uint32_t(final_key));
+            const int dred = Dt - pit;
+            if (tid < nown) {
+                const int c = tid, q = k * n + j0 + c;
+                pout[c] = min(dout[c], pout[c] + dred);
+                gpot[3 + 2 * q] = min(din[c], gpot[3 + 2 * q] + dred);
+                gp.pred[q] = int16_t(prin[c]);
+                gp.pred[SN + q] = int16_t(prout[c]);
+            }
+            if (!bar.sync(&sh_ok)) {
+                timed_out = true;
+                break;
+            }
+
+            // ---- (3) workgroup 0: walk the path, find the bottleneck ----
+            if (g == 0) {
+                const int n4 = (2 * SN + 7) / 8;
+                const int4 *src4 = reinterpret_cast<const int4 *>(gp.pred);
+                int4 *dst4 = reinterpret_cast<int4 *>(smem);
+                for (int x = tid; x < n4; x += kGridThreads) dst4[x] = src4[x];
+                __syncthreads();
+                if (tid == 0) {
+                    int kk = S - 1, i = predt, len = 0;
+                    bool at_exit = true, okw = predt >= 0 && predt < n;
+                    for (int steps = 0; okw; ++steps) {
+                        if (steps > 2 * SN + 4) {
+                            okw = false;
+                            break;
+                        }
+                        // Arc codes: type | stage << 2 | node << 12.  Splits
+                        // name their node; links name their tail exit (the
+                        // link's stage and row) and keep the head in path_j.
+                        int code, ak = kk, ai = i, j = 0;
+                        if (at_exit) {
+                            const int pr = all_pred[SN + kk * n + i];
+                            if (pr == kPredSplit) {
+                                code = kArcSplitFwd; // entry -> exit of (kk, i)
+                                at_exit = false;
+                            } else if (pr >= 0 && kk + 1 < S) {
+                                code = kArcLinkRev; // entry (kk+1, pr) -> exit (kk, i)
+                                j = pr;
+                                kk = kk + 1;
+                                i = pr;
+                                at_exit = false;
+                            } else {
+                                okw = false;
+                                break;
+                            }
+                        } else {
+                            const int pr = all_pred[kk * n + i];
+                            if (pr == kPredSrc) break;
+                            if (pr == kPredSplit) {
+                                code = kArcSplitRev; // exit -> entry of (kk, i)
+                                at_exit = true;
+                            } else if (pr >= 0 && kk >= 1) {
+                                code = kArcLinkFwd; // exit (kk-1, pr) -> entry (kk, i)
+                                ak = kk - 1;
+                                ai = pr;
+                                j = i;
+                                kk = kk - 1;
+                                i = pr;
+                                at_exit = true;
+                            } else {
+                                okw = false;
+                                break;
+                            }
+                        }
+                        gp.path[len] = code | (ak << 2) | (ai << 12);
+                        gp.path_j[len] = j;
+                        ++len;
+                    }
+                    sh_len = okw ? len : -1;
+                    sh_delta = supply - int(F);
+                }
+                __syncthreads();
+                const int len = sh_len;
+                if (len >= 0) {
+                    int r = 0x7fffffff;
+                    for (int e = tid; e < len; e += kGridThreads) {
+                        const int code = gp.path[e], type = code & 3, ak = (code >> 2) & 1023, ai = code >> 12;
+                        const int q = ak * n + ai;
+                        if (type == kArcSplitFwd) r = min(r, gcap[q] - gnf[q]);
+                        else if (type == kArcSplitRev) r = min(r, gnf[q]);
+                        else if (type == kArcLinkRev) r = min(r, gaf[size_t(q) * n + gp.path_j[e]]);
+                    }
+                    atomicMin(&sh_delta, r);
+                }
+                __syncthreads();
+                if (tid == 0) {
+                    ctrl[kCtlDelta] = len < 0 ? -1 : sh_delta;
+                    ctrl[kCtlLen] = len;
+                }
+            }
+            if (!bar.sync(&sh_ok)) {
+                timed_out = true;
+                break;
+            }
+
+            // ---- (4) owners apply the augmentation: decrements, then increments ----
+            const int delta = load_acq(&ctrl[kCtlDelta]), len = load_acq(&ctrl[kCtlLen]);
+            if (delta <= 0 || len < 0) {
+                if (tid == 0) sh_fault = 1;
+                break;
+            }
+            for (int pass = 0; pass < 2; ++pass) {
+                for (int e = tid; e < len; e += kGridThreads) {
+                    const int code = gp.path[e], type = code & 3, ak = (code >> 2) & 1023, ai = code >> 12;
+                    if (ak != k || ai < j0 || ai >= j0 + nown) continue;
+                    const int c = ai - j0, q = ak * n + ai, j = gp.path_j[e];
+                    if (pass == 0) {
+                        if (type == kArcSplitFwd || type == kArcSplitRev) {
+                            flow[c] += type == kArcSplitFwd ? delta : -delta;
+                            gnf[q] = flow[c];
+                        } else if (type == kArcLinkRev) {
+                            const int lo = loff[c], hi = lo + llen[c];
+                            int le = -1;
+                            for (int x = lo; x < hi; ++x)
+                                if (lpart[x] == j) le = x;
+                            if (le < 0 || lamt[le] < delta) {
+                                sh_fault = 1;
+                                continue;
+                            }
+                            if (lamt[le] == delta) { // the arc empties: move the last entry here
+                                lpart[le] = lpart[hi - 1];
+                                lamt[le] = lamt[hi - 1];
+                                lcost[le] = lcost[hi - 1];
+                                llen[c] = hi - 1 - lo;
+                            } else {
+                                lamt[le] -= delta;
+                            }
+                            gaf[size_t(q) * n + j] -= delta;
+                        }
+                    } else if (type == kArcLinkFwd) {
+                        const int lo = loff[c], hi = lo + llen[c];
+                        int le = -1;
+                        for (int x = lo; x < hi; ++x)
+                            if (lpart[x] == j) le = x;
+                        if (le >= 0) {
+                            lamt[le] += delta;
+                        } else if (hi - lo >= min(min(cap[c], n), supply)) {
+                            sh_fault = 1;
+                            continue;
+                        } else {
+                            lpart[hi] = int16_t(j);
+                            lamt[hi] = delta;
+                            lcost[hi] = gac[size_t(q) * n + j];
+                            llen[c] = hi + 1 - lo;
+                        }
+                        gaf[size_t(q) * n + j] += delta;
+                    }
+                }
+                __syncthreads();
+            }
+            F += delta;
+            cost += (long long)delta * Dt;
+            augs++;
+            pit = Dt;
+            if (tid == 0 && sh_fault) atomicOr(&ctrl[kCtlFlags], kFlagFault);
+            if (F >= supply) break;
+            reset_labels();
+            if (!bar.sync(&sh_ok)) {
+                timed_out = true;
+                break;
+            }
+            if (load_acq(&ctrl[kCtlFlags]) & kFlagFault) break; // every workgroup reads the same word
+        }
+    }
+
+    // ---------------- export ----------------
+    if (tid == 0) {
+        if (sh_fault || timed_out) atomicOr(&ctrl[kCtlFlags], kFlagFault);
+        atomicAdd(reinterpret_cast<unsigned long long *>(ctrl + kCtlRelax), (unsigned long long)my_relax);
+    }
+    if (my_pulls) atomicAdd(reinterpret_cast<unsigned long long *>(ctrl + kCtlPulls), (unsigned long long)my_pulls);
+    // A barrier that times out here still ends the kernel; the workgroup
+    // then reports a fault.
+    const bool fault = !bar.sync(&sh_ok) || (load_acq(&ctrl[kCtlFlags]) & kFlagFault) || timed_out;
+    const bool ok = status == 0 && !fault;
+    if (tid < nown) {
+        const int q = k * n + j0 + tid;
+        gpot[4 + 2 * q] = ok ? pout[tid] : 0;
+        if (!ok) {
+            gpot[3 + 2 * q] = 0;
+            gnf[q] = 0;
+        }
+    }
+    if (!ok && has_next) {
+        int32_t *rows = gaf + size_t(k) * n * n + size_t(j0) * n;
+        for (int e = tid; e < nown * n; e += kGridThreads) rows[e] = 0;
+    }
+    if (g == 0 && tid == 0) {
+        gpot[2] = ok ? pit : 0;
+        p.F_out[b] = ok ? F : 0;
+        p.cost_out[b] = ok ? cost : 0;
+        p.status_out[b] = status != 0 ? status : (fault ? kStatusInternal : 0);
+        p.route[b] = kRouteGrid;
+        int64_t *st = p.stats + size_t(b) * kStatsPerInstance;
+        st[0] = augs;
+        st[1] = rounds;
+        st[2] = int64_t(load_acq_u64(reinterpret_cast<unsigned long long *>(ctrl + kCtlRelax)) / uint64_t(n));
+        st[3] = int64_t(load_acq_u64(reinterpret_cast<unsigned long long *>(ctrl + kCtlPulls)));
+        for (int x = 4; x < kStatsPerInstance; ++x) st[x] = 0;
+    }
+}
+
+__global__ void grid_ctrl_reset_kernel(int32_t *ctrl)
+{
+    if (threadIdx.x < kGridCtrlInts) ctrl[threadIdx.x] = 0;
+}
+
+size_t lds_fixed(int S, int n)
+{
+    size_t o = align16(grid_pass_big_bytes(S, n));
+    for (int a = 0; a < 3; ++a) o = align16(o + 4 * size_t(n));
+    for (int a = 0; a < 12; ++a) o = align16(o + 4 * size_t(kGridNB));
+    o = align16(o + 8 * size_t(kGridRowGroups) * kGridNB);
+    return o;
+}
+
+} // namespace
+
+size_t grid_pass_big_bytes(int S, int n)
+{
+    const size_t preds = size_t((2 * int64_t(S) * n + 7) / 8) * 16;
+    return std::max(size_t(n) * kGridNB * 2, preds);
+}
+
+size_t grid_pass_lds_bytes(int S, int n, int64_t list_slots)
+{
+    size_t o = lds_fixed(S, n);
+    o = align16(o + 4 * size_t(list_slots));
+    o = align16(o + 4 * size_t(list_slots));
+    o = align16(o + 2 * size_t(list_slots));
+    return o;
+}
+
+int64_t grid_pass_list_slots(int S, int n, size_t lds_max)
+{
+    const size_t fixed = lds_fixed(S, n) + kGridStaticLds + 64;
+    if (fixed >= lds_max) return 0;
+    return int64_t((lds_max - fixed) / 10);
+}
+
+int grid_pass_slices(int n) { return (n + kGridNB - 1) / kGridNB; }
+
+int grid_pass_blocks_per_cu(size_t lds_bytes)
+{
+    // Raising the dynamic-LDS ceiling is not needed on every runtime; a
+    // refusal is harmless but must not linger for a later launch check.
+    if (hipFuncSetAttribute(reinterpret_cast<const void *>(solve_grid_kernel),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, int(lds_bytes)) != hipSuccess)
+        (void)hipGetLastError();
+    int per_cu = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(solve_grid_kernel),
+                                                     kGridThreads, lds_bytes) != hipSuccess) {
+        (void)hipGetLastError();
+        return 0;
+    }
+    return per_cu;
+}
+
+hipError_t launch_grid_pass(const GridParams &gp, size_t lds_bytes, hipStream_t s)
+{
+    hipLaunchKernelGGL(grid_ctrl_reset_kernel, dim3(1), dim3(kGridCtrlInts), 0, s, gp.ctrl);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    GridParams arg = gp;
+    void *args[] = {&arg};
+    return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(solve_grid_kernel),
+                                      dim3(unsigned(gp.base.S * gp.slices)), dim3(kGridThreads), args,
+                                      unsigned(lds_bytes), s);
+}
+
+} // namespace gwtf

@@ -227,7 +227,7 @@ __global__ __launch_bounds__(kRegThreads) void solve_reg_kernel(SolveParams p)
         if (tid == 0) p.route[b] = kRouteFallback;
         return;
     }
-    if (tid == 0) p.route[b] = kRouteDone;
+    if (tid == 0) p.route[b] = kRouteReg;
 
     long long my_pulls = 0, wave_rows = 0, fwd_steps = 0, bwd_steps = 0;
     const int lq = min(lane, n - 1);            // in-bounds stand-in index for lanes >= n

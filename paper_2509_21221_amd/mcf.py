@@ -29,6 +29,10 @@ GWTF_INST_BAD_INPUT = 1
 GWTF_INST_OVERFLOW = 2
 GWTF_NO_ARC = -1
 STATS_PER_INSTANCE = 10
+GWTF_PASS_REGISTER = 1
+GWTF_PASS_LDS = 2
+GWTF_PASS_GRID = 3
+GWTF_PASS_GLOBAL = 4
 
 STATUS_NAMES = {0: "GWTF_OK", 1: "GWTF_ERR_INVALID_ARG", 2: "GWTF_ERR_OUT_OF_MEMORY",
                 3: "GWTF_ERR_DEVICE", 4: "GWTF_ERR_NOT_SOLVED", 5: "GWTF_ERR_RANGE"}
@@ -78,6 +82,8 @@ def load_library(path: str = LIB_PATH):
         lib.gwtf_mcf_get_flows.restype = ctypes.c_int
         lib.gwtf_mcf_get_stats.argtypes = [vp, i32, i32, i64p]
         lib.gwtf_mcf_get_stats.restype = ctypes.c_int
+        lib.gwtf_mcf_get_passes.argtypes = [vp, i32, i32, vp]
+        lib.gwtf_mcf_get_passes.restype = ctypes.c_int
         lib.gwtf_mcf_destroy.argtypes = [vp]
         lib.gwtf_mcf_destroy.restype = None
         lib.gwtf_mcf_last_error.argtypes = [vp]
@@ -126,6 +132,11 @@ def gwtf_mcf_get_flows(handle, first: int, count: int, node_flow: int = 0, arc_f
 def gwtf_mcf_get_stats(handle, first: int, count: int, stats: int) -> None:
     _check(load_library().gwtf_mcf_get_stats(ctypes.c_void_p(handle), first, count,
                                              stats or None), handle)
+
+
+def gwtf_mcf_get_passes(handle, first: int, count: int, passes: int) -> None:
+    _check(load_library().gwtf_mcf_get_passes(ctypes.c_void_p(handle), first, count,
+                                              passes or None), handle)
 
 
 def gwtf_mcf_destroy(handle) -> None:
@@ -206,6 +217,13 @@ class Solver:
         st = torch.empty((count, STATS_PER_INSTANCE), dtype=torch.int64, device=torch.device("cuda", self.device))
         gwtf_mcf_get_stats(self.handle, first, count, st.data_ptr())
         return st
+
+    def passes(self, first: int = 0, count: int | None = None):
+        torch = self.torch
+        count = self.last_batch - first if count is None else count
+        out = torch.empty(count, dtype=torch.int32, device=torch.device("cuda", self.device))
+        gwtf_mcf_get_passes(self.handle, first, count, out.data_ptr())
+        return out
 
     def close(self):
         if self.handle:

@@ -27,6 +27,7 @@ def gpu_solve(batch, flows=True, stats=False, solver=None):
         out.update({k: v.cpu().numpy() for k, v in solver.flows().items()})
     if stats:
         out["stats"] = solver.stats().cpu().numpy()
+    out["passes"] = solver.passes().cpu().numpy()
     torch.cuda.synchronize()
     out.update(F=F.cpu().numpy(), cost=cost.cpu().numpy(), status=status.cpu().numpy())
     if own:

@@ -43,7 +43,9 @@ def test_header_constants_match_binding():
     assert "GWTF_NO_ARC (-1)" in text and mcf.GWTF_NO_ARC == -1
     for name, value in [("GWTF_OK", 0), ("GWTF_ERR_INVALID_ARG", 1), ("GWTF_ERR_OUT_OF_MEMORY", 2),
                         ("GWTF_ERR_DEVICE", 3), ("GWTF_ERR_NOT_SOLVED", 4), ("GWTF_ERR_RANGE", 5),
-                        ("GWTF_INST_OK", 0), ("GWTF_INST_BAD_INPUT", 1), ("GWTF_INST_OVERFLOW", 2)]:
+                        ("GWTF_INST_OK", 0), ("GWTF_INST_BAD_INPUT", 1), ("GWTF_INST_OVERFLOW", 2),
+                        ("GWTF_PASS_REGISTER", 1), ("GWTF_PASS_LDS", 2), ("GWTF_PASS_GRID", 3),
+                        ("GWTF_PASS_GLOBAL", 4)]:
         assert re.search(rf"\b{name}\s*=\s*{value}\b", text), name
         assert getattr(mcf, name) == value
 
@@ -54,6 +56,7 @@ def test_null_handle_calls_fail_cleanly():
     assert lib.gwtf_mcf_solve_batch(None, None) == mcf.GWTF_ERR_INVALID_ARG
     assert lib.gwtf_mcf_get_flows(None, 0, 1, None, None, None, None, None) == mcf.GWTF_ERR_INVALID_ARG
     assert lib.gwtf_mcf_get_stats(None, 0, 1, None) == mcf.GWTF_ERR_INVALID_ARG
+    assert lib.gwtf_mcf_get_passes(None, 0, 1, None) == mcf.GWTF_ERR_INVALID_ARG
     lib.gwtf_mcf_destroy(None)
     out = ctypes.c_void_p(1)
     assert lib.gwtf_mcf_create(None, None, ctypes.byref(out)) == mcf.GWTF_ERR_INVALID_ARG

@@ -14,6 +14,7 @@ import numpy as np
 import pytest
 
 import oracle
+from paper_2509_21221_amd import mcf
 from paper_2509_21221_amd import workloads as W
 import mcf_checks as C
 from gpu_util import gpu_solve
@@ -110,11 +111,53 @@ def test_random_shapes(S, n, holes, zero):
 
 
 @pytest.mark.parametrize("S,n", [(3, 65), (4, 100), (2, 130)])
-def test_wide_stages_use_fallback(S, n):
+def test_wide_stages(S, n):
     batch = W.random_small(6, S, n, seed=3, cap_hi=4, cost_hi=300, supply_hi=2 * n, holes=0.1,
                            zero_cap=0.1)
     say("wide", S, n)
-    compare(batch, gpu_solve(batch), oracle.solve(batch))
+    g = gpu_solve(batch)
+    compare(batch, g, oracle.solve(batch))
+    assert (g["passes"] == mcf.GWTF_PASS_GRID).all()
+
+
+@pytest.mark.parametrize("S,n,holes,zero", [
+    (1, 200, 0.0, 0.1), (2, 512, 0.1, 0.0), (5, 128, 0.2, 0.1), (4, 129, 0.0, 0.0),
+    (3, 300, 0.3, 0.2), (16, 256, 0.05, 0.05), (40, 97, 0.1, 0.1),
+])
+def test_grid_pass_shapes(S, n, holes, zero):
+    """Shapes served by the grid-cooperative pass (64 < n <= 512): one
+    ragged or full column block per workgroup, one to many stages."""
+    batch = W.random_small(3, S, n, seed=23, cap_hi=6, cost_hi=400, supply_hi=3 * n,
+                           holes=holes, zero_cap=zero)
+    say("grid pass", S, n)
+    g = gpu_solve(batch)
+    compare(batch, g, oracle.solve(batch))
+    assert (g["passes"] == mcf.GWTF_PASS_GRID).all()
+
+
+def test_grid_pass_routing_and_status():
+    """At n = 512 a workgroup's LDS holds about 1400 flow-list slots: an
+    instance with capacities of 64 reserves 128 * 64 and moves to the global
+    pass, as does one with a link cost above 16 bits; bad input and label
+    overflow are reported by the grid pass itself."""
+    batch = W.random_small(6, 3, 512, seed=29, cap_hi=8, cost_hi=900, supply_hi=600, holes=0.05,
+                           zero_cap=0.05)
+    batch.node_cap[1] = 64
+    batch.supply[1] = 600
+    batch.arc_cost[2, 1, 7, 9] = 70000
+    batch.node_cap[3, 2, 5] = -1
+    batch.node_cost[4, 0, 3] = 2 ** 28
+    say("grid routing")
+    g = gpu_solve(batch)
+    assert g["status"].tolist() == [0, 0, 0, 1, 2, 0]
+    assert g["passes"].tolist() == [3, 4, 4, 3, 3, 3]
+    assert (g["F"][3:5] == 0).all() and (g["cost"][3:5] == 0).all()
+    keep = [0, 1, 2, 5]
+    ref = oracle.solve(batch.subset(keep))
+    assert (g["F"][keep] == ref["F"]).all() and (g["cost"][keep] == ref["cost"]).all()
+    for b in keep:
+        C.certify(batch, b, int(g["F"][b]), int(g["cost"][b]), g["node_flow"][b], g["arc_flow"][b],
+                  g["src_flow"][b], g["snk_flow"][b], g["potential"][b])
 
 
 def test_lists_outgrow_lds_use_fallback():
@@ -230,7 +273,7 @@ def test_config5_full_against_stored_oracle():
     assert _digest(batch) == gold["input_sha256"], "generator no longer reproduces the stored inputs"
     say("c5 (about a minute)")
     g = gpu_solve(batch)
-    assert g["status"][0] == 0
+    assert g["status"][0] == 0 and g["passes"][0] == mcf.GWTF_PASS_GRID
     assert int(g["F"][0]) == gold["F"][0] == C.closed_form_value(batch, 0)
     assert int(g["cost"][0]) == gold["cost"][0]
     C.certify(batch, 0, int(g["F"][0]), int(g["cost"][0]), g["node_flow"][0], g["arc_flow"][0],
