@@ -62,6 +62,23 @@ def measured_traffic(config: int, kernel_s: float):
     return rec["traffic_bytes_per_launch"] / kernel_s / 1e9
 
 
+KERNELS = {1: "solve_reg_kernel", 2: "solve_kernel (LDS state)", 3: "solve_grid_kernel",
+           4: "solve_kernel (global-memory state)"}
+
+
+def stored_oracle_baseline(config: int):
+    """The oracle's time on a workload too long to re-run inside a bench
+    (one instance of c5 takes about 16 minutes on one core), as recorded when
+    its stored optimum was produced."""
+    path = os.path.join(ROOT, "tests", "golden", f"c{config}_oracle.json")
+    rec = json.load(open(path))
+    return {"value": rec["B"] / rec["oracle_seconds"], "unit": "instances/s",
+            "cores": rec["oracle_threads"], "kind": "oracle",
+            "sample": f"all {rec['B']} instance(s), {rec['oracle_seconds']:.0f} s on "
+                      f"{rec['oracle_threads']} thread(s), timed when tests/golden/c{config}_oracle.json "
+                      f"was written (not re-run by this bench)"}
+
+
 def cpu_baseline(batch, budget_s: float, threads: int):
     """The oracle on the host cores, on a bounded prefix of the workload."""
     import numpy as np
@@ -151,6 +168,8 @@ def main():
     if (status != 0).any():
         raise SystemExit(f"solver reported non-ok status on {(status != 0).sum()} instances")
     stats = solver.stats().cpu().numpy()
+    passes = solver.passes().cpu().numpy()
+    main_pass = int(np.bincount(passes).argmax())
     rows, pulls = int(stats[:, 2].sum()), int(stats[:, 3].sum())
     dense_relax = rows * batch.n
     relax = dense_relax + pulls
@@ -178,10 +197,14 @@ def main():
             "backward": float(stats[:, 9].sum() / max(1, stats[:, 0].sum()))},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(args.config, kernel_s),
-                     "kernel": "solve_kernel (one launch per step)",
+                     "kernel": KERNELS.get(main_pass, "?") +
+                     (" (one launch per step)" if main_pass != 3 else " (one cooperative launch per instance)"),
+                     "instances_per_pass": {KERNELS[p]: int((passes == p).sum()) for p in np.unique(passes)},
                      "kernel_ms": kernel_s * 1e3},
     }
-    if args.cpu_budget > 0:
+    if args.cpu_budget > 0 and args.config == 5:
+        line["cpu_baseline"] = stored_oracle_baseline(args.config)
+    elif args.cpu_budget > 0:
         threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
         threads = max(1, min(threads, os.cpu_count() or 1))
         line["cpu_baseline"] = cpu_baseline(batch, args.cpu_budget, threads)

@@ -31,8 +31,8 @@ struct gwtf_mcf {
     bool grid = false;
     int64_t grid_slots = 0;
     size_t grid_lds = 0;
-    int32_t *g_ex = nullptr, *g_en = nullptr, *g_path = nullptr, *g_path_j = nullptr, *g_ctrl = nullptr;
-    int16_t *g_pred = nullptr;
+    int32_t *g_ex = nullptr, *g_en = nullptr, *g_pred = nullptr, *g_path = nullptr, *g_path_j = nullptr,
+            *g_ctrl = nullptr;
     int32_t solved = 0; // batch size of the last successful solve (0 = none)
 };
 
@@ -97,8 +97,7 @@ void free_ws(gwtf_mcf_t *h)
     h->route = h->node_flow = h->arc_flow = h->pot = nullptr;
     h->stats = nullptr;
     h->state = nullptr;
-    h->g_ex = h->g_en = h->g_path = h->g_path_j = h->g_ctrl = nullptr;
-    h->g_pred = nullptr;
+    h->g_ex = h->g_en = h->g_pred = h->g_path = h->g_path_j = h->g_ctrl = nullptr;
 }
 
 } // namespace
@@ -175,7 +174,7 @@ extern "C" gwtf_status_t gwtf_mcf_create(const gwtf_mcf_shape_t *shape, void *hi
         {(void **)&h->state, h->state_stride * B},
         {(void **)&h->g_ex, sizeof(int32_t) * 2 * gsn},
         {(void **)&h->g_en, sizeof(int32_t) * 2 * gsn},
-        {(void **)&h->g_pred, 16 * ((2 * gsn + 7) / 8)},
+        {(void **)&h->g_pred, sizeof(int32_t) * gsn},
         {(void **)&h->g_path, sizeof(int32_t) * (2 * gsn + 8)},
         {(void **)&h->g_path_j, sizeof(int32_t) * (2 * gsn + 8)},
         {(void **)&h->g_ctrl, sizeof(int32_t) * kGridCtrlInts},

@@ -114,7 +114,7 @@ struct GridParams {
     int64_t list_slots; // flow-list capacity of one workgroup
     size_t big_bytes;   // leading LDS area: link-cost block or staged predecessors
     int32_t *ex, *en;   // [2][S*n] exit / entry labels, double-buffered by iteration
-    int16_t *pred;      // [2*S*n rounded up to 8]: entry predecessors, then exit ones
+    int32_t *pred;      // [S*n] entry predecessor (low 16 bits) and exit predecessor (high)
     int32_t *path;      // [2*S*n + 8] arc codes of the augmenting path
     int32_t *path_j;    // [2*S*n + 8] head node of each link arc on the path
     int32_t *ctrl;      // [kGridCtrlInts], cleared before each launch

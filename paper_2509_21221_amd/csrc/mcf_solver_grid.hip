@@ -22,10 +22,16 @@
 //    predecessors in its LDS, walks the augmenting path and finds its
 //    bottleneck; each owner then applies the path to its nodes and lists.
 //
-// The grid barrier is an arrival counter plus a generation word updated with
-// device-scope atomics.  Its wait is bounded: a barrier that does not complete
-// within the bound ends the solve with the internal-error status instead of
-// hanging the device.
+// Memory ordering.  The L2 cache is private to each XCD, so every value one
+// workgroup writes for another (labels, predecessors, path, flows, control
+// words) moves through device-scope atomic loads and stores, which bypass
+// the non-coherent cache state, and no cache-wide write-back or invalidate is
+// needed: before a workgroup arrives at the grid barrier, each of its threads
+// waits for its own stores to complete.  The barrier itself is one arrival
+// counter and one epoch word; it also ORs a one-bit flag over the grid (used
+// for "some label changed"), and its wait is bounded: a barrier that does not
+// complete within the bound ends the solve with the internal-error status
+// instead of hanging the device.
 #include "mcf_device.h"
 
 namespace gwtf {
@@ -48,10 +54,9 @@ enum : int { kFlagBad = 1, kFlagWide = 2, kFlagLists = 4, kFlagFault = 8 };
 enum : int {
     kCtlFlags = 0,
     kCtlMaxCost = 1,
-    kCtlBarCount = 2,
-    kCtlBarGen = 3,
-    kCtlChanged = 4, // [3]
-    kCtlDtKey = 8,   // 3 x uint64
+    kCtlBarCount = 2, // arrivals in the low 16 bits, raised flags above
+    kCtlBarWord = 3,  // epoch << 1 | OR of the last barrier's flags
+    kCtlDtKey = 8,    // 3 x uint64, rotating per iteration
     kCtlDelta = 16,
     kCtlLen = 17,
     kCtlRelax = 20, // uint64
@@ -65,33 +70,42 @@ __device__ __forceinline__ uint64_t pack_key(int label, int idx)
 }
 __device__ __forceinline__ int key_label(uint64_t key) { return int(uint32_t(key >> 32)) - kBias; }
 
-__device__ __forceinline__ int load_acq(const int *p)
+// Device-coherent accesses for data shared between workgroups.
+template <typename T> __device__ __forceinline__ T ld(const T *p)
 {
-    return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+    return __hip_atomic_load(const_cast<T *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ unsigned long long load_acq_u64(const unsigned long long *p)
+template <typename T> __device__ __forceinline__ void st(T *p, T v)
 {
-    return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+// Wait until this thread's outstanding global accesses have completed.
+__device__ __forceinline__ void drain() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
-// Grid barrier; the call returns the same value in every thread of a block.
+// Grid barrier.  sync() returns false if the barrier did not complete within
+// the spin bound; *flag_lds receives the OR of the flags the workgroups
+// passed.  Both are the same in every thread of a workgroup.
 struct GridBarrier {
-    unsigned *count, *gen;
-    unsigned nblocks, local_gen;
+    unsigned *count, *word;
+    unsigned nblocks, epoch;
 
-    __device__ bool sync(int *ok_lds)
+    __device__ bool sync(bool raise, int *ok_lds, int *flag_lds)
     {
+        drain();
         __syncthreads();
         if (threadIdx.x == 0) {
-            __threadfence();
-            const unsigned g = local_gen;
+            const unsigned mine = raise ? 0x10001u : 1u;
+            const unsigned total = atomicAdd(count, mine) + mine;
             bool good = true;
-            if (atomicAdd(count, 1u) + 1u == nblocks) {
-                __hip_atomic_store(count, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                __hip_atomic_fetch_add(gen, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+            unsigned w;
+            if ((total & 0xffffu) == nblocks) {
+                st(count, 0u);
+                drain();
+                w = ((epoch + 1u) << 1) | unsigned((total >> 16) != 0);
+                st(word, w);
             } else {
                 int spins = 0;
-                while (__hip_atomic_load(gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == g) {
+                while (((w = ld(word)) >> 1) == epoch) {
                     if (++spins > kSpinLimit) {
                         good = false;
                         break;
@@ -99,13 +113,14 @@ struct GridBarrier {
                     __builtin_amdgcn_s_sleep(1);
                 }
             }
-            __threadfence();
-            local_gen = g + 1u;
+            epoch += 1u;
             *ok_lds = good;
+            *flag_lds = int(w & 1u);
         }
         __syncthreads();
         return *ok_lds != 0;
     }
+    __device__ bool sync(int *ok_lds, int *flag_lds) { return sync(false, ok_lds, flag_lds); }
 };
 
 __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams gp)
@@ -120,7 +135,7 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
     const bool has_prev = k >= 1, has_next = k + 1 < S;
 
     extern __shared__ __align__(16) unsigned char smem[];
-    __shared__ int sh_ok, sh_bad, sh_maxc, sh_changed, sh_len, sh_delta, sh_fault;
+    __shared__ int sh_ok, sh_flag, sh_bad, sh_maxc, sh_changed, sh_len, sh_delta, sh_fault;
     __shared__ unsigned long long sh_key;
     __shared__ int wcnt[kGridWaves];
 
@@ -128,7 +143,7 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
     // The leading area holds the link-cost block; workgroup 0 (no incoming
     // links) uses it for the staged predecessors instead.
     uint16_t *cost16 = reinterpret_cast<uint16_t *>(smem);
-    int16_t *all_pred = reinterpret_cast<int16_t *>(smem); // [2*SN]: entries, then exits
+    int *all_pred = reinterpret_cast<int *>(smem); // [SN]: entry pred low 16 bits, exit pred high
     size_t o = align16(gp.big_bytes);
     auto take = [&](size_t bytes) {
         unsigned char *at = smem + o;
@@ -157,11 +172,10 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
     int *scanbuf = reinterpret_cast<int *>(red); // ingest only; red holds >= kGridThreads ints
 
     int *ctrl = gp.ctrl;
-    int *changed = ctrl + kCtlChanged;
     unsigned long long *dtkey = reinterpret_cast<unsigned long long *>(ctrl + kCtlDtKey);
-    GridBarrier bar{reinterpret_cast<unsigned *>(ctrl + kCtlBarCount), reinterpret_cast<unsigned *>(ctrl + kCtlBarGen),
+    GridBarrier bar{reinterpret_cast<unsigned *>(ctrl + kCtlBarCount), reinterpret_cast<unsigned *>(ctrl + kCtlBarWord),
                     gridDim.x, 0u};
-    if (tid == 0) bar.local_gen = __hip_atomic_load(bar.gen, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (tid == 0) bar.epoch = ld(bar.word) >> 1;
 
     const int32_t *gcap = p.cap + size_t(b) * SN;
     const int32_t *gnc = p.ncost + size_t(b) * SN;
@@ -196,7 +210,7 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
         flow[c] = 0;
         pout[c] = 0;
         if (own) {
-            gnf[q] = 0;
+            st(&gnf[q], 0);
             gpot[3 + 2 * q] = 0;
             gpot[4 + 2 * q] = 0;
         }
@@ -214,7 +228,7 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
     }
     if (has_next) {
         int32_t *rows = gaf + size_t(k) * n * n + size_t(j0) * n;
-        for (int e = tid; e < nown * n; e += kGridThreads) rows[e] = 0;
+        for (int e = tid; e < nown * n; e += kGridThreads) st(&rows[e], 0);
     }
     if (g == 0 && tid < 3) gpot[tid] = 0;
     if (bad) atomicOr(&sh_bad, 1);
@@ -237,10 +251,10 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
         if (f) atomicOr(&ctrl[kCtlFlags], f);
         atomicMax(&ctrl[kCtlMaxCost], sh_maxc);
     }
-    bool timed_out = !bar.sync(&sh_ok);
+    bool timed_out = !bar.sync(&sh_ok, &sh_flag);
     int status = 0;
     if (!timed_out) {
-        const int fl0 = load_acq(&ctrl[kCtlFlags]), maxc = load_acq(&ctrl[kCtlMaxCost]);
+        const int fl0 = ld(&ctrl[kCtlFlags]), maxc = ld(&ctrl[kCtlMaxCost]);
         if (fl0 & kFlagBad) status = 1;
         else if (int64_t(V) * maxc >= kLabelBound) status = 2;
         if (status == 0 && (fl0 & (kFlagWide | kFlagLists))) {
@@ -264,20 +278,17 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
             prin[c] = k == 0 ? kPredSrc : kPredNone;
             prout[c] = kPredNone;
             if (c < nown) {
-                gp.ex[q] = kInf;
-                gp.en[q] = d0;
+                st(&gp.ex[q], kInf);
+                st(&gp.en[q], d0);
             }
         }
         for (int i = tid; i < n; i += kGridThreads) exrow[i] = kInf;
-        if (g == 0 && tid < 3) {
-            changed[tid] = 0;
-            dtkey[tid] = ~0ull;
-        }
+        if (g == 0 && tid < 3) st(&dtkey[tid], ~0ull);
     };
 
     if (!timed_out && status == 0 && supply > 0) {
         reset_labels();
-        timed_out = !bar.sync(&sh_ok);
+        timed_out = !bar.sync(&sh_ok, &sh_flag);
         while (!timed_out) {
             // ---- (1) Jacobi label-correcting iteration ----
             uint64_t final_key = ~0ull;
@@ -290,11 +301,11 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
                 int dropped = 0;
                 if (tid < n) {
                     if (has_prev) {
-                        const int d = ex_in[(k - 1) * n + tid];
+                        const int d = ld(&ex_in[(k - 1) * n + tid]);
                         dropped = d < exrow[tid];
                         if (dropped) exrow[tid] = d;
                     }
-                    if (has_next) enrow[tid] = en_in[(k + 1) * n + tid];
+                    if (has_next) enrow[tid] = ld(&en_in[(k + 1) * n + tid]);
                 }
                 const uint64_t m = __ballot(dropped);
                 if (lane == 0) wcnt[wave] = __popcll(m);
@@ -367,32 +378,28 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
                     dout[c] = dq;
                     prin[c] = pi;
                     prout[c] = po;
-                    ex_out[q] = dq;
-                    en_out[q] = di;
+                    st(&ex_out[q], dq);
+                    st(&en_out[q], di);
                     if ((di != di0) | (dq != dq0)) sh_changed = 1;
                     if (k == S - 1 && dq < kInf) atomicMin(&sh_key, (unsigned long long)pack_key(dq + snkc[c], j0 + c));
                 }
                 __syncthreads();
                 if (tid == 0) {
-                    if (sh_changed) atomicAdd(&changed[t % 3], 1);
                     if (sh_key != ~0ull) atomicMin(&dtkey[t % 3], sh_key);
                     sh_key = ~0ull;
                     my_relax += (long long)nrows * nown;
                 }
                 rounds++;
-                if (!bar.sync(&sh_ok)) {
+                if (!bar.sync(sh_changed != 0, &sh_ok, &sh_flag)) {
                     timed_out = true;
                     break;
                 }
-                if (g == 0 && tid == 0) {
-                    changed[(t + 2) % 3] = 0;
-                    dtkey[(t + 2) % 3] = ~0ull;
-                }
-                if (load_acq(&changed[t % 3]) == 0) {
-                    final_key = load_acq_u64(&dtkey[t % 3]);
+                if (!sh_flag) { // no label changed anywhere: converged
+                    final_key = ld(&dtkey[t % 3]);
                     converged = true;
                     break;
                 }
+                if (g == 0 && tid == 0) st(&dtkey[(t + 2) % 3], ~0ull);
             }
             if (timed_out) break;
             if (!converged) {
@@ -408,20 +415,16 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
                 const int c = tid, q = k * n + j0 + c;
                 pout[c] = min(dout[c], pout[c] + dred);
                 gpot[3 + 2 * q] = min(din[c], gpot[3 + 2 * q] + dred);
-                gp.pred[q] = int16_t(prin[c]);
-                gp.pred[SN + q] = int16_t(prout[c]);
+                st(&gp.pred[q], (prin[c] & 0xffff) | (prout[c] << 16));
             }
-            if (!bar.sync(&sh_ok)) {
+            if (!bar.sync(&sh_ok, &sh_flag)) {
                 timed_out = true;
                 break;
             }
 
             // ---- (3) workgroup 0: walk the path, find the bottleneck ----
             if (g == 0) {
-                const int n4 = (2 * SN + 7) / 8;
-                const int4 *src4 = reinterpret_cast<const int4 *>(gp.pred);
-                int4 *dst4 = reinterpret_cast<int4 *>(smem);
-                for (int x = tid; x < n4; x += kGridThreads) dst4[x] = src4[x];
+                for (int q = tid; q < SN; q += kGridThreads) all_pred[q] = ld(&gp.pred[q]);
                 __syncthreads();
                 if (tid == 0) {
                     int kk = S - 1, i = predt, len = 0;
@@ -436,11 +439,11 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
                         // link's stage and row) and keep the head in path_j.
                         int code, ak = kk, ai = i, j = 0;
                         if (at_exit) {
-                            const int pr = all_pred[SN + kk * n + i];
+                            const int pr = all_pred[kk * n + i] >> 16;
                             if (pr == kPredSplit) {
                                 code = kArcSplitFwd; // entry -> exit of (kk, i)
                                 at_exit = false;
-                            } else if (pr >= 0 && kk + 1 < S) {
+                            } else if (pr >= 0 && pr < n && kk + 1 < S) {
                                 code = kArcLinkRev; // entry (kk+1, pr) -> exit (kk, i)
                                 j = pr;
                                 kk = kk + 1;
@@ -451,12 +454,12 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
                                 break;
                             }
                         } else {
-                            const int pr = all_pred[kk * n + i];
+                            const int pr = int(int16_t(all_pred[kk * n + i] & 0xffff));
                             if (pr == kPredSrc) break;
                             if (pr == kPredSplit) {
                                 code = kArcSplitRev; // exit -> entry of (kk, i)
                                 at_exit = true;
-                            } else if (pr >= 0 && kk >= 1) {
+                            } else if (pr >= 0 && pr < n && kk >= 1) {
                                 code = kArcLinkFwd; // exit (kk-1, pr) -> entry (kk, i)
                                 ak = kk - 1;
                                 ai = pr;
@@ -469,8 +472,8 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
                                 break;
                             }
                         }
-                        gp.path[len] = code | (ak << 2) | (ai << 12);
-                        gp.path_j[len] = j;
+                        st(&gp.path[len], code | (ak << 2) | (ai << 12));
+                        st(&gp.path_j[len], j);
                         ++len;
                     }
                     sh_len = okw ? len : -1;
@@ -481,40 +484,44 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
                 if (len >= 0) {
                     int r = 0x7fffffff;
                     for (int e = tid; e < len; e += kGridThreads) {
-                        const int code = gp.path[e], type = code & 3, ak = (code >> 2) & 1023, ai = code >> 12;
+                        const int code = ld(&gp.path[e]), type = code & 3, ak = (code >> 2) & 1023, ai = code >> 12;
                         const int q = ak * n + ai;
-                        if (type == kArcSplitFwd) r = min(r, gcap[q] - gnf[q]);
-                        else if (type == kArcSplitRev) r = min(r, gnf[q]);
-                        else if (type == kArcLinkRev) r = min(r, gaf[size_t(q) * n + gp.path_j[e]]);
+                        if (type == kArcSplitFwd) r = min(r, gcap[q] - ld(&gnf[q]));
+                        else if (type == kArcSplitRev) r = min(r, ld(&gnf[q]));
+                        else if (type == kArcLinkRev) r = min(r, ld(&gaf[size_t(q) * n + ld(&gp.path_j[e])]));
                     }
                     atomicMin(&sh_delta, r);
                 }
                 __syncthreads();
                 if (tid == 0) {
-                    ctrl[kCtlDelta] = len < 0 ? -1 : sh_delta;
-                    ctrl[kCtlLen] = len;
+                    st(&ctrl[kCtlDelta], len < 0 ? -1 : sh_delta);
+                    st(&ctrl[kCtlLen], len);
                 }
             }
-            if (!bar.sync(&sh_ok)) {
+            if (!bar.sync(&sh_ok, &sh_flag)) {
                 timed_out = true;
                 break;
             }
 
             // ---- (4) owners apply the augmentation: decrements, then increments ----
-            const int delta = load_acq(&ctrl[kCtlDelta]), len = load_acq(&ctrl[kCtlLen]);
-            if (delta <= 0 || len < 0) {
+            const int delta = ld(&ctrl[kCtlDelta]), len = ld(&ctrl[kCtlLen]);
+            if (delta <= 0 || len < 0 || len > 2 * SN + 5) {
                 if (tid == 0) sh_fault = 1;
                 break;
             }
             for (int pass = 0; pass < 2; ++pass) {
                 for (int e = tid; e < len; e += kGridThreads) {
-                    const int code = gp.path[e], type = code & 3, ak = (code >> 2) & 1023, ai = code >> 12;
+                    const int code = ld(&gp.path[e]), type = code & 3, ak = (code >> 2) & 1023, ai = code >> 12;
                     if (ak != k || ai < j0 || ai >= j0 + nown) continue;
-                    const int c = ai - j0, q = ak * n + ai, j = gp.path_j[e];
+                    const int c = ai - j0, q = ak * n + ai, j = ld(&gp.path_j[e]);
+                    if (unsigned(j) >= unsigned(n)) {
+                        sh_fault = 1;
+                        continue;
+                    }
                     if (pass == 0) {
                         if (type == kArcSplitFwd || type == kArcSplitRev) {
                             flow[c] += type == kArcSplitFwd ? delta : -delta;
-                            gnf[q] = flow[c];
+                            st(&gnf[q], flow[c]);
                         } else if (type == kArcLinkRev) {
                             const int lo = loff[c], hi = lo + llen[c];
                             int le = -1;
@@ -524,23 +531,26 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
                                 sh_fault = 1;
                                 continue;
                             }
-                            if (lamt[le] == delta) { // the arc empties: move the last entry here
+                            const int left = lamt[le] - delta;
+                            if (left == 0) { // the arc empties: move the last entry here
                                 lpart[le] = lpart[hi - 1];
                                 lamt[le] = lamt[hi - 1];
                                 lcost[le] = lcost[hi - 1];
                                 llen[c] = hi - 1 - lo;
                             } else {
-                                lamt[le] -= delta;
+                                lamt[le] = left;
                             }
-                            gaf[size_t(q) * n + j] -= delta;
+                            st(&gaf[size_t(q) * n + j], left);
                         }
                     } else if (type == kArcLinkFwd) {
                         const int lo = loff[c], hi = lo + llen[c];
                         int le = -1;
                         for (int x = lo; x < hi; ++x)
                             if (lpart[x] == j) le = x;
+                        int now = delta;
                         if (le >= 0) {
-                            lamt[le] += delta;
+                            now = lamt[le] + delta;
+                            lamt[le] = now;
                         } else if (hi - lo >= min(min(cap[c], n), supply)) {
                             sh_fault = 1;
                             continue;
@@ -550,7 +560,7 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
                             lcost[hi] = gac[size_t(q) * n + j];
                             llen[c] = hi + 1 - lo;
                         }
-                        gaf[size_t(q) * n + j] += delta;
+                        st(&gaf[size_t(q) * n + j], now);
                     }
                 }
                 __syncthreads();
@@ -559,14 +569,14 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
             cost += (long long)delta * Dt;
             augs++;
             pit = Dt;
-            if (tid == 0 && sh_fault) atomicOr(&ctrl[kCtlFlags], kFlagFault);
             if (F >= supply) break;
             reset_labels();
-            if (!bar.sync(&sh_ok)) {
+            // the barrier's flag reports a fault seen by any workgroup
+            if (!bar.sync(sh_fault != 0, &sh_ok, &sh_flag)) {
                 timed_out = true;
                 break;
             }
-            if (load_acq(&ctrl[kCtlFlags]) & kFlagFault) break; // every workgroup reads the same word
+            if (sh_flag) break;
         }
     }
 
@@ -578,7 +588,7 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
     if (my_pulls) atomicAdd(reinterpret_cast<unsigned long long *>(ctrl + kCtlPulls), (unsigned long long)my_pulls);
     // A barrier that times out here still ends the kernel; the workgroup
     // then reports a fault.
-    const bool fault = !bar.sync(&sh_ok) || (load_acq(&ctrl[kCtlFlags]) & kFlagFault) || timed_out;
+    const bool fault = !bar.sync(&sh_ok, &sh_flag) || (ld(&ctrl[kCtlFlags]) & kFlagFault) || timed_out;
     const bool ok = status == 0 && !fault;
     if (tid < nown) {
         const int q = k * n + j0 + tid;
@@ -598,12 +608,12 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
         p.cost_out[b] = ok ? cost : 0;
         p.status_out[b] = status != 0 ? status : (fault ? kStatusInternal : 0);
         p.route[b] = kRouteGrid;
-        int64_t *st = p.stats + size_t(b) * kStatsPerInstance;
-        st[0] = augs;
-        st[1] = rounds;
-        st[2] = int64_t(load_acq_u64(reinterpret_cast<unsigned long long *>(ctrl + kCtlRelax)) / uint64_t(n));
-        st[3] = int64_t(load_acq_u64(reinterpret_cast<unsigned long long *>(ctrl + kCtlPulls)));
-        for (int x = 4; x < kStatsPerInstance; ++x) st[x] = 0;
+        int64_t *stats = p.stats + size_t(b) * kStatsPerInstance;
+        stats[0] = augs;
+        stats[1] = rounds;
+        stats[2] = int64_t(ld(reinterpret_cast<unsigned long long *>(ctrl + kCtlRelax)) / uint64_t(n));
+        stats[3] = int64_t(ld(reinterpret_cast<unsigned long long *>(ctrl + kCtlPulls)));
+        for (int x = 4; x < kStatsPerInstance; ++x) stats[x] = 0;
     }
 }
 
@@ -623,11 +633,7 @@ size_t lds_fixed(int S, int n)
 
 } // namespace
 
-size_t grid_pass_big_bytes(int S, int n)
-{
-    const size_t preds = size_t((2 * int64_t(S) * n + 7) / 8) * 16;
-    return std::max(size_t(n) * kGridNB * 2, preds);
-}
+size_t grid_pass_big_bytes(int S, int n) { return std::max(size_t(n) * kGridNB * 2, size_t(4) * S * n); }
 
 size_t grid_pass_lds_bytes(int S, int n, int64_t list_slots)
 {
