@@ -31,8 +31,9 @@ struct gwtf_mcf {
     bool grid = false;
     int64_t grid_slots = 0;
     size_t grid_lds = 0;
-    int32_t *g_ex = nullptr, *g_en = nullptr, *g_pred = nullptr, *g_path = nullptr, *g_path_j = nullptr,
-            *g_ctrl = nullptr;
+    uint32_t *g_ex = nullptr, *g_en = nullptr, *g_ring = nullptr;
+    unsigned long long *g_ring_key = nullptr;
+    int32_t *g_pred = nullptr, *g_path = nullptr, *g_path_j = nullptr, *g_ctrl = nullptr;
     int32_t solved = 0; // batch size of the last successful solve (0 = none)
 };
 
@@ -94,10 +95,14 @@ void free_ws(gwtf_mcf_t *h)
     (void)hipFree(h->g_path);
     (void)hipFree(h->g_path_j);
     (void)hipFree(h->g_ctrl);
+    (void)hipFree(h->g_ring);
+    (void)hipFree(h->g_ring_key);
     h->route = h->node_flow = h->arc_flow = h->pot = nullptr;
     h->stats = nullptr;
     h->state = nullptr;
-    h->g_ex = h->g_en = h->g_pred = h->g_path = h->g_path_j = h->g_ctrl = nullptr;
+    h->g_ex = h->g_en = h->g_ring = nullptr;
+    h->g_ring_key = nullptr;
+    h->g_pred = h->g_path = h->g_path_j = h->g_ctrl = nullptr;
 }
 
 } // namespace
@@ -172,12 +177,14 @@ extern "C" gwtf_status_t gwtf_mcf_create(const gwtf_mcf_shape_t *shape, void *hi
         {(void **)&h->pot, sizeof(int32_t) * V * B},
         {(void **)&h->stats, sizeof(int64_t) * kStatsPerInstance * B},
         {(void **)&h->state, h->state_stride * B},
-        {(void **)&h->g_ex, sizeof(int32_t) * 2 * gsn},
-        {(void **)&h->g_en, sizeof(int32_t) * 2 * gsn},
+        {(void **)&h->g_ex, sizeof(uint32_t) * 2 * gsn},
+        {(void **)&h->g_en, sizeof(uint32_t) * 2 * gsn},
         {(void **)&h->g_pred, sizeof(int32_t) * gsn},
         {(void **)&h->g_path, sizeof(int32_t) * (2 * gsn + 8)},
         {(void **)&h->g_path_j, sizeof(int32_t) * (2 * gsn + 8)},
         {(void **)&h->g_ctrl, sizeof(int32_t) * kGridCtrlInts},
+        {(void **)&h->g_ring, h->grid ? sizeof(uint32_t) * grid_ring_slots(S) : 0},
+        {(void **)&h->g_ring_key, h->grid ? sizeof(unsigned long long) * grid_ring_slots(S) : 0},
     };
     for (auto &a : allocs) {
         if (a.bytes == 0) continue;
@@ -252,6 +259,9 @@ extern "C" gwtf_status_t gwtf_mcf_solve_batch(gwtf_mcf_t *h, const gwtf_mcf_batc
         gp.path = h->g_path;
         gp.path_j = h->g_path_j;
         gp.ctrl = h->g_ctrl;
+        gp.ring = h->g_ring;
+        gp.ring_key = h->g_ring_key;
+        gp.ring_slots = grid_ring_slots(S);
         for (int i = 0; i < b->batch; ++i) {
             gp.instance = i;
             if ((e = launch_grid_pass(gp, h->grid_lds, h->stream)) != hipSuccess)

@@ -46,6 +46,10 @@ constexpr int kGridRowGroups = kGridThreads / kGridNB; // rows split over 4 grou
 constexpr uint16_t kNoArc16 = 0xffff;
 constexpr int kBias = 1 << 30;
 constexpr int kSpinLimit = 1 << 20;
+// Packed relaxation keys: label << 9 | row (n <= 512), valid while every
+// label fed in stays below kPackLimit so that label + cost keeps 22 bits.
+constexpr uint32_t kPackLimit = (1u << 22) - (1u << 16);
+constexpr uint32_t kNoRowKey = 0xfe000000u; // row without a new label; + cost << 9 cannot wrap
 
 enum : int { kArcSplitFwd = 0, kArcSplitRev = 1, kArcLinkFwd = 2, kArcLinkRev = 3 };
 // grid-wide status bits
@@ -56,13 +60,14 @@ enum : int {
     kCtlMaxCost = 1,
     kCtlBarCount = 2, // arrivals in the low 16 bits, raised flags above
     kCtlBarWord = 3,  // epoch << 1 | OR of the last barrier's flags
-    kCtlDtKey = 8,    // 3 x uint64, rotating per iteration
     kCtlDelta = 16,
     kCtlLen = 17,
-    kCtlRelax = 20, // uint64
-    kCtlPulls = 22, // uint64
+    kCtlStop = 18,     // iteration at which the search converged, 0 while it runs
+    kCtlRelax = 20,    // uint64
+    kCtlPulls = 22,    // uint64
+    kCtlFinalKey = 24, // uint64: sink label and exit of the converged search
 };
-static_assert(kCtlPulls + 2 <= kGridCtrlInts, "control block too small");
+static_assert(kCtlFinalKey + 2 <= kGridCtrlInts, "control block too small");
 
 __device__ __forceinline__ uint64_t pack_key(int label, int idx)
 {
@@ -135,9 +140,9 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
     const bool has_prev = k >= 1, has_next = k + 1 < S;
 
     extern __shared__ __align__(16) unsigned char smem[];
-    __shared__ int sh_ok, sh_flag, sh_bad, sh_maxc, sh_changed, sh_len, sh_delta, sh_fault;
+    __shared__ int sh_ok, sh_flag, sh_bad, sh_maxc, sh_changed, sh_len, sh_delta, sh_fault, sh_why[2];
     __shared__ unsigned long long sh_key;
-    __shared__ int wcnt[kGridWaves];
+    __shared__ int wcnt[kGridWaves], wmaxd[kGridWaves];
 
     // ---- LDS layout (same offsets in every workgroup) ----
     // The leading area holds the link-cost block; workgroup 0 (no incoming
@@ -153,6 +158,7 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
     int *exrow = reinterpret_cast<int *>(take(4 * size_t(n)));   // last seen exit labels of stage k-1
     int *enrow = reinterpret_cast<int *>(take(4 * size_t(n)));   // entry labels of stage k+1
     int *rowlist = reinterpret_cast<int *>(take(4 * size_t(n))); // rows of stage k-1 that dropped
+    uint32_t *rowkey = reinterpret_cast<uint32_t *>(take(4 * size_t(n))); // packed key per row
     int *din = reinterpret_cast<int *>(take(4 * kGridNB));
     int *dout = reinterpret_cast<int *>(take(4 * kGridNB));
     int *pout = reinterpret_cast<int *>(take(4 * kGridNB));
@@ -172,7 +178,7 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
     int *scanbuf = reinterpret_cast<int *>(red); // ingest only; red holds >= kGridThreads ints
 
     int *ctrl = gp.ctrl;
-    unsigned long long *dtkey = reinterpret_cast<unsigned long long *>(ctrl + kCtlDtKey);
+    unsigned long long *final_key_w = reinterpret_cast<unsigned long long *>(ctrl + kCtlFinalKey);
     GridBarrier bar{reinterpret_cast<unsigned *>(ctrl + kCtlBarCount), reinterpret_cast<unsigned *>(ctrl + kCtlBarWord),
                     gridDim.x, 0u};
     if (tid == 0) bar.epoch = ld(bar.word) >> 1;
@@ -190,6 +196,8 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
         sh_bad = supply < 0;
         sh_maxc = 0;
         sh_fault = 0;
+        sh_changed = 0;
+        sh_why[0] = sh_why[1] = 0;
         sh_key = ~0ull;
     }
     __syncthreads();
@@ -268,7 +276,9 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
     long long F = 0, cost = 0, rounds = 0, augs = 0, my_relax = 0, my_pulls = 0;
     int pit = 0;
 
-    // Labels of a fresh shortest-path search; buffer 0 holds its inputs.
+    // Labels of a fresh shortest-path search: buffer 0 holds them as the
+    // output of iteration 0; buffer 1 gets a tag no reader awaits before
+    // iteration 1 overwrites it.
     auto reset_labels = [&]() {
         if (tid < kGridNB) {
             const int c = tid, q = k * n + j0 + c;
@@ -278,61 +288,172 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
             prin[c] = k == 0 ? kPredSrc : kPredNone;
             prout[c] = kPredNone;
             if (c < nown) {
-                st(&gp.ex[q], kInf);
-                st(&gp.en[q], d0);
+                st(&gp.ex[q], uint32_t(kInf) << 2);
+                st(&gp.en[q], uint32_t(d0) << 2);
+                st(&gp.ex[SN + q], (uint32_t(kInf) << 2) | 3u);
+                st(&gp.en[SN + q], (uint32_t(kInf) << 2) | 3u);
             }
         }
         for (int i = tid; i < n; i += kGridThreads) exrow[i] = kInf;
-        if (g == 0 && tid < 3) st(&dtkey[tid], ~0ull);
+        if (g == 0) {
+            for (int r = tid; r < gp.ring_slots; r += kGridThreads) {
+                st(&gp.ring[r], 0u);
+                st(&gp.ring_key[r], ~0ull);
+            }
+            if (tid == 0) {
+                st(&ctrl[kCtlStop], 0);
+                st(final_key_w, ~0ull);
+            }
+        }
+        if (tid == 0) sh_why[0] = sh_why[1] = 0;
     };
 
     if (!timed_out && status == 0 && supply > 0) {
         reset_labels();
         timed_out = !bar.sync(&sh_ok, &sh_flag);
         while (!timed_out) {
-            // ---- (1) Jacobi label-correcting iteration ----
+            // ---- (1) label-correcting iterations, pipelined over the stages ----
+            // Iteration t of stage k relaxes from stage k-1's output of the
+            // same iteration (forward links: one wave carries a label through
+            // every stage) and stage k+1's output of iteration t-1 (reverse
+            // links).  Each published word carries a 2-bit iteration tag,
+            // (t >> 1) & 3, so a reader waits on the data itself: the buffer
+            // it reads holds either the awaited iteration or the one two
+            // before it, whose tag differs.
             uint64_t final_key = ~0ull;
             bool converged = false;
-            for (int t = 0; t < 4 * V + 8; ++t) {
-                const int *ex_in = gp.ex + size_t(t & 1) * SN;
-                const int *en_in = gp.en + size_t(t & 1) * SN;
-                int *ex_out = gp.ex + size_t((t + 1) & 1) * SN;
-                int *en_out = gp.en + size_t((t + 1) & 1) * SN;
-                int dropped = 0;
+            for (int t = 1; t <= 4 * V + 8; ++t) {
+                const uint32_t *ex_f = gp.ex + size_t(t & 1) * SN + size_t(has_prev ? k - 1 : 0) * n;
+                const uint32_t *en_b = gp.en + size_t((t - 1) & 1) * SN + size_t(has_next ? k + 1 : 0) * n;
+                uint32_t *ex_out = gp.ex + size_t(t & 1) * SN;
+                uint32_t *en_out = gp.en + size_t(t & 1) * SN;
+                const uint32_t tag_f = uint32_t(t >> 1) & 3u, tag_b = uint32_t((t - 1) >> 1) & 3u;
+                bool need_ex = has_prev && tid < n, need_en = has_next && tid < n;
+                uint32_t wex = 0, wen = 0;
+                int why = 0; // 1: the search has converged, 2: wait bound exceeded
+                for (int spins = 0;; ++spins) {
+                    const uint32_t a = need_ex ? ld(&ex_f[tid]) : 0u;
+                    const uint32_t c = need_en ? ld(&en_b[tid]) : 0u;
+                    const int stop = (tid == 0 || (spins & 15) == 15) ? ld(&ctrl[kCtlStop]) : 0;
+                    if (need_ex) {
+                        wex = a;
+                        need_ex = (a & 3u) != tag_f;
+                    }
+                    if (need_en) {
+                        wen = c;
+                        need_en = (c & 3u) != tag_b;
+                    }
+                    if (stop) {
+                        why = 1;
+                        break;
+                    }
+                    if (!(need_ex | need_en)) break;
+                    if (spins > kSpinLimit) {
+                        why = 2;
+                        break;
+                    }
+                    __builtin_amdgcn_s_sleep(1);
+                }
+                if (why) atomicOr(&sh_why[t & 1], why);
+                int dropped = 0, dnew = 0;
                 if (tid < n) {
                     if (has_prev) {
-                        const int d = ld(&ex_in[(k - 1) * n + tid]);
-                        dropped = d < exrow[tid];
-                        if (dropped) exrow[tid] = d;
+                        dnew = int(wex >> 2);
+                        dropped = dnew < exrow[tid];
+                        if (dropped) exrow[tid] = dnew;
+                        rowkey[tid] = dropped ? (uint32_t(dnew) << 9) | uint32_t(tid) : kNoRowKey;
                     }
-                    if (has_next) enrow[tid] = ld(&en_in[(k + 1) * n + tid]);
+                    if (has_next) enrow[tid] = int(wen >> 2);
                 }
                 const uint64_t m = __ballot(dropped);
-                if (lane == 0) wcnt[wave] = __popcll(m);
-                if (tid == 0) sh_changed = 0;
+                int wmax = dropped ? dnew : 0;
+#pragma unroll
+                for (int off = 32; off > 0; off >>= 1) wmax = max(wmax, __shfl_xor(wmax, off));
+                if (lane == 0) {
+                    wcnt[wave] = __popcll(m);
+                    wmaxd[wave] = wmax;
+                }
                 __syncthreads();
-                int base = 0, nrows = 0;
+                const int whyb = sh_why[t & 1];
+                if (whyb) { // a stop seen by any thread wins over a wait that ran out
+                    if (whyb & 1) converged = true;
+                    else timed_out = true;
+                    break;
+                }
+                if (tid == 0) sh_why[(t + 1) & 1] = 0;
+                int base = 0, nrows = 0, maxd = 0;
                 for (int w = 0; w < kGridWaves; ++w) {
                     const int cnt = wcnt[w];
                     base += w < wave ? cnt : 0;
                     nrows += cnt;
+                    maxd = max(maxd, wmaxd[w]);
                 }
-                if (dropped) rowlist[base + __popcll(m & ((1ull << lane) - 1ull))] = tid;
+                // Packed keys while labels allow; a stage where most rows
+                // dropped is swept densely by row index, otherwise through
+                // the compacted list (which then holds the packed keys).
+                const bool packed = uint32_t(maxd) < kPackLimit;
+                const bool dense = packed && 2 * nrows > n;
+                if (dropped) rowlist[base + __popcll(m & ((1ull << lane) - 1ull))] = packed ? int(rowkey[tid]) : tid;
                 __syncthreads();
 
                 // links into this block's entries, from the rows that dropped
                 uint64_t key = ~0ull;
-                if (col < nown) {
-                    int best = kInf, arg = -1;
-                    for (int e = rgrp; e < nrows; e += kGridRowGroups) {
-                        const int i = rowlist[e];
-                        const uint16_t c = cost16[i * kGridNB + col];
-                        const int cand = exrow[i] + int(c);
-                        const bool take_it = (c != kNoArc16) & (cand < best);
-                        best = take_it ? cand : best;
-                        arg = take_it ? i : arg;
+                if (col < nown && nrows > 0) {
+                    // this thread's share: a quarter of the rows (dense) or of the list
+                    const int span = dense ? n : nrows;
+                    const int chunk = (((span + kGridRowGroups - 1) / kGridRowGroups) + 3) & ~3;
+                    const int lo = min(span, rgrp * chunk), hi = min(span, lo + chunk);
+                    auto exact = [&]() {
+                        int best = kInf, arg = -1;
+                        for (int e = lo; e < hi; ++e) {
+                            int i;
+                            if (dense) {
+                                if (rowkey[e] == kNoRowKey) continue;
+                                i = e;
+                            } else {
+                                i = packed ? (rowlist[e] & 511) : rowlist[e];
+                            }
+                            const uint16_t c = cost16[i * kGridNB + col];
+                            const int cand = exrow[i] + int(c);
+                            const bool take_it = (c != kNoArc16) & (cand < best);
+                            best = take_it ? cand : best;
+                            arg = take_it ? i : arg;
+                        }
+                        return best < kInf ? pack_key(best, arg) : ~0ull;
+                    };
+                    if (packed) {
+                        uint32_t best = ~0u;
+                        const uint16_t *cc = cost16 + col;
+                        if (dense) {
+                            int e = lo;
+                            for (; e + 4 <= hi; e += 4) {
+                                const uint4 kq = *reinterpret_cast<const uint4 *>(&rowkey[e]);
+                                const uint32_t c0 = cc[(e + 0) * kGridNB], c1 = cc[(e + 1) * kGridNB];
+                                const uint32_t c2 = cc[(e + 2) * kGridNB], c3 = cc[(e + 3) * kGridNB];
+                                best = min(best, min((c0 << 9) + kq.x, (c1 << 9) + kq.y));
+                                best = min(best, min((c2 << 9) + kq.z, (c3 << 9) + kq.w));
+                            }
+                            for (; e < hi; ++e) best = min(best, (uint32_t(cc[e * kGridNB]) << 9) + rowkey[e]);
+                        } else {
+                            const uint32_t *kl = reinterpret_cast<const uint32_t *>(rowlist);
+                            int e = lo;
+                            for (; e + 4 <= hi; e += 4) {
+                                const uint4 kq = *reinterpret_cast<const uint4 *>(&kl[e]);
+                                const uint32_t c0 = cc[(kq.x & 511u) * kGridNB], c1 = cc[(kq.y & 511u) * kGridNB];
+                                const uint32_t c2 = cc[(kq.z & 511u) * kGridNB], c3 = cc[(kq.w & 511u) * kGridNB];
+                                best = min(best, min((c0 << 9) + kq.x, (c1 << 9) + kq.y));
+                                best = min(best, min((c2 << 9) + kq.z, (c3 << 9) + kq.w));
+                            }
+                            for (; e < hi; ++e) best = min(best, (uint32_t(cc[(kl[e] & 511u) * kGridNB]) << 9) + kl[e]);
+                        }
+                        if (best < kNoRowKey) {
+                            const int row = int(best & 511u);
+                            // a missing link reads as cost 65535; if one won, redo exactly
+                            key = cc[row * kGridNB] != kNoArc16 ? pack_key(int(best >> 9), row) : exact();
+                        }
+                    } else {
+                        key = exact();
                     }
-                    if (best < kInf) key = pack_key(best, arg);
                 }
                 red[rgrp * kGridNB + col] = key;
                 __syncthreads();
@@ -360,6 +481,7 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
                     }
                     if (has_next) {
                         const int lo = loff[c], hi = lo + llen[c];
+#pragma unroll 4
                         for (int e = lo; e < hi; ++e) {
                             const int j = lpart[e];
                             const int dj = enrow[j];
@@ -378,34 +500,45 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
                     dout[c] = dq;
                     prin[c] = pi;
                     prout[c] = po;
-                    st(&ex_out[q], dq);
-                    st(&en_out[q], di);
+                    st(&ex_out[q], (uint32_t(dq) << 2) | tag_f);
+                    st(&en_out[q], (uint32_t(di) << 2) | tag_f);
                     if ((di != di0) | (dq != dq0)) sh_changed = 1;
                     if (k == S - 1 && dq < kInf) atomicMin(&sh_key, (unsigned long long)pack_key(dq + snkc[c], j0 + c));
                 }
                 __syncthreads();
+                // Count this workgroup into iteration t.  The last one in
+                // learns whether any label changed; if none did, the labels
+                // are a fixed point and it publishes the sink's key and stop.
                 if (tid == 0) {
-                    if (sh_key != ~0ull) atomicMin(&dtkey[t % 3], sh_key);
+                    const int slot = t % gp.ring_slots;
+                    if (sh_key != ~0ull) {
+                        atomicMin(&gp.ring_key[slot], sh_key);
+                        drain();
+                    }
+                    const unsigned mine = sh_changed ? 0x10001u : 1u;
+                    const unsigned total = atomicAdd(&gp.ring[slot], mine) + mine;
+                    if ((total & 0xffffu) == gridDim.x) {
+                        if ((total >> 16) == 0) {
+                            st(final_key_w, ld(&gp.ring_key[slot]));
+                            drain();
+                            st(&ctrl[kCtlStop], t);
+                        } else {
+                            st(&gp.ring[slot], 0u);
+                            st(&gp.ring_key[slot], ~0ull);
+                        }
+                    }
                     sh_key = ~0ull;
+                    sh_changed = 0;
                     my_relax += (long long)nrows * nown;
                 }
-                rounds++;
-                if (!bar.sync(sh_changed != 0, &sh_ok, &sh_flag)) {
-                    timed_out = true;
-                    break;
-                }
-                if (!sh_flag) { // no label changed anywhere: converged
-                    final_key = ld(&dtkey[t % 3]);
-                    converged = true;
-                    break;
-                }
-                if (g == 0 && tid == 0) st(&dtkey[(t + 2) % 3], ~0ull);
             }
             if (timed_out) break;
             if (!converged) {
                 if (tid == 0) sh_fault = 1;
                 break;
             }
+            rounds += ld(&ctrl[kCtlStop]);
+            final_key = ld(final_key_w);
             if (final_key == ~0ull) break; // sink unreachable: the flow is maximum
 
             // ---- (2) potentials; publish predecessors ----
@@ -424,7 +557,18 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
 
             // ---- (3) workgroup 0: walk the path, find the bottleneck ----
             if (g == 0) {
-                for (int q = tid; q < SN; q += kGridThreads) all_pred[q] = ld(&gp.pred[q]);
+                {
+                    // eight loads in flight per thread
+                    int q = tid;
+                    for (; q + 7 * kGridThreads < SN; q += 8 * kGridThreads) {
+                        int v[8];
+#pragma unroll
+                        for (int u = 0; u < 8; ++u) v[u] = ld(&gp.pred[q + u * kGridThreads]);
+#pragma unroll
+                        for (int u = 0; u < 8; ++u) all_pred[q + u * kGridThreads] = v[u];
+                    }
+                    for (; q < SN; q += kGridThreads) all_pred[q] = ld(&gp.pred[q]);
+                }
                 __syncthreads();
                 if (tid == 0) {
                     int kk = S - 1, i = predt, len = 0;
@@ -625,7 +769,7 @@ __global__ void grid_ctrl_reset_kernel(int32_t *ctrl)
 size_t lds_fixed(int S, int n)
 {
     size_t o = align16(grid_pass_big_bytes(S, n));
-    for (int a = 0; a < 3; ++a) o = align16(o + 4 * size_t(n));
+    for (int a = 0; a < 4; ++a) o = align16(o + 4 * size_t(n));
     for (int a = 0; a < 12; ++a) o = align16(o + 4 * size_t(kGridNB));
     o = align16(o + 8 * size_t(kGridRowGroups) * kGridNB);
     return o;
