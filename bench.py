@@ -37,15 +37,15 @@ WORKLOADS = {
 }
 
 
-def measured_traffic(config: int, kernel_s: float):
-    """HBM bytes per launch from the committed rocprofv3 counter summary,
-    as GB/s over the measured launch time; None when the summary does not
-    cover this workload or the kernel sources changed since it was taken."""
-    import glob
+def measured_traffic(kernel: str, config: int, kernel_s: float):
+    """HBM bytes per launch from the committed rocprofv3 counter summary of
+    this kernel on this workload, as GB/s over the measured launch time; None
+    when there is no summary or the kernel's sources changed since it was
+    taken."""
     import hashlib
 
-    path = os.path.join(ROOT, "profiles", "solve_reg_kernel_c4_traffic.json")
-    if config != 4 or not os.path.exists(path):
+    path = os.path.join(ROOT, "profiles", f"{kernel}_c{config}_traffic.json")
+    if not os.path.exists(path):
         return None
     rec = json.load(open(path))
     h = hashlib.sha256()
@@ -54,16 +54,14 @@ def measured_traffic(config: int, kernel_s: float):
         if not os.path.exists(full):
             return None
         h.update(open(full, "rb").read())
-    now = sorted(glob.glob(os.path.join(ROOT, "paper_2509_21221_amd", "csrc", "*.hip")) +
-                 glob.glob(os.path.join(ROOT, "paper_2509_21221_amd", "csrc", "*.h")))
-    if h.hexdigest() != rec["kernel_sources_sha256"] or \
-            sorted(os.path.relpath(f, ROOT) for f in now) != sorted(f for f in rec["sources"] if "csrc" in f):
+    if h.hexdigest() != rec["kernel_sources_sha256"]:
         return None
     return rec["traffic_bytes_per_launch"] / kernel_s / 1e9
 
 
 KERNELS = {1: "solve_reg_kernel", 2: "solve_kernel (LDS state)", 3: "solve_grid_kernel",
            4: "solve_kernel (global-memory state)"}
+KERNEL_SYMBOLS = {1: "solve_reg_kernel", 2: "solve_kernel_lds", 3: "solve_grid_kernel", 4: "solve_kernel_global"}
 
 
 def stored_oracle_baseline(config: int):
@@ -196,7 +194,7 @@ def main():
             "forward": float(stats[:, 8].sum() / max(1, stats[:, 0].sum())),
             "backward": float(stats[:, 9].sum() / max(1, stats[:, 0].sum()))},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(args.config, kernel_s),
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(KERNEL_SYMBOLS.get(main_pass, "?"), args.config, kernel_s),
                      "kernel": KERNELS.get(main_pass, "?") +
                      (" (one launch per step)" if main_pass != 3 else " (one cooperative launch per instance)"),
                      "instances_per_pass": {KERNELS[p]: int((passes == p).sum()) for p in np.unique(passes)},

@@ -5,6 +5,7 @@
 // workgroups), and the global-memory fallback pass (any n, or instances
 // whose link costs or flow lists do not fit the faster passes).
 #include "gwtf_mcf.h"
+#include "mcf_grid.h"
 #include "mcf_internal.h"
 
 #include <algorithm>

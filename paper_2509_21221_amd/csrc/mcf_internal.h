@@ -1,5 +1,5 @@
 // Internal interface between the host API (mcf_api.hip) and the solver
-// kernels (mcf_solver.hip).  Not part of the public C ABI.
+// kernels.  Not part of the public C ABI.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -101,33 +101,5 @@ size_t reg_pass_scratch_bytes();
 bool reg_pass_fits(int S, int n);
 constexpr size_t kRegStaticLds = 4096; // static LDS of the register-resident kernel (upper bound)
 hipError_t set_lds_limits(size_t max_bytes);
-
-// Grid-cooperative pass (mcf_solver_grid.hip): one instance at a time over
-// S * ceil(n / 128) co-resident workgroups, for 64 < n <= 512.
-constexpr int kGridCtrlInts = 32;      // control block: flags, barrier, per-iteration words
-constexpr int kGridMaxNodes = 512;     // a stage's labels are staged with one thread per node
-constexpr size_t kGridStaticLds = 512; // static LDS of the grid kernel (upper bound)
-struct GridParams {
-    SolveParams base;
-    int32_t instance;   // instance solved by this launch
-    int32_t slices;     // workgroups per stage
-    int64_t list_slots; // flow-list capacity of one workgroup
-    size_t big_bytes;   // leading LDS area: link-cost block or staged predecessors
-    uint32_t *ex, *en;  // [2][S*n] exit / entry labels << 2 | iteration tag, by iteration parity
-    uint32_t *ring;     // [ring_slots] per-iteration arrivals (low 16 bits) and changed count
-    unsigned long long *ring_key; // [ring_slots] per-iteration minimum sink key
-    int32_t ring_slots; // > S + 2: iterations in flight at once across the stages
-    int32_t *pred;      // [S*n] entry predecessor (low 16 bits) and exit predecessor (high)
-    int32_t *path;      // [2*S*n + 8] arc codes of the augmenting path
-    int32_t *path_j;    // [2*S*n + 8] head node of each link arc on the path
-    int32_t *ctrl;      // [kGridCtrlInts], cleared before each launch
-};
-inline int grid_ring_slots(int S) { return S + 8; }
-size_t grid_pass_big_bytes(int S, int n);
-size_t grid_pass_lds_bytes(int S, int n, int64_t list_slots);
-int64_t grid_pass_list_slots(int S, int n, size_t lds_max);
-int grid_pass_slices(int n);
-int grid_pass_blocks_per_cu(size_t lds_bytes);
-hipError_t launch_grid_pass(const GridParams &gp, size_t lds_bytes, hipStream_t s);
 
 } // namespace gwtf

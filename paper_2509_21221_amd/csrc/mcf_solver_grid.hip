@@ -33,6 +33,7 @@
 // complete within the bound ends the solve with the internal-error status
 // instead of hanging the device.
 #include "mcf_device.h"
+#include "mcf_grid.h"
 
 namespace gwtf {
 namespace {
