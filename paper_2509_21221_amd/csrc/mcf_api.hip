@@ -7,6 +7,7 @@
 #include "gwtf_mcf.h"
 #include "mcf_grid.h"
 #include "mcf_internal.h"
+#include "mcf_pipe.h"
 
 #include <algorithm>
 #include <cstdio>
@@ -239,10 +240,11 @@ extern "C" gwtf_status_t gwtf_mcf_solve_batch(gwtf_mcf_t *h, const gwtf_mcf_batc
     h->solved = 0;
     const int64_t worst = int64_t(std::max(S - 1, 0)) * n * n;
     bool need_fallback = true;
-    const int64_t reg_slots = (n > 16 && reg_pass_fits(S, n))
+    const int64_t pipe_slots = (n > 16 && pipe_pass_fits(S, n)) ? pipe_pass_slots(S, h->lds_max) : 0;
+    const int64_t reg_slots = (pipe_slots == 0 && n > 16 && reg_pass_fits(S, n))
         ? lds_slots_with(S, n, reg_pass_scratch_bytes() + kRegStaticLds, h->lds_max) : 0;
     const int waves = lds_waves(n);
-    const int64_t slots = reg_slots > 0 ? 0 : lds_slots(S, n, waves, h->lds_max);
+    const int64_t slots = (reg_slots > 0 || pipe_slots > 0) ? 0 : lds_slots(S, n, waves, h->lds_max);
     if (h->grid) {
         // One cooperative launch per instance; instances whose link costs
         // need more than 16 bits or whose flow lists outgrow LDS go to the
@@ -268,6 +270,13 @@ extern "C" gwtf_status_t gwtf_mcf_solve_batch(gwtf_mcf_t *h, const gwtf_mcf_batc
             if ((e = launch_grid_pass(gp, h->grid_lds, h->stream)) != hipSuccess)
                 return hip_fail(h, e, "grid solver launch");
         }
+        need_fallback = true;
+    } else if (pipe_slots > 0) {
+        // Stage-pipelined register pass; instances needing wider link costs
+        // or more flow-list slots go to the fallback pass.
+        p.list_slots = pipe_slots;
+        p.route_all = 0;
+        if ((e = launch_pipe_pass(p, h->stream)) != hipSuccess) return hip_fail(h, e, "pipelined solver launch");
         need_fallback = true;
     } else if (reg_slots > 0) {
         // Register-resident pass; instances whose link costs need more than
