@@ -11,7 +11,7 @@ constexpr int kPipeMaxStages = 32;
 
 // Dynamic LDS of one workgroup (node arrays are [S][64], one row per stage).
 struct PipeLayout {
-    size_t exmb, enmb, yrow, nf, capl, prin, prout, loff, llen, path, lamt, lcost, lpart;
+    size_t exmb, enmb, nf, capl, prin, prout, loff, llen, path, lamt, lent;
     size_t total;
 };
 
@@ -23,7 +23,6 @@ __host__ __device__ inline PipeLayout pipe_layout(int S, int64_t slots)
     auto take = [&](size_t bytes) { size_t at = o; o = align16(o + bytes); return at; };
     L.exmb = take(4 * rows);
     L.enmb = take(4 * rows);
-    L.yrow = take(4 * 8 * 64);
     L.nf = take(4 * rows);
     L.capl = take(4 * rows);
     L.prin = take(rows);
@@ -32,8 +31,7 @@ __host__ __device__ inline PipeLayout pipe_layout(int S, int64_t slots)
     L.llen = take(rows);
     L.path = take(4 * (2 * rows + 8));
     L.lamt = take(4 * lslots);
-    L.lcost = take(2 * lslots);
-    L.lpart = take(lslots);
+    L.lent = take(4 * lslots); // partner | cost << 8
     L.total = o;
     return L;
 }

@@ -134,7 +134,6 @@ __global__ __launch_bounds__(kPipeThreads, 1) void solve_pipe_kernel(SolveParams
     const PipeLayout L = pipe_layout(S, p.list_slots);
     uint32_t *exmb = reinterpret_cast<uint32_t *>(smem + L.exmb); // [S][64] exit labels << 1 | parity
     uint32_t *enmb = reinterpret_cast<uint32_t *>(smem + L.enmb); // [S][64] entry labels << 1 | parity
-    int *yrow = reinterpret_cast<int *>(smem + L.yrow) + w * 64;  // this wave's partner-label row
     int *nf = reinterpret_cast<int *>(smem + L.nf);               // [S][64] node flow mirror
     int *capl = reinterpret_cast<int *>(smem + L.capl);           // [S][64]
     int8_t *prin8 = reinterpret_cast<int8_t *>(smem + L.prin);    // [S][64]
@@ -143,8 +142,7 @@ __global__ __launch_bounds__(kPipeThreads, 1) void solve_pipe_kernel(SolveParams
     uint8_t *llen = reinterpret_cast<uint8_t *>(smem + L.llen);   // [S][64]
     int *path = reinterpret_cast<int *>(smem + L.path);           // [2*S*64 + 8]
     int *lamt = reinterpret_cast<int *>(smem + L.lamt);
-    uint16_t *lcost = reinterpret_cast<uint16_t *>(smem + L.lcost);
-    uint8_t *lpart = reinterpret_cast<uint8_t *>(smem + L.lpart);
+    uint32_t *lent = reinterpret_cast<uint32_t *>(smem + L.lent); // partner | cost << 8
 
     const int32_t *gcap = p.cap + size_t(b) * SN;
     const int32_t *gnc = p.ncost + size_t(b) * SN;
@@ -216,7 +214,7 @@ __global__ __launch_bounds__(kPipeThreads, 1) void solve_pipe_kernel(SolveParams
         for (int s = 0; s < P; ++s) {
             const int k = k0 + s;
             const bool own = k <= klast && k < S - 1;
-            const int c = (own && jv && supply > 0 && capr[s] > 0) ? min(min(capr[s], n), supply) : 0;
+            const int c = (own && jv && supply > 0 && capr[s] > 0) ? (min(min(capr[s], n), supply) + 3) & ~3 : 0;
             int incl = c;
 #pragma unroll
             for (int off = 1; off < 64; off <<= 1) {
@@ -313,18 +311,25 @@ __global__ __launch_bounds__(kPipeThreads, 1) void solve_pipe_kernel(SolveParams
                         if (k >= 1) {
                             const bool dr = X < seen[s];
                             seen[s] = dr ? X : seen[s];
-                            uint64_t mask = __ballot(dr);
+                            const uint64_t mask = __ballot(dr);
                             rows += __popcll(mask);
-                            while (mask) {
-                                const int r = __builtin_ctzll(mask);
-                                mask &= mask - 1;
-                                const int xr = __builtin_amdgcn_readlane(X, r);
-                                const uint32_t wd = lw[s][r >> 1];
-                                const uint32_t c = (r & 1) ? (wd >> 16) : (wd & 0xffffu);
+                            // rows that dropped, two per cost register, in row order
+                            auto relax = [&](int xr, uint32_t c, int r) {
                                 const int cand = xr + int(c);
                                 const bool take = (c != kNoArc16) & (cand < di);
                                 di = take ? cand : di;
                                 pi = take ? r : pi;
+                            };
+                            if (mask) {
+#pragma unroll
+                                for (int r2 = 0; r2 < 32; ++r2) {
+                                    const uint32_t bits = uint32_t(mask >> (2 * r2)) & 3u;
+                                    if (bits) {
+                                        const uint32_t wd = lw[s][r2];
+                                        if (bits & 1u) relax(__builtin_amdgcn_readlane(X, 2 * r2), wd & 0xffffu, 2 * r2);
+                                        if (bits & 2u) relax(__builtin_amdgcn_readlane(X, 2 * r2 + 1), wd >> 16, 2 * r2 + 1);
+                                    }
+                                }
                             }
                         }
                         const int fl = flow[s], nc = ncr[s];
@@ -337,20 +342,30 @@ __global__ __launch_bounds__(kPipeThreads, 1) void solve_pipe_kernel(SolveParams
                             po = kPredSplit;
                         }
                         if (k + 1 < S) {
-                            yrow[lane] = Y;
-                            __builtin_amdgcn_wave_barrier();
+                            // reverse links: four list entries per read, partner
+                            // labels from the partner's lane
+                            // (the loop runs to the wave's longest list so that every
+                            // cross-lane read happens with all lanes active)
                             const int lo = loff[k * 64 + lane], len = jv ? llen[k * 64 + lane] : 0;
-                            for (int e = lo; e < lo + len; ++e) {
-                                const int j = lpart[e];
-                                const int dj = yrow[j];
-                                const int c = lcost[e];
-                                if (dj < kInf && dj - c < dq) {
-                                    dq = dj - c;
-                                    po = j;
+                            int maxlen = len;
+#pragma unroll
+                            for (int off = 32; off > 0; off >>= 1) maxlen = max(maxlen, __shfl_xor(maxlen, off));
+                            maxlen = __builtin_amdgcn_readfirstlane(maxlen);
+                            for (int e = 0; e < maxlen; e += 4) {
+                                const uint4 v4 = *reinterpret_cast<const uint4 *>(&lent[lo + e]);
+                                const uint32_t ent[4] = {v4.x, v4.y, v4.z, v4.w};
+#pragma unroll
+                                for (int u = 0; u < 4; ++u) {
+                                    const bool here = e + u < len;
+                                    const int j = here ? int(ent[u] & 255u) : 0, c = int(ent[u] >> 8);
+                                    const int dj = __shfl(Y, j);
+                                    if (here && dj < kInf && dj - c < dq) {
+                                        dq = dj - c;
+                                        po = j;
+                                    }
                                 }
                             }
                             pulls += len;
-                            __builtin_amdgcn_wave_barrier();
                         }
                         if (fl > 0 && dq < kInf && dq - nc < di) {
                             di = dq - nc;
@@ -443,7 +458,7 @@ __global__ __launch_bounds__(kPipeThreads, 1) void solve_pipe_kernel(SolveParams
                         } else if (pr >= 0 && pr < n && kk + 1 < S) {
                             int amt = 0;
                             for (int e = loff[q]; e < loff[q] + llen[q]; ++e)
-                                if (lpart[e] == pr) amt = lamt[e];
+                                if (int(lent[e] & 255u) == pr) amt = lamt[e];
                             path[len++] = arc_code(kArcLinkRev, kk, i, pr);
                             delta = min(delta, amt);
                             kk = kk + 1;
@@ -494,13 +509,12 @@ __global__ __launch_bounds__(kPipeThreads, 1) void solve_pipe_kernel(SolveParams
                                 const int lo = loff[q], hi = lo + llen[q];
                                 int le = -1;
                                 for (int x = lo; x < hi; ++x)
-                                    if (lpart[x] == j) le = x;
+                                    if (int(lent[x] & 255u) == j) le = x;
                                 if (le < 0 || lamt[le] < delta) {
                                     atomicOr(&ps.fault, 1);
                                 } else if (lamt[le] == delta) { // the arc empties: move the last entry here
-                                    lpart[le] = lpart[hi - 1];
+                                    lent[le] = lent[hi - 1];
                                     lamt[le] = lamt[hi - 1];
-                                    lcost[le] = lcost[hi - 1];
                                     llen[q] = uint8_t(hi - 1 - lo);
                                 } else {
                                     lamt[le] -= delta;
@@ -510,15 +524,14 @@ __global__ __launch_bounds__(kPipeThreads, 1) void solve_pipe_kernel(SolveParams
                             const int lo = loff[q], hi = lo + llen[q];
                             int le = -1;
                             for (int x = lo; x < hi; ++x)
-                                if (lpart[x] == j) le = x;
+                                if (int(lent[x] & 255u) == j) le = x;
                             if (le >= 0) {
                                 lamt[le] += delta;
                             } else if (hi - lo >= min(min(capl[q], n), supply)) {
                                 atomicOr(&ps.fault, 1);
                             } else {
-                                lpart[hi] = uint8_t(j);
+                                lent[hi] = uint32_t(j) | (uint32_t(gac[(size_t(kk) * n + i) * n + j]) << 8);
                                 lamt[hi] = delta;
-                                lcost[hi] = uint16_t(gac[(size_t(kk) * n + i) * n + j]);
                                 llen[q] = uint8_t(hi + 1 - lo);
                             }
                         }
@@ -567,7 +580,7 @@ __global__ __launch_bounds__(kPipeThreads, 1) void solve_pipe_kernel(SolveParams
         for (int q = tid; q < (S - 1) * 64; q += kPipeThreads) {
             const int k = q >> 6, i = q & 63;
             if (i >= n) continue;
-            for (int e = loff[q]; e < loff[q] + llen[q]; ++e) af[(size_t(k) * n + i) * n + lpart[e]] = lamt[e];
+            for (int e = loff[q]; e < loff[q] + llen[q]; ++e) af[(size_t(k) * n + i) * n + (lent[e] & 255u)] = lamt[e];
         }
     }
     if (tid == 0) {
@@ -603,7 +616,7 @@ int64_t pipe_pass_slots(int S, size_t lds_max)
 {
     const size_t fixed = pipe_layout(S, 0).total + sizeof(PipeShared) + 256;
     if (fixed >= lds_max) return 0;
-    return std::min<int64_t>(int64_t((lds_max - fixed) / 7), 65535);
+    return std::min<int64_t>(int64_t((lds_max - fixed) / 8), 65535);
 }
 
 hipError_t launch_pipe_pass(const SolveParams &p, hipStream_t s)
