@@ -59,9 +59,9 @@ def measured_traffic(kernel: str, config: int, kernel_s: float):
     return rec["traffic_bytes_per_launch"] / kernel_s / 1e9
 
 
-KERNELS = {1: "solve_reg_kernel", 2: "solve_kernel (LDS state)", 3: "solve_grid_kernel",
+KERNELS = {1: "solve_pipe_kernel", 2: "solve_kernel (LDS state)", 3: "solve_grid_kernel",
            4: "solve_kernel (global-memory state)"}
-KERNEL_SYMBOLS = {1: "solve_reg_kernel", 2: "solve_kernel_lds", 3: "solve_grid_kernel", 4: "solve_kernel_global"}
+KERNEL_SYMBOLS = {1: "solve_pipe_kernel", 2: "solve_kernel_lds", 3: "solve_grid_kernel", 4: "solve_kernel_global"}
 
 
 def stored_oracle_baseline(config: int):

@@ -1,6 +1,6 @@
 // Host side of the C ABI declared in include/gwtf_mcf.h: argument checks,
-// workspace ownership, and the choice of solver pass: register-resident
-// (16 < n <= 64, S <= 32), LDS-resident (n <= 64, one workgroup per
+// workspace ownership, and the choice of solver pass: stage-pipelined
+// register-resident (16 < n <= 64, S <= 32), LDS-resident (n <= 64, one workgroup per
 // instance), grid-cooperative (64 < n <= 512, one instance over many
 // workgroups), and the global-memory fallback pass (any n, or instances
 // whose link costs or flow lists do not fit the faster passes).
@@ -69,19 +69,6 @@ int64_t lds_slots(int S, int n, int waves, size_t lds_max)
 }
 
 int lds_waves(int n) { return n <= 16 ? 1 : 4; }
-
-// Flow-list capacity left in LDS beside a narrow state layout and `extra`
-// bytes of other LDS use.
-int64_t lds_slots_with(int S, int n, size_t extra, size_t lds_max)
-{
-    if (n > 64) return 0;
-    size_t fixed = make_layout(S, n, 0, true).total + extra + 64;
-    if (fixed >= lds_max) return 0;
-    int64_t slots = int64_t((lds_max - fixed) / 9) - 16;
-    int64_t worst = int64_t(std::max(S - 1, 0)) * n * n;
-    slots = std::min<int64_t>(std::min<int64_t>(slots, worst), 65535);
-    return std::max<int64_t>(slots, 0);
-}
 
 void free_ws(gwtf_mcf_t *h)
 {
@@ -241,10 +228,8 @@ extern "C" gwtf_status_t gwtf_mcf_solve_batch(gwtf_mcf_t *h, const gwtf_mcf_batc
     const int64_t worst = int64_t(std::max(S - 1, 0)) * n * n;
     bool need_fallback = true;
     const int64_t pipe_slots = (n > 16 && pipe_pass_fits(S, n)) ? pipe_pass_slots(S, h->lds_max) : 0;
-    const int64_t reg_slots = (pipe_slots == 0 && n > 16 && reg_pass_fits(S, n))
-        ? lds_slots_with(S, n, reg_pass_scratch_bytes() + kRegStaticLds, h->lds_max) : 0;
     const int waves = lds_waves(n);
-    const int64_t slots = (reg_slots > 0 || pipe_slots > 0) ? 0 : lds_slots(S, n, waves, h->lds_max);
+    const int64_t slots = pipe_slots > 0 ? 0 : lds_slots(S, n, waves, h->lds_max);
     if (h->grid) {
         // One cooperative launch per instance; instances whose link costs
         // need more than 16 bits or whose flow lists outgrow LDS go to the
@@ -277,14 +262,6 @@ extern "C" gwtf_status_t gwtf_mcf_solve_batch(gwtf_mcf_t *h, const gwtf_mcf_batc
         p.list_slots = pipe_slots;
         p.route_all = 0;
         if ((e = launch_pipe_pass(p, h->stream)) != hipSuccess) return hip_fail(h, e, "pipelined solver launch");
-        need_fallback = true;
-    } else if (reg_slots > 0) {
-        // Register-resident pass; instances whose link costs need more than
-        // 16 bits or whose flow lists outgrow LDS go to the fallback pass.
-        p.list_slots = reg_slots;
-        p.route_all = 0;
-        size_t lds = make_layout(S, n, reg_slots, true).total + reg_pass_scratch_bytes();
-        if ((e = launch_reg_pass(p, lds, h->stream)) != hipSuccess) return hip_fail(h, e, "register solver launch");
         need_fallback = true;
     } else if (slots > 0) {
         p.list_slots = slots;

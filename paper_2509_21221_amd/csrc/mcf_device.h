@@ -62,8 +62,6 @@ struct Shared {
     long long rows, pulls, rounds, augs;
     unsigned long long tbest;
     int Dt, predt, pit, any, bad, maxc, status, route;
-    int maxc_link_holes; // register pass: some link is absent (GWTF_NO_ARC)
-    int kmax;            // register pass: largest flow-list capacity of a node
     long long slots;
 };
 

@@ -94,12 +94,6 @@ hipError_t launch_fallback_pass(const SolveParams &p, size_t lds_bytes, hipStrea
 hipError_t launch_export(const int32_t *node_flow_ws, int32_t S, int32_t n, int32_t first, int32_t count,
                          int32_t *src_flow, int32_t *snk_flow, hipStream_t s);
 int fallback_waves();
-// Register-resident pass (mcf_solver_reg.hip): S <= 32, n <= 64, link costs
-// below 65535; instances outside that route to the fallback pass.
-hipError_t launch_reg_pass(const SolveParams &p, size_t lds_bytes, hipStream_t s);
-size_t reg_pass_scratch_bytes();
-bool reg_pass_fits(int S, int n);
-constexpr size_t kRegStaticLds = 4096; // static LDS of the register-resident kernel (upper bound)
 hipError_t set_lds_limits(size_t max_bytes);
 
 } // namespace gwtf
