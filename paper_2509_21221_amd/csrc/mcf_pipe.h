@@ -9,22 +9,24 @@ namespace gwtf {
 
 constexpr int kPipeMaxStages = 32;
 
-// Dynamic LDS of one workgroup (node arrays are [S][64], one row per stage).
+// Dynamic LDS of one workgroup: mailboxes per wave, node arrays [S][64]
+// (one row per stage), the path buffer and the flow lists.
 struct PipeLayout {
-    size_t exmb, enmb, nf, capl, prin, prout, loff, llen, path, lamt, lent;
+    size_t exmb, enmb, nf, capl, ncl, prin, prout, loff, llen, path, lamt, lent;
     size_t total;
 };
 
-__host__ __device__ inline PipeLayout pipe_layout(int S, int64_t slots)
+__host__ __device__ inline PipeLayout pipe_layout(int S, int waves, int64_t slots)
 {
     PipeLayout L;
     const size_t rows = size_t(S) * 64, lslots = size_t(slots) + 64;
     size_t o = 0;
     auto take = [&](size_t bytes) { size_t at = o; o = align16(o + bytes); return at; };
-    L.exmb = take(4 * rows);
-    L.enmb = take(4 * rows);
+    L.exmb = take(4 * size_t(waves) * 64);
+    L.enmb = take(4 * size_t(waves) * 64);
     L.nf = take(4 * rows);
     L.capl = take(4 * rows);
+    L.ncl = take(4 * rows);
     L.prin = take(rows);
     L.prout = take(rows);
     L.loff = take(2 * rows);

@@ -1,6 +1,5 @@
-// Stage-pipelined register pass: one workgroup of 8 waves per instance, for
-// pipelines of at most 32 stages of at most 64 nodes whose link costs fit in
-// 16 bits.
+// Stage-pipelined register pass: one workgroup per instance, for pipelines of
+// at most 32 stages of at most 64 nodes whose link costs fit in 16 bits.
 //
 // Same method as the other passes (successive shortest paths with Johnson
 // potentials on the node-split stage graph, paper Sec. V-A Eq. 2), with the
@@ -8,8 +7,9 @@
 //
 //  * Wave w owns P consecutive stages (k = w*P ...).  For each it keeps, in
 //    vector registers, the 16-bit costs of every link into that stage (lane
-//    j = receiving node, two rows per register: 32 registers per stage), and
-//    the nodes' labels, predecessors, flows and potentials (lane = node).
+//    j = receiving node, two rows per register: 32 registers per stage) and
+//    the nodes' labels and predecessors (lane = node); capacities, compute
+//    costs, node flows and the flow lists of the exits sit in LDS.
 //  * Iteration t of stage k relaxes the links from stage k-1's exit labels
 //    of the same iteration (only the rows whose label dropped since the stage
 //    last saw them), applies its compute arcs in both directions and pulls
@@ -22,17 +22,17 @@
 //  * Convergence is counted per iteration on a ring of LDS counters: the last
 //    wave to finish an iteration in which no label changed anywhere publishes
 //    the sink's key and a stop word.
-//  * After convergence: potentials, then lane 0 of wave 0 walks the path over
-//    predecessors staged in LDS and takes the bottleneck from the LDS mirror
-//    of node flows and the flow lists; every wave applies the path to its own
-//    stages.
+//  * After convergence: potentials (kept in the device workspace), then lane
+//    0 of wave 0 walks the path over predecessors staged in LDS and takes the
+//    bottleneck from the LDS node flows and flow lists; every wave applies
+//    the path to its own stages.
 //
 // Each mailbox is written by one wave and read by one other.  The reader of an
-// exit mailbox (stage k's labels for iteration t) cannot be overtaken: the
-// writer's iteration t+1 needs the reader's stage k+1 output of iteration t,
-// which the reader publishes after its read, so a mailbox holds the awaited
-// iteration or the one before it and one parity bit tells them apart.  The
-// same holds for the entry mailboxes one iteration behind.
+// exit mailbox (a wave's last-stage labels for iteration t) cannot be
+// overtaken: the writer's iteration t+1 needs the reader's first-stage output
+// of iteration t, which the reader publishes after its read, so a mailbox
+// holds the awaited iteration or the one before it and one parity bit tells
+// them apart.  The same holds for the entry mailboxes one iteration behind.
 #include "mcf_device.h"
 #include "mcf_pipe.h"
 
@@ -41,9 +41,7 @@ namespace {
 
 using namespace dev;
 
-constexpr int kPipeWaves = 8;
-constexpr int kPipeThreads = kPipeWaves * 64;
-constexpr int kRing = 16; // iterations in flight across the waves: at most kPipeWaves
+constexpr int kRing = 32; // iterations in flight across the waves: fewer than the waves
 constexpr int kSpinLimit = 1 << 22;
 constexpr uint32_t kNoArc16 = 0xffff;
 constexpr int kBias = 1 << 30;
@@ -84,12 +82,17 @@ __device__ __forceinline__ int arc_code(int type, int k, int i, int j)
     return type | (k << 2) | (i << 7) | (j << 13);
 }
 
+// predecessors of one node, entry side in the low half, exit side in the high
+__device__ __forceinline__ int pred_in(int pp) { return int(int16_t(pp & 0xffff)); }
+__device__ __forceinline__ int pred_out(int pp) { return pp >> 16; }
+__device__ __forceinline__ int pred_pack(int pi, int po) { return (pi & 0xffff) | (po << 16); }
+
 struct PipeShared {
     unsigned ring[kRing];
     unsigned long long ring_key[kRing];
     unsigned long long final_key;
-    int stop;    // iteration at which the search converged; 0 while it runs
-    int fault;   // a wait ran out, or an iteration bound was exceeded
+    int stop;  // iteration at which the search converged; 0 while it runs
+    int fault; // a wait ran out, an iteration bound was exceeded, or a self-check failed
     int bad, wide, maxc;
     int plen, delta;
     int stage_tot[kPipeMaxStages];
@@ -97,7 +100,7 @@ struct PipeShared {
 };
 
 // Waits until all 64 words of a mailbox carry parity `par`; returns this
-// lane's label.  Sets *why to 1 if the search stopped meanwhile, 2 if the
+// lane's label.  Sets why to 1 if the search stopped meanwhile, 2 if the
 // wait ran out.
 __device__ __forceinline__ int mailbox_wait(const uint32_t *mb, uint32_t par, const int *stop, int &why)
 {
@@ -117,31 +120,33 @@ __device__ __forceinline__ int mailbox_wait(const uint32_t *mb, uint32_t par, co
     }
 }
 
-template <int P>
-__global__ __launch_bounds__(kPipeThreads, 1) void solve_pipe_kernel(SolveParams p)
+template <int W, int P>
+__global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
 {
+    constexpr int NT = 64 * W;
     const int b = blockIdx.x;
     const int S = p.S, n = p.n, SN = S * n, V = 2 * SN + 3;
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int nw = (S + P - 1) / P;         // waves that own stages
-    const int k0 = w * P;                   // this wave's first stage
-    const int klast = min(S, k0 + P) - 1;   // and last (k0 > klast for idle waves)
+    const int nw = (S + P - 1) / P;       // waves that own stages
+    const int k0 = w * P;                 // this wave's first stage
+    const int klast = min(S, k0 + P) - 1; // and last (k0 > klast for idle waves)
     const bool jv = lane < n;
 
     extern __shared__ __align__(16) unsigned char smem[];
     __shared__ PipeShared ps;
-    const PipeLayout L = pipe_layout(S, p.list_slots);
-    uint32_t *exmb = reinterpret_cast<uint32_t *>(smem + L.exmb); // [S][64] exit labels << 1 | parity
-    uint32_t *enmb = reinterpret_cast<uint32_t *>(smem + L.enmb); // [S][64] entry labels << 1 | parity
-    int *nf = reinterpret_cast<int *>(smem + L.nf);               // [S][64] node flow mirror
-    int *capl = reinterpret_cast<int *>(smem + L.capl);           // [S][64]
+    const PipeLayout L = pipe_layout(S, W, p.list_slots);
+    uint32_t *exmb = reinterpret_cast<uint32_t *>(smem + L.exmb); // [W][64] last-stage exit labels << 1 | parity
+    uint32_t *enmb = reinterpret_cast<uint32_t *>(smem + L.enmb); // [W][64] first-stage entry labels << 1 | parity
+    int *nf = reinterpret_cast<int *>(smem + L.nf);               // [S][64] node flow
+    int *capl = reinterpret_cast<int *>(smem + L.capl);           // [S][64] node capacity
+    int *ncl = reinterpret_cast<int *>(smem + L.ncl);             // [S][64] node compute cost
     int8_t *prin8 = reinterpret_cast<int8_t *>(smem + L.prin);    // [S][64]
     int8_t *prout8 = reinterpret_cast<int8_t *>(smem + L.prout);  // [S][64]
     uint16_t *loff = reinterpret_cast<uint16_t *>(smem + L.loff); // [S][64]
     uint8_t *llen = reinterpret_cast<uint8_t *>(smem + L.llen);   // [S][64]
     int *path = reinterpret_cast<int *>(smem + L.path);           // [2*S*64 + 8]
-    int *lamt = reinterpret_cast<int *>(smem + L.lamt);
+    int *lamt = reinterpret_cast<int *>(smem + L.lamt);           // flow of each list entry
     uint32_t *lent = reinterpret_cast<uint32_t *>(smem + L.lent); // partner | cost << 8
 
     const int32_t *gcap = p.cap + size_t(b) * SN;
@@ -161,7 +166,8 @@ __global__ __launch_bounds__(kPipeThreads, 1) void solve_pipe_kernel(SolveParams
 
     // ---------------- ingest + validate ----------------
     u32x32 lw[P];
-    int capr[P], ncr[P], flow[P], din[P], dout[P], prin[P], prout[P], seen[P], potin[P], potout[P];
+    int din[P], dout[P], pp[P], seen[P];
+    uint32_t holes = 0; // bit s: some link into stage k0+s is missing
     int srcc = 0, snkc = 0;
     {
         int bad = 0, wide = 0, mx = 0;
@@ -169,13 +175,12 @@ __global__ __launch_bounds__(kPipeThreads, 1) void solve_pipe_kernel(SolveParams
         for (int s = 0; s < P; ++s) {
             const int k = k0 + s;
             const bool own = k <= klast;
-            capr[s] = (own && jv) ? gcap[k * n + lane] : 0;
-            ncr[s] = (own && jv) ? gnc[k * n + lane] : 0;
-            bad |= (capr[s] < 0) | (ncr[s] < 0);
-            mx = max(mx, ncr[s]);
-            flow[s] = 0;
-            potin[s] = potout[s] = 0;
+            const int cp = (own && jv) ? gcap[k * n + lane] : 0;
+            const int nc = (own && jv) ? gnc[k * n + lane] : 0;
+            bad |= (cp < 0) | (nc < 0);
+            mx = max(mx, nc);
             u32x32 v = (u32x32)(0xffffffffu);
+            int hole = 0;
             if (own && k >= 1) {
                 const int32_t *layer = gac + size_t(k - 1) * n * n;
 #pragma unroll
@@ -184,6 +189,7 @@ __global__ __launch_bounds__(kPipeThreads, 1) void solve_pipe_kernel(SolveParams
                     const int a1 = (jv && 2 * r + 1 < n) ? layer[(2 * r + 1) * n + lane] : -1;
                     bad |= (a0 < -1) | (a1 < -1);
                     wide |= (a0 > 65534) | (a1 > 65534);
+                    hole |= (jv & (2 * r < n) & (a0 < 0)) | (jv & (2 * r + 1 < n) & (a1 < 0));
                     mx = max(mx, max(a0, a1));
                     const uint32_t c0 = a0 < 0 ? kNoArc16 : uint32_t(min(a0, 65535));
                     const uint32_t c1 = a1 < 0 ? kNoArc16 : uint32_t(min(a1, 65535));
@@ -191,9 +197,15 @@ __global__ __launch_bounds__(kPipeThreads, 1) void solve_pipe_kernel(SolveParams
                 }
             }
             lw[s] = v;
+            if (__any(hole)) holes |= 1u << s;
             if (own) {
-                capl[k * 64 + lane] = capr[s];
+                capl[k * 64 + lane] = cp;
+                ncl[k * 64 + lane] = nc;
                 nf[k * 64 + lane] = 0;
+                if (jv) {
+                    gpot[3 + 2 * (k * n + lane)] = 0;
+                    gpot[4 + 2 * (k * n + lane)] = 0;
+                }
             }
         }
         if (k0 == 0 && jv && p.src) srcc = p.src[size_t(b) * n + lane];
@@ -202,10 +214,11 @@ __global__ __launch_bounds__(kPipeThreads, 1) void solve_pipe_kernel(SolveParams
         mx = max(mx, max(srcc, snkc));
         if (__any(bad)) atomicOr(&ps.bad, 1);
         if (__any(wide)) atomicOr(&ps.wide, 1);
-        mx = max(mx, __shfl_xor(mx, 32));
-        for (int off = 16; off > 0; off >>= 1) mx = max(mx, __shfl_xor(mx, off));
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) mx = max(mx, __shfl_xor(mx, off));
         if (lane == 0) atomicMax(&ps.maxc, mx);
     }
+    holes = __builtin_amdgcn_readfirstlane(holes);
 
     // flow-list capacity of each exit: min(cap, n, supply); none in the last stage
     {
@@ -214,7 +227,8 @@ __global__ __launch_bounds__(kPipeThreads, 1) void solve_pipe_kernel(SolveParams
         for (int s = 0; s < P; ++s) {
             const int k = k0 + s;
             const bool own = k <= klast && k < S - 1;
-            const int c = (own && jv && supply > 0 && capr[s] > 0) ? (min(min(capr[s], n), supply) + 3) & ~3 : 0;
+            const int cp = own ? capl[k * 64 + lane] : 0;
+            const int c = (own && jv && supply > 0 && cp > 0) ? min(min(cp, n), supply) : 0;
             int incl = c;
 #pragma unroll
             for (int off = 1; off < 64; off <<= 1) {
@@ -236,6 +250,11 @@ __global__ __launch_bounds__(kPipeThreads, 1) void solve_pipe_kernel(SolveParams
             before += ps.stage_tot[k];
         }
         if (klast == S - 1 && k0 <= klast && lane == 0 && before > p.list_slots) atomicOr(&ps.wide, 2);
+    }
+    if (tid == 0) {
+        gpot[0] = 0;
+        gpot[1] = 0;
+        gpot[2] = 0;
     }
     __syncthreads();
     int status = 0;
@@ -261,12 +280,12 @@ __global__ __launch_bounds__(kPipeThreads, 1) void solve_pipe_kernel(SolveParams
                 const int k = k0 + s;
                 din[s] = (k == 0 && jv) ? srcc : kInf;
                 dout[s] = kInf;
-                prin[s] = k == 0 ? kPredSrc : kPredNone;
-                prout[s] = kPredNone;
+                pp[s] = pred_pack(k == 0 ? kPredSrc : kPredNone, kPredNone);
                 seen[s] = kInf;
-                if (k > klast) continue;
-                if (s == 0 && k >= 1) lds_st(&enmb[k * 64 + lane], uint32_t(din[s]) << 1);
-                if (k == klast && k + 1 < S) lds_st(&exmb[k * 64 + lane], uint32_t(kInf) << 1);
+            }
+            if (k0 <= klast) {
+                if (k0 >= 1) lds_st(&enmb[w * 64 + lane], uint32_t(din[0]) << 1);
+                if (klast + 1 < S) lds_st(&exmb[w * 64 + lane], uint32_t(kInf) << 1);
             }
             if (tid < kRing) {
                 ps.ring[tid] = 0;
@@ -297,16 +316,19 @@ __global__ __launch_bounds__(kPipeThreads, 1) void solve_pipe_kernel(SolveParams
                     for (int s = 0; s < P; ++s) {
                         const int k = k0 + s;
                         if (k > klast) break;
+                        const int q = k * 64 + lane;
+                        // node data for this step, read ahead of the waits
+                        const int fl = nf[q], cp = capl[q], nc = ncl[q];
                         // forward input: exit labels of stage k-1, iteration t
                         int X = kInf;
-                        if (k >= 1) X = s == 0 ? mailbox_wait(&exmb[(k - 1) * 64], par, &ps.stop, why) : dout[s - 1];
+                        if (k >= 1) X = s == 0 ? mailbox_wait(&exmb[(w - 1) * 64], par, &ps.stop, why) : dout[s - 1];
                         // backward input: entry labels of stage k+1, iteration t-1
                         int Y = kInf;
                         if (k + 1 < S && !why)
-                            Y = k == klast ? mailbox_wait(&enmb[(k + 1) * 64], par ^ 1u, &ps.stop, why) : din[s + 1];
+                            Y = k == klast ? mailbox_wait(&enmb[(w + 1) * 64], par ^ 1u, &ps.stop, why) : din[s + 1];
                         if (why) break;
                         ++steps;
-                        int di = din[s], dq = dout[s], pi = prin[s], po = prout[s];
+                        int di = din[s], dq = dout[s], pi = pred_in(pp[s]), po = pred_out(pp[s]);
                         const int di0 = di, dq0 = dq;
                         if (k >= 1) {
                             const bool dr = X < seen[s];
@@ -314,46 +336,62 @@ __global__ __launch_bounds__(kPipeThreads, 1) void solve_pipe_kernel(SolveParams
                             const uint64_t mask = __ballot(dr);
                             rows += __popcll(mask);
                             // rows that dropped, two per cost register, in row order
-                            auto relax = [&](int xr, uint32_t c, int r) {
-                                const int cand = xr + int(c);
-                                const bool take = (c != kNoArc16) & (cand < di);
-                                di = take ? cand : di;
-                                pi = take ? r : pi;
-                            };
                             if (mask) {
+                                if (!((holes >> s) & 1u)) {
 #pragma unroll
-                                for (int r2 = 0; r2 < 32; ++r2) {
-                                    const uint32_t bits = uint32_t(mask >> (2 * r2)) & 3u;
-                                    if (bits) {
-                                        const uint32_t wd = lw[s][r2];
-                                        if (bits & 1u) relax(__builtin_amdgcn_readlane(X, 2 * r2), wd & 0xffffu, 2 * r2);
-                                        if (bits & 2u) relax(__builtin_amdgcn_readlane(X, 2 * r2 + 1), wd >> 16, 2 * r2 + 1);
+                                    for (int r2 = 0; r2 < 32; ++r2) {
+                                        const uint32_t bits = uint32_t(mask >> (2 * r2)) & 3u;
+                                        if (bits) {
+                                            const uint32_t wd = lw[s][r2];
+                                            if (bits & 1u) {
+                                                const int cand = __builtin_amdgcn_readlane(X, 2 * r2) + int(wd & 0xffffu);
+                                                pi = cand < di ? 2 * r2 : pi;
+                                                di = min(di, cand);
+                                            }
+                                            if (bits & 2u) {
+                                                const int cand = __builtin_amdgcn_readlane(X, 2 * r2 + 1) + int(wd >> 16);
+                                                pi = cand < di ? 2 * r2 + 1 : pi;
+                                                di = min(di, cand);
+                                            }
+                                        }
+                                    }
+                                } else {
+                                    // some links are missing (cost 0xffff): skip them
+                                    uint64_t m = mask;
+                                    while (m) {
+                                        const int r = __builtin_ctzll(m);
+                                        m &= m - 1;
+                                        const uint32_t c = (lw[s][r >> 1] >> (16 * (r & 1))) & 0xffffu;
+                                        const int cand = __builtin_amdgcn_readlane(X, r) + int(c);
+                                        const bool take = (c != kNoArc16) & (cand < di);
+                                        pi = take ? r : pi;
+                                        di = take ? cand : di;
                                     }
                                 }
                             }
                         }
-                        const int fl = flow[s], nc = ncr[s];
                         if (fl > 0 && dq < kInf && dq - nc < di) {
                             di = dq - nc;
                             pi = kPredSplit;
                         }
-                        if (di < kInf && fl < capr[s] && di + nc < dq) {
+                        if (di < kInf && fl < cp && di + nc < dq) {
                             dq = di + nc;
                             po = kPredSplit;
                         }
                         if (k + 1 < S) {
-                            // reverse links: four list entries per read, partner
-                            // labels from the partner's lane
-                            // (the loop runs to the wave's longest list so that every
-                            // cross-lane read happens with all lanes active)
-                            const int lo = loff[k * 64 + lane], len = jv ? llen[k * 64 + lane] : 0;
+                            // reverse links: four list entries per pass, partner
+                            // labels from the partner's lane (the loop runs to the
+                            // wave's longest list so every cross-lane read has all
+                            // lanes active)
+                            const int lo = loff[q], len = jv ? llen[q] : 0;
                             int maxlen = len;
 #pragma unroll
                             for (int off = 32; off > 0; off >>= 1) maxlen = max(maxlen, __shfl_xor(maxlen, off));
                             maxlen = __builtin_amdgcn_readfirstlane(maxlen);
                             for (int e = 0; e < maxlen; e += 4) {
-                                const uint4 v4 = *reinterpret_cast<const uint4 *>(&lent[lo + e]);
-                                const uint32_t ent[4] = {v4.x, v4.y, v4.z, v4.w};
+                                uint32_t ent[4];
+#pragma unroll
+                                for (int u = 0; u < 4; ++u) ent[u] = lent[lo + e + u];
 #pragma unroll
                                 for (int u = 0; u < 4; ++u) {
                                     const bool here = e + u < len;
@@ -374,10 +412,9 @@ __global__ __launch_bounds__(kPipeThreads, 1) void solve_pipe_kernel(SolveParams
                         chg |= (di != di0) | (dq != dq0);
                         din[s] = di;
                         dout[s] = dq;
-                        prin[s] = pi;
-                        prout[s] = po;
-                        if (s == 0 && k >= 1) lds_st(&enmb[k * 64 + lane], (uint32_t(di) << 1) | par);
-                        if (k == klast && k + 1 < S) lds_st(&exmb[k * 64 + lane], (uint32_t(dq) << 1) | par);
+                        pp[s] = pred_pack(pi, po);
+                        if (s == 0 && k >= 1) lds_st(&enmb[w * 64 + lane], (uint32_t(di) << 1) | par);
+                        if (k == klast && k + 1 < S) lds_st(&exmb[w * 64 + lane], (uint32_t(dq) << 1) | par);
                         if (k == S - 1) {
                             const uint64_t key = (jv && dq < kInf) ? pack_key(dq + snkc, lane) : ~0ull;
                             skey = wave_min_u64(key);
@@ -406,13 +443,13 @@ __global__ __launch_bounds__(kPipeThreads, 1) void solve_pipe_kernel(SolveParams
                     }
                 }
             }
+#pragma unroll
+            for (int off = 32; off > 0; off >>= 1) pulls += __shfl_xor(pulls, off);
             if (lane == 0) {
                 atomicAdd(reinterpret_cast<unsigned long long *>(&ps.rows), (unsigned long long)rows);
                 atomicAdd(reinterpret_cast<unsigned long long *>(&ps.steps), (unsigned long long)steps);
+                atomicAdd(reinterpret_cast<unsigned long long *>(&ps.pulls), (unsigned long long)pulls);
             }
-#pragma unroll
-            for (int off = 32; off > 0; off >>= 1) pulls += __shfl_xor(pulls, off);
-            if (lane == 0) atomicAdd(reinterpret_cast<unsigned long long *>(&ps.pulls), (unsigned long long)pulls);
             __syncthreads();
             clk_iter += lap(tick);
             if (ps.fault) {
@@ -431,11 +468,12 @@ __global__ __launch_bounds__(kPipeThreads, 1) void solve_pipe_kernel(SolveParams
                 const int k = k0 + s;
                 if (k > klast) break;
                 if (jv) {
-                    potin[s] = min(din[s], potin[s] + dred);
-                    potout[s] = min(dout[s], potout[s] + dred);
+                    int32_t *pin = gpot + 3 + 2 * (k * n + lane);
+                    pin[0] = min(din[s], pin[0] + dred);
+                    pin[1] = min(dout[s], pin[1] + dred);
                 }
-                prin8[k * 64 + lane] = int8_t(prin[s]);
-                prout8[k * 64 + lane] = int8_t(prout[s]);
+                prin8[k * 64 + lane] = int8_t(pred_in(pp[s]));
+                prout8[k * 64 + lane] = int8_t(pred_out(pp[s]));
             }
             __syncthreads();
 
@@ -539,12 +577,6 @@ __global__ __launch_bounds__(kPipeThreads, 1) void solve_pipe_kernel(SolveParams
                     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
                     __builtin_amdgcn_wave_barrier();
                 }
-#pragma unroll
-                for (int s = 0; s < P; ++s) {
-                    const int k = k0 + s;
-                    if (k > klast) break;
-                    flow[s] = nf[k * 64 + lane];
-                }
             }
             F += delta;
             cost += (long long)delta * Dt;
@@ -562,22 +594,26 @@ __global__ __launch_bounds__(kPipeThreads, 1) void solve_pipe_kernel(SolveParams
     // ---------------- export ----------------
     const bool ok = status == 0 && !fault;
     int32_t *nfo = p.node_flow + size_t(b) * SN;
+    if (k0 <= klast && jv) {
 #pragma unroll
-    for (int s = 0; s < P; ++s) {
-        const int k = k0 + s;
-        if (k <= klast && jv) {
-            const int q = k * n + lane;
-            nfo[q] = ok ? flow[s] : 0;
-            gpot[3 + 2 * q] = ok ? potin[s] : 0;
-            gpot[4 + 2 * q] = ok ? potout[s] : 0;
+        for (int s = 0; s < P; ++s) {
+            const int k = k0 + s;
+            if (k <= klast) {
+                const int q = k * n + lane;
+                nfo[q] = ok ? nf[k * 64 + lane] : 0;
+                if (!ok) {
+                    gpot[3 + 2 * q] = 0;
+                    gpot[4 + 2 * q] = 0;
+                }
+            }
         }
     }
     const size_t na = size_t(S - 1) * n * n;
     int32_t *af = p.arc_flow + size_t(b) * na;
-    for (size_t e = tid; e < na; e += kPipeThreads) af[e] = 0;
+    for (size_t e = tid; e < na; e += NT) af[e] = 0;
     __syncthreads();
     if (ok) {
-        for (int q = tid; q < (S - 1) * 64; q += kPipeThreads) {
+        for (int q = tid; q < (S - 1) * 64; q += NT) {
             const int k = q >> 6, i = q & 63;
             if (i >= n) continue;
             for (int e = loff[q]; e < loff[q] + llen[q]; ++e) af[(size_t(k) * n + i) * n + (lent[e] & 255u)] = lamt[e];
@@ -606,30 +642,42 @@ __global__ __launch_bounds__(kPipeThreads, 1) void solve_pipe_kernel(SolveParams
     }
 }
 
-} // namespace
+// Waves and stages per wave for a pipeline of S stages.
+void pipe_shape(int S, int &W, int &P)
+{
+    if (S <= 8) {
+        W = 8;
+        P = 1;
+    } else if (S <= 16) {
+        W = 16;
+        P = 1;
+    } else {
+        W = 16;
+        P = 2;
+    }
+}
 
-PipeLayout pipe_layout_host(int S, int64_t slots) { return pipe_layout(S, slots); }
+} // namespace
 
 bool pipe_pass_fits(int S, int n) { return S >= 1 && S <= kPipeMaxStages && n >= 1 && n <= 64; }
 
 int64_t pipe_pass_slots(int S, size_t lds_max)
 {
-    const size_t fixed = pipe_layout(S, 0).total + sizeof(PipeShared) + 256;
+    int W, P;
+    pipe_shape(S, W, P);
+    const size_t fixed = pipe_layout(S, W, 0).total + sizeof(PipeShared) + 256;
     if (fixed >= lds_max) return 0;
     return std::min<int64_t>(int64_t((lds_max - fixed) / 8), 65535);
 }
 
 hipError_t launch_pipe_pass(const SolveParams &p, hipStream_t s)
 {
-    const size_t lds = pipe_layout(p.S, p.list_slots).total;
-    const int P = (p.S + kPipeWaves - 1) / kPipeWaves;
-    switch (P) {
-    case 1: hipLaunchKernelGGL(solve_pipe_kernel<1>, dim3(p.B), dim3(kPipeThreads), lds, s, p); break;
-    case 2: hipLaunchKernelGGL(solve_pipe_kernel<2>, dim3(p.B), dim3(kPipeThreads), lds, s, p); break;
-    case 3: hipLaunchKernelGGL(solve_pipe_kernel<3>, dim3(p.B), dim3(kPipeThreads), lds, s, p); break;
-    case 4: hipLaunchKernelGGL(solve_pipe_kernel<4>, dim3(p.B), dim3(kPipeThreads), lds, s, p); break;
-    default: return hipErrorInvalidValue;
-    }
+    int W, P;
+    pipe_shape(p.S, W, P);
+    const size_t lds = pipe_layout(p.S, W, p.list_slots).total;
+    if (W == 8) hipLaunchKernelGGL((solve_pipe_kernel<8, 1>), dim3(p.B), dim3(512), lds, s, p);
+    else if (P == 1) hipLaunchKernelGGL((solve_pipe_kernel<16, 1>), dim3(p.B), dim3(1024), lds, s, p);
+    else hipLaunchKernelGGL((solve_pipe_kernel<16, 2>), dim3(p.B), dim3(1024), lds, s, p);
     return hipGetLastError();
 }
 
