@@ -12,7 +12,7 @@ constexpr int kPipeMaxStages = 32;
 // Dynamic LDS of one workgroup: mailboxes per wave, node arrays [S][64]
 // (one row per stage), the path buffer and the flow lists.
 struct PipeLayout {
-    size_t exmb, enmb, nf, capl, ncl, prin, prout, loff, llen, path, lamt, lent;
+    size_t exmb, enmb, nf, capl, ncl, chain, loff, llen, path, lamt, lent;
     size_t total;
 };
 
@@ -27,8 +27,7 @@ __host__ __device__ inline PipeLayout pipe_layout(int S, int waves, int64_t slot
     L.nf = take(4 * rows);
     L.capl = take(4 * rows);
     L.ncl = take(4 * rows);
-    L.prin = take(rows);
-    L.prout = take(rows);
+    L.chain = take(4 * 2 * rows); // per vertex: predecessor vertex | arc code << 13
     L.loff = take(2 * rows);
     L.llen = take(rows);
     L.path = take(4 * (2 * rows + 8));

@@ -82,6 +82,15 @@ __device__ __forceinline__ int arc_code(int type, int k, int i, int j)
     return type | (k << 2) | (i << 7) | (j << 13);
 }
 
+// Path-walk table: one word per vertex (entry 2q, exit 2q+1 of node q =
+// k*64 + i, so below 4096): the vertex its predecessor arc comes from (13
+// bits) and that arc's code (19 bits).
+constexpr uint32_t kChainMask = 0x1fff;
+constexpr uint32_t kChainDone = 0x1fff; // entry of stage 0 reached from the data node
+constexpr uint32_t kChainBad = 0x1ffe;  // no usable predecessor
+static_assert(2 * kPipeMaxStages * 64 <= 0x1ffe, "vertex ids below the markers");
+__device__ __forceinline__ uint32_t chain_word(uint32_t next, int code) { return next | (uint32_t(code) << 13); }
+
 // predecessors of one node, entry side in the low half, exit side in the high
 __device__ __forceinline__ int pred_in(int pp) { return int(int16_t(pp & 0xffff)); }
 __device__ __forceinline__ int pred_out(int pp) { return pp >> 16; }
@@ -141,8 +150,7 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
     int *nf = reinterpret_cast<int *>(smem + L.nf);               // [S][64] node flow
     int *capl = reinterpret_cast<int *>(smem + L.capl);           // [S][64] node capacity
     int *ncl = reinterpret_cast<int *>(smem + L.ncl);             // [S][64] node compute cost
-    int8_t *prin8 = reinterpret_cast<int8_t *>(smem + L.prin);    // [S][64]
-    int8_t *prout8 = reinterpret_cast<int8_t *>(smem + L.prout);  // [S][64]
+    uint32_t *chain = reinterpret_cast<uint32_t *>(smem + L.chain); // [S][64][entry, exit]
     uint16_t *loff = reinterpret_cast<uint16_t *>(smem + L.loff); // [S][64]
     uint8_t *llen = reinterpret_cast<uint8_t *>(smem + L.llen);   // [S][64]
     int *path = reinterpret_cast<int *>(smem + L.path);           // [2*S*64 + 8]
@@ -166,7 +174,7 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
 
     // ---------------- ingest + validate ----------------
     u32x32 lw[P];
-    int din[P], dout[P], pp[P], seen[P];
+    int din[P], dout[P], pp[P], seen[P], seeny[P];
     uint32_t holes = 0; // bit s: some link into stage k0+s is missing
     int srcc = 0, snkc = 0;
     {
@@ -282,6 +290,7 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
                 dout[s] = kInf;
                 pp[s] = pred_pack(k == 0 ? kPredSrc : kPredNone, kPredNone);
                 seen[s] = kInf;
+                seeny[s] = kInf;
             }
             if (k0 <= klast) {
                 if (k0 >= 1) lds_st(&enmb[w * 64 + lane], uint32_t(din[0]) << 1);
@@ -378,11 +387,14 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
                             dq = di + nc;
                             po = kPredSplit;
                         }
-                        if (k + 1 < S) {
-                            // reverse links: four list entries per pass, partner
-                            // labels from the partner's lane (the loop runs to the
-                            // wave's longest list so every cross-lane read has all
-                            // lanes active)
+                        // reverse links, only when some entry label of stage k+1 dropped
+                        // since this stage last pulled (lists change only between
+                        // searches): four list entries per pass, partner labels from
+                        // the partner's lane (the loop runs to the wave's longest
+                        // list so every cross-lane read has all lanes active)
+                        const bool ydr = Y < seeny[s];
+                        seeny[s] = ydr ? Y : seeny[s];
+                        if (k + 1 < S && __ballot(ydr) != 0) {
                             const int lo = loff[q], len = jv ? llen[q] : 0;
                             int maxlen = len;
 #pragma unroll
@@ -460,70 +472,85 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
             rounds += ps.stop;
             if (fk == ~0ull) break; // sink unreachable: the flow is maximum
 
-            // ---- (2) potentials; stage predecessors ----
+            // ---- (2) stage predecessors ----
             const int Dt = key_label(fk), predt = int(uint32_t(fk));
             const int dred = Dt - pit;
 #pragma unroll
             for (int s = 0; s < P; ++s) {
                 const int k = k0 + s;
                 if (k > klast) break;
-                if (jv) {
-                    int32_t *pin = gpot + 3 + 2 * (k * n + lane);
-                    pin[0] = min(din[s], pin[0] + dred);
-                    pin[1] = min(dout[s], pin[1] + dred);
-                }
-                prin8[k * 64 + lane] = int8_t(pred_in(pp[s]));
-                prout8[k * 64 + lane] = int8_t(pred_out(pp[s]));
+                const int q = k * 64 + lane, pi = pred_in(pp[s]), po = pred_out(pp[s]);
+                uint32_t ein, eout;
+                if (pi == kPredSrc) ein = kChainDone;
+                else if (pi == kPredSplit) ein = chain_word(2 * q + 1, arc_code(kArcSplitRev, k, lane, 0));
+                else if (pi >= 0 && pi < n && k >= 1) ein = chain_word(2 * ((k - 1) * 64 + pi) + 1, arc_code(kArcLinkFwd, k - 1, pi, lane));
+                else ein = kChainBad;
+                if (po == kPredSplit) eout = chain_word(2 * q, arc_code(kArcSplitFwd, k, lane, 0));
+                else if (po >= 0 && po < n && k + 1 < S) eout = chain_word(2 * ((k + 1) * 64 + po), arc_code(kArcLinkRev, k, lane, po));
+                else eout = kChainBad;
+                chain[2 * q] = ein;
+                chain[2 * q + 1] = eout;
             }
             __syncthreads();
-
-            // ---- (3) lane 0 of wave 0: walk, record, bottleneck ----
-            if (tid == 0) {
-                int kk = S - 1, i = predt, len = 0, delta = supply - int(F);
-                bool at_exit = true, okw = predt >= 0 && predt < n;
-                for (int steps_w = 0; okw; ++steps_w) {
-                    if (steps_w > 2 * SN + 4) {
-                        okw = false;
-                        break;
-                    }
-                    const int q = kk * 64 + i;
-                    if (at_exit) {
-                        const int pr = prout8[q];
-                        if (pr == kPredSplit) {
-                            path[len++] = arc_code(kArcSplitFwd, kk, i, 0);
-                            delta = min(delta, capl[q] - nf[q]);
-                            at_exit = false;
-                        } else if (pr >= 0 && pr < n && kk + 1 < S) {
-                            int amt = 0;
-                            for (int e = loff[q]; e < loff[q] + llen[q]; ++e)
-                                if (int(lent[e] & 255u) == pr) amt = lamt[e];
-                            path[len++] = arc_code(kArcLinkRev, kk, i, pr);
-                            delta = min(delta, amt);
-                            kk = kk + 1;
-                            i = pr;
-                            at_exit = false;
-                        } else {
-                            okw = false;
-                        }
-                    } else {
-                        const int pr = prin8[q];
-                        if (pr == kPredSrc) break;
-                        if (pr == kPredSplit) {
-                            path[len++] = arc_code(kArcSplitRev, kk, i, 0);
-                            delta = min(delta, nf[q]);
-                            at_exit = true;
-                        } else if (pr >= 0 && pr < n && kk >= 1) {
-                            path[len++] = arc_code(kArcLinkFwd, kk - 1, pr, i);
-                            kk = kk - 1;
-                            i = pr;
-                            at_exit = true;
-                        } else {
-                            okw = false;
-                        }
+            // potentials of this wave's nodes (the other waves do theirs while
+            // wave 0 walks; wave 0 after its walk)
+            auto update_potentials = [&]() {
+#pragma unroll
+                for (int s = 0; s < P; ++s) {
+                    const int k = k0 + s;
+                    if (k <= klast && jv) {
+                        int32_t *pin = gpot + 3 + 2 * (k * n + lane);
+                        const int a = pin[0], c = pin[1];
+                        pin[0] = min(din[s], a + dred);
+                        pin[1] = min(dout[s], c + dred);
                     }
                 }
-                ps.plen = okw ? len : -1;
-                ps.delta = delta;
+            };
+            if (w != 0) update_potentials();
+
+            // ---- (3) wave 0: lane 0 walks the predecessor chain, then the
+            // whole wave takes the bottleneck over the recorded arcs ----
+            if (w == 0) {
+                // the whole wave follows the chain (uniform values); lane 0 records
+                {
+                    int len = 0;
+                    bool okw = predt >= 0 && predt < n;
+                    uint32_t v = 2 * ((S - 1) * 64 + predt) + 1;
+                    while (okw) {
+                        const uint32_t word = __builtin_amdgcn_readfirstlane(chain[v]);
+                        const uint32_t nx = word & kChainMask;
+                        if (nx == kChainDone) break;
+                        if (nx == kChainBad || len > 2 * SN + 4) {
+                            okw = false;
+                            break;
+                        }
+                        if (lane == 0) path[len] = int(word >> 13);
+                        ++len;
+                        v = nx;
+                    }
+                    if (lane == 0) ps.plen = okw ? len : -1;
+                }
+                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+                __builtin_amdgcn_wave_barrier();
+                const int len = __builtin_amdgcn_readfirstlane(ps.plen);
+                int r = supply - int(F);
+                for (int e = lane; e < len; e += 64) {
+                    const int code = path[e], type = code & 3, kk = (code >> 2) & 31;
+                    const int i = (code >> 7) & 63, j = (code >> 13) & 63;
+                    const int q = kk * 64 + i;
+                    if (type == kArcSplitFwd) r = min(r, capl[q] - nf[q]);
+                    else if (type == kArcSplitRev) r = min(r, nf[q]);
+                    else if (type == kArcLinkRev) {
+                        int amt = 0;
+                        for (int x = loff[q]; x < loff[q] + llen[q]; ++x)
+                            if (int(lent[x] & 255u) == j) amt = lamt[x];
+                        r = min(r, amt);
+                    }
+                }
+#pragma unroll
+                for (int off = 32; off > 0; off >>= 1) r = min(r, __shfl_xor(r, off));
+                if (lane == 0) ps.delta = r;
+                update_potentials();
             }
             __syncthreads();
             const int len = ps.plen, delta = ps.delta;
