@@ -125,7 +125,7 @@ __device__ __forceinline__ int mailbox_wait(const uint32_t *mb, uint32_t par, co
             why = 2;
             return kInf;
         }
-        __builtin_amdgcn_s_sleep(1);
+        __builtin_amdgcn_s_sleep(4);
     }
 }
 
