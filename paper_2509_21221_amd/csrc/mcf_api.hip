@@ -35,7 +35,7 @@ struct gwtf_mcf {
     size_t grid_lds = 0;
     uint32_t *g_ex = nullptr, *g_en = nullptr, *g_ring = nullptr;
     unsigned long long *g_ring_key = nullptr;
-    int32_t *g_pred = nullptr, *g_path = nullptr, *g_path_j = nullptr, *g_ctrl = nullptr;
+    int32_t *g_pred = nullptr, *g_path = nullptr, *g_ctrl = nullptr;
     int32_t solved = 0; // batch size of the last successful solve (0 = none)
 };
 
@@ -82,7 +82,6 @@ void free_ws(gwtf_mcf_t *h)
     (void)hipFree(h->g_en);
     (void)hipFree(h->g_pred);
     (void)hipFree(h->g_path);
-    (void)hipFree(h->g_path_j);
     (void)hipFree(h->g_ctrl);
     (void)hipFree(h->g_ring);
     (void)hipFree(h->g_ring_key);
@@ -91,7 +90,7 @@ void free_ws(gwtf_mcf_t *h)
     h->state = nullptr;
     h->g_ex = h->g_en = h->g_ring = nullptr;
     h->g_ring_key = nullptr;
-    h->g_pred = h->g_path = h->g_path_j = h->g_ctrl = nullptr;
+    h->g_pred = h->g_path = h->g_ctrl = nullptr;
 }
 
 } // namespace
@@ -170,7 +169,6 @@ extern "C" gwtf_status_t gwtf_mcf_create(const gwtf_mcf_shape_t *shape, void *hi
         {(void **)&h->g_en, sizeof(uint32_t) * 2 * gsn},
         {(void **)&h->g_pred, sizeof(int32_t) * gsn},
         {(void **)&h->g_path, sizeof(int32_t) * (2 * gsn + 8)},
-        {(void **)&h->g_path_j, sizeof(int32_t) * (2 * gsn + 8)},
         {(void **)&h->g_ctrl, sizeof(int32_t) * kGridCtrlInts},
         {(void **)&h->g_ring, h->grid ? sizeof(uint32_t) * grid_ring_slots(S) : 0},
         {(void **)&h->g_ring_key, h->grid ? sizeof(unsigned long long) * grid_ring_slots(S) : 0},
@@ -245,7 +243,6 @@ extern "C" gwtf_status_t gwtf_mcf_solve_batch(gwtf_mcf_t *h, const gwtf_mcf_batc
         gp.en = h->g_en;
         gp.pred = h->g_pred;
         gp.path = h->g_path;
-        gp.path_j = h->g_path_j;
         gp.ctrl = h->g_ctrl;
         gp.ring = h->g_ring;
         gp.ring_key = h->g_ring_key;

@@ -22,7 +22,6 @@ struct GridParams {
     int32_t ring_slots; // > S + 2: iterations in flight at once across the stages
     int32_t *pred;      // [S*n] entry predecessor (low 16 bits) and exit predecessor (high)
     int32_t *path;      // [2*S*n + 8] arc codes of the augmenting path
-    int32_t *path_j;    // [2*S*n + 8] head node of each link arc on the path
     int32_t *ctrl;      // [kGridCtrlInts], cleared before each launch
 };
 inline int grid_ring_slots(int S) { return S + 8; }

@@ -53,6 +53,15 @@ constexpr uint32_t kPackLimit = (1u << 22) - (1u << 16);
 constexpr uint32_t kNoRowKey = 0xfe000000u; // row without a new label; + cost << 9 cannot wrap
 
 enum : int { kArcSplitFwd = 0, kArcSplitRev = 1, kArcLinkFwd = 2, kArcLinkRev = 3 };
+// Path arc codes: type | stage << 2 | node << 12 | head << 21.  Splits name
+// their node; links name their tail exit (the link's stage and row) and the
+// head node in the next stage.
+__device__ __forceinline__ int path_code(int type, int k, int i, int j) { return type | (k << 2) | (i << 12) | (j << 21); }
+__device__ __forceinline__ int code_type(int c) { return c & 3; }
+__device__ __forceinline__ int code_stage(int c) { return (c >> 2) & 1023; }
+__device__ __forceinline__ int code_node(int c) { return (c >> 12) & 511; }
+__device__ __forceinline__ int code_head(int c) { return (c >> 21) & 511; }
+constexpr int kPathLds = 1024; // path arcs workgroup 0 keeps in LDS (the rest only in memory)
 // grid-wide status bits
 enum : int { kFlagBad = 1, kFlagWide = 2, kFlagLists = 4, kFlagFault = 8 };
 // control words (int32 indices into GridParams::ctrl)
@@ -143,7 +152,7 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
     extern __shared__ __align__(16) unsigned char smem[];
     __shared__ int sh_ok, sh_flag, sh_bad, sh_maxc, sh_changed, sh_len, sh_delta, sh_fault, sh_why[2];
     __shared__ unsigned long long sh_key;
-    __shared__ int wcnt[kGridWaves], wmaxd[kGridWaves];
+    __shared__ int wcnt[kGridWaves], wmaxd[kGridWaves], wendrop[kGridWaves];
 
     // ---- LDS layout (same offsets in every workgroup) ----
     // The leading area holds the link-cost block; workgroup 0 (no incoming
@@ -163,6 +172,7 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
     int *din = reinterpret_cast<int *>(take(4 * kGridNB));
     int *dout = reinterpret_cast<int *>(take(4 * kGridNB));
     int *pout = reinterpret_cast<int *>(take(4 * kGridNB));
+    int *pin = reinterpret_cast<int *>(take(4 * kGridNB));
     int *flow = reinterpret_cast<int *>(take(4 * kGridNB));
     int *cap = reinterpret_cast<int *>(take(4 * kGridNB));
     int *ncost = reinterpret_cast<int *>(take(4 * kGridNB));
@@ -218,6 +228,7 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
         snkc[c] = z;
         flow[c] = 0;
         pout[c] = 0;
+        pin[c] = 0;
         if (own) {
             st(&gnf[q], 0);
             gpot[3 + 2 * q] = 0;
@@ -295,7 +306,10 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
                 st(&gp.en[SN + q], (uint32_t(kInf) << 2) | 3u);
             }
         }
-        for (int i = tid; i < n; i += kGridThreads) exrow[i] = kInf;
+        for (int i = tid; i < n; i += kGridThreads) {
+            exrow[i] = kInf;
+            enrow[i] = kInf;
+        }
         if (g == 0) {
             for (int r = tid; r < gp.ring_slots; r += kGridThreads) {
                 st(&gp.ring[r], 0u);
@@ -357,6 +371,7 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
                 }
                 if (why) atomicOr(&sh_why[t & 1], why);
                 int dropped = 0, dnew = 0;
+                bool en_drop = false;
                 if (tid < n) {
                     if (has_prev) {
                         dnew = int(wex >> 2);
@@ -364,15 +379,21 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
                         if (dropped) exrow[tid] = dnew;
                         rowkey[tid] = dropped ? (uint32_t(dnew) << 9) | uint32_t(tid) : kNoRowKey;
                     }
-                    if (has_next) enrow[tid] = int(wen >> 2);
+                    if (has_next) {
+                        const int y = int(wen >> 2);
+                        en_drop = y < enrow[tid];
+                        enrow[tid] = y;
+                    }
                 }
                 const uint64_t m = __ballot(dropped);
+                const int en_any = __any(en_drop) ? 1 : 0;
                 int wmax = dropped ? dnew : 0;
 #pragma unroll
                 for (int off = 32; off > 0; off >>= 1) wmax = max(wmax, __shfl_xor(wmax, off));
                 if (lane == 0) {
                     wcnt[wave] = __popcll(m);
                     wmaxd[wave] = wmax;
+                    wendrop[wave] = en_any;
                 }
                 __syncthreads();
                 const int whyb = sh_why[t & 1];
@@ -382,12 +403,13 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
                     break;
                 }
                 if (tid == 0) sh_why[(t + 1) & 1] = 0;
-                int base = 0, nrows = 0, maxd = 0;
+                int base = 0, nrows = 0, maxd = 0, pull = 0;
                 for (int w = 0; w < kGridWaves; ++w) {
                     const int cnt = wcnt[w];
                     base += w < wave ? cnt : 0;
                     nrows += cnt;
                     maxd = max(maxd, wmaxd[w]);
+                    pull |= wendrop[w];
                 }
                 // Packed keys while labels allow; a stage where most rows
                 // dropped is swept densely by row index, otherwise through
@@ -480,7 +502,9 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
                         dq = di + nc;
                         po = kPredSplit;
                     }
-                    if (has_next) {
+                    // reverse links: only when an entry label of stage k+1 dropped
+                    // since the last pull (the lists change only between searches)
+                    if (has_next && pull) {
                         const int lo = loff[c], hi = lo + llen[c];
 #pragma unroll 4
                         for (int e = lo; e < hi; ++e) {
@@ -548,7 +572,7 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
             if (tid < nown) {
                 const int c = tid, q = k * n + j0 + c;
                 pout[c] = min(dout[c], pout[c] + dred);
-                gpot[3 + 2 * q] = min(din[c], gpot[3 + 2 * q] + dred);
+                pin[c] = min(din[c], pin[c] + dred);
                 st(&gp.pred[q], (prin[c] & 0xffff) | (prout[c] << 16));
             }
             if (!bar.sync(&sh_ok, &sh_flag)) {
@@ -571,26 +595,27 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
                     for (; q < SN; q += kGridThreads) all_pred[q] = ld(&gp.pred[q]);
                 }
                 __syncthreads();
-                if (tid == 0) {
+                // Wave 0 follows the predecessors from the sink (uniform values:
+                // every lane walks, lane 0 records); one predecessor word serves
+                // both vertices of a node.  The first kPathLds arcs stay in LDS.
+                int *lpath = reinterpret_cast<int *>(red);
+                if (wave == 0) {
                     int kk = S - 1, i = predt, len = 0;
                     bool at_exit = true, okw = predt >= 0 && predt < n;
-                    for (int steps = 0; okw; ++steps) {
-                        if (steps > 2 * SN + 4) {
+                    while (okw) {
+                        if (len > 2 * SN + 4) {
                             okw = false;
                             break;
                         }
-                        // Arc codes: type | stage << 2 | node << 12.  Splits
-                        // name their node; links name their tail exit (the
-                        // link's stage and row) and keep the head in path_j.
-                        int code, ak = kk, ai = i, j = 0;
+                        const int word = __builtin_amdgcn_readfirstlane(all_pred[kk * n + i]);
+                        int code;
                         if (at_exit) {
-                            const int pr = all_pred[kk * n + i] >> 16;
+                            const int pr = word >> 16;
                             if (pr == kPredSplit) {
-                                code = kArcSplitFwd; // entry -> exit of (kk, i)
+                                code = path_code(kArcSplitFwd, kk, i, 0);
                                 at_exit = false;
                             } else if (pr >= 0 && pr < n && kk + 1 < S) {
-                                code = kArcLinkRev; // entry (kk+1, pr) -> exit (kk, i)
-                                j = pr;
+                                code = path_code(kArcLinkRev, kk, i, pr); // entry (kk+1, pr) -> exit (kk, i)
                                 kk = kk + 1;
                                 i = pr;
                                 at_exit = false;
@@ -599,16 +624,13 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
                                 break;
                             }
                         } else {
-                            const int pr = int(int16_t(all_pred[kk * n + i] & 0xffff));
+                            const int pr = int(int16_t(word & 0xffff));
                             if (pr == kPredSrc) break;
                             if (pr == kPredSplit) {
-                                code = kArcSplitRev; // exit -> entry of (kk, i)
+                                code = path_code(kArcSplitRev, kk, i, 0);
                                 at_exit = true;
                             } else if (pr >= 0 && pr < n && kk >= 1) {
-                                code = kArcLinkFwd; // exit (kk-1, pr) -> entry (kk, i)
-                                ak = kk - 1;
-                                ai = pr;
-                                j = i;
+                                code = path_code(kArcLinkFwd, kk - 1, pr, i); // exit (kk-1, pr) -> entry (kk, i)
                                 kk = kk - 1;
                                 i = pr;
                                 at_exit = true;
@@ -617,23 +639,28 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
                                 break;
                             }
                         }
-                        st(&gp.path[len], code | (ak << 2) | (ai << 12));
-                        st(&gp.path_j[len], j);
+                        if (lane == 0) {
+                            if (len < kPathLds) lpath[len] = code;
+                            else st(&gp.path[len], code);
+                        }
                         ++len;
                     }
-                    sh_len = okw ? len : -1;
-                    sh_delta = supply - int(F);
+                    if (lane == 0) {
+                        sh_len = okw ? len : -1;
+                        sh_delta = supply - int(F);
+                    }
                 }
                 __syncthreads();
                 const int len = sh_len;
                 if (len >= 0) {
                     int r = 0x7fffffff;
                     for (int e = tid; e < len; e += kGridThreads) {
-                        const int code = ld(&gp.path[e]), type = code & 3, ak = (code >> 2) & 1023, ai = code >> 12;
-                        const int q = ak * n + ai;
+                        const int code = e < kPathLds ? lpath[e] : ld(&gp.path[e]);
+                        if (e < kPathLds) st(&gp.path[e], code);
+                        const int type = code_type(code), q = code_stage(code) * n + code_node(code);
                         if (type == kArcSplitFwd) r = min(r, gcap[q] - ld(&gnf[q]));
                         else if (type == kArcSplitRev) r = min(r, ld(&gnf[q]));
-                        else if (type == kArcLinkRev) r = min(r, ld(&gaf[size_t(q) * n + ld(&gp.path_j[e])]));
+                        else if (type == kArcLinkRev) r = min(r, ld(&gaf[size_t(q) * n + code_head(code)]));
                     }
                     atomicMin(&sh_delta, r);
                 }
@@ -656,9 +683,9 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
             }
             for (int pass = 0; pass < 2; ++pass) {
                 for (int e = tid; e < len; e += kGridThreads) {
-                    const int code = ld(&gp.path[e]), type = code & 3, ak = (code >> 2) & 1023, ai = code >> 12;
+                    const int code = ld(&gp.path[e]), type = code_type(code), ak = code_stage(code), ai = code_node(code);
                     if (ak != k || ai < j0 || ai >= j0 + nown) continue;
-                    const int c = ai - j0, q = ak * n + ai, j = ld(&gp.path_j[e]);
+                    const int c = ai - j0, q = ak * n + ai, j = code_head(code);
                     if (unsigned(j) >= unsigned(n)) {
                         sh_fault = 1;
                         continue;
@@ -737,6 +764,7 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
     const bool ok = status == 0 && !fault;
     if (tid < nown) {
         const int q = k * n + j0 + tid;
+        gpot[3 + 2 * q] = ok ? pin[tid] : 0;
         gpot[4 + 2 * q] = ok ? pout[tid] : 0;
         if (!ok) {
             gpot[3 + 2 * q] = 0;
@@ -771,7 +799,7 @@ size_t lds_fixed(int S, int n)
 {
     size_t o = align16(grid_pass_big_bytes(S, n));
     for (int a = 0; a < 4; ++a) o = align16(o + 4 * size_t(n));
-    for (int a = 0; a < 12; ++a) o = align16(o + 4 * size_t(kGridNB));
+    for (int a = 0; a < 13; ++a) o = align16(o + 4 * size_t(kGridNB));
     o = align16(o + 8 * size_t(kGridRowGroups) * kGridNB);
     return o;
 }
