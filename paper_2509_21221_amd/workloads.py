@@ -273,3 +273,119 @@ def concat(batches) -> Batch:
     cat = lambda key: np.ascontiguousarray(np.concatenate([getattr(x, key) for x in batches]))
     return Batch(S, n, cat("node_cap"), cat("node_cost"), cat("arc_cost"),
                  cat("src_cost"), cat("snk_cost"), cat("supply"), name=batches[0].name)
+
+
+@dataclass
+class Candidates:
+    """m nodes that may join a pipeline, with their costs for every stage
+    (paper Sec. VI, handling joining nodes: every candidate knows its costs
+    for each stage).  All int32, C-contiguous:
+
+        cap  [m][S]     memory capacity if it joins stage k
+        cost [m][S]     compute cost if it joins stage k
+        inn  [m][S][n]  delay from node i of stage k-1 to it in stage k
+                        (row k = 0 unused)
+        out  [m][S][n]  delay from it in stage k to node j of stage k+1
+                        (row k = S-1 unused)
+        link [m][m]     delay from candidate c (stage k) to d (stage k+1)
+        src  [m]        data node -> it, when it joins stage 0
+        snk  [m]        it -> data node, when it joins stage S-1
+    """
+
+    cap: np.ndarray
+    cost: np.ndarray
+    inn: np.ndarray
+    out: np.ndarray
+    link: np.ndarray
+    src: np.ndarray
+    snk: np.ndarray
+
+    @property
+    def m(self) -> int:
+        return int(self.cap.shape[0])
+
+    def permuted(self, order) -> "Candidates":
+        """The same candidates listed in another order."""
+        o = np.asarray(order, dtype=np.int64)
+        return Candidates(*(np.ascontiguousarray(a[o]) for a in (self.cap, self.cost, self.inn,
+                                                                 self.out)),
+                          np.ascontiguousarray(self.link[o][:, o]),
+                          np.ascontiguousarray(self.src[o]), np.ascontiguousarray(self.snk[o]))
+
+
+# Node-addition settings of the paper's test table (Sec. VI): stages,
+# capacity range, inter-stage (link) cost range, each floor(U(a, b)).
+NODE_ADD_SETTINGS = {1: (8, (1, 20), (1, 100)), 2: (8, (1, 20), (20, 100)),
+                     3: (8, (1, 5), (1, 100)), 4: (12, (1, 20), (1, 100))}
+
+
+def node_addition(setting: int = 1, instance: int = 0, supply: int = 64):
+    """One what-if problem of the paper's node-addition tests (Sec. VI):
+    96 relays (97 nodes, one of them the data holder) split evenly over the
+    stages, plus one empty position per stage (the last) for a joining node,
+    and S candidates, one per stage in every placement.
+
+    Capacities floor(U(a, b)); every link delay (between relays, with the
+    data node, and of the candidates) floor(U(a, b)); a node's compute cost
+    is phi + floor(U(50, 100)), phi being the largest delay of its links
+    into and out of its stage (for a candidate, of the stage it would join).
+    The empty position has capacity 0 and no links.  The data node's supply
+    is not given by the paper; ``supply`` microbatches (64, as in the
+    8 x 8 preset) are pushed.
+
+    Returns (base Batch with B = 1, slot, Candidates)."""
+    S, (clo, chi), (alo, ahi) = NODE_ADD_SETTINGS[setting]
+    n0 = 96 // S
+    n = n0 + 1
+    slot = n - 1
+    rng = _rng(200 + setting, instance)
+    flo = lambda lo, hi, size: np.floor(rng.uniform(lo, hi, size=size)).astype(np.int32)
+    base = _empty(1, S, n, f"node-addition setting {setting}")
+    cap = np.zeros((S, n), np.int32)
+    cap[:, :n0] = flo(clo, chi, (S, n0))
+    arc = np.full((max(S - 1, 0), n, n), NO_ARC, np.int32)
+    arc[:, :n0, :n0] = flo(alo, ahi, (S - 1, n0, n0))
+    src = np.zeros(n, np.int32)
+    snk = np.zeros(n, np.int32)
+    src[:n0] = flo(alo, ahi, n0)
+    snk[:n0] = flo(alo, ahi, n0)
+    phi = np.zeros((S, n0), np.int32)
+    for k in range(S):
+        into = src[None, :n0] if k == 0 else arc[k - 1, :n0, :n0]
+        outof = snk[None, :n0].T if k == S - 1 else arc[k, :n0, :n0].T
+        phi[k] = np.maximum(into.max(axis=0), outof.max(axis=0))
+    cost = np.zeros((S, n), np.int32)
+    cost[:, :n0] = phi + flo(50, 100, (S, n0))
+    base.node_cap[0], base.node_cost[0], base.arc_cost[0] = cap, cost, arc
+    base.src_cost[0], base.snk_cost[0], base.supply[0] = src, snk, supply
+
+    m = S
+    ccap = np.repeat(flo(clo, chi, (m, 1)), S, axis=1)
+    inn = flo(alo, ahi, (m, S, n))
+    out = flo(alo, ahi, (m, S, n))
+    inn[:, :, slot] = flo(alo, ahi, (m, S))
+    inn[:, 0, :] = 0
+    out[:, S - 1, :] = 0
+    link = flo(alo, ahi, (m, m))
+    csrc, csnk = flo(alo, ahi, m), flo(alo, ahi, m)
+    cphi = np.maximum(inn[:, :, :n0].max(axis=2), out[:, :, :n0].max(axis=2))
+    cphi[:, 0] = np.maximum(csrc, out[:, 0, :n0].max(axis=1))
+    cphi[:, S - 1] = np.maximum(csnk, inn[:, S - 1, :n0].max(axis=1))
+    ccost = (cphi + flo(50, 100, (m, S))).astype(np.int32)
+    c = Candidates(ccap, ccost, inn, out, link, csrc, csnk)
+    return base, slot, c
+
+
+def random_candidates(S: int, n: int, m: int, seed: int, cap_hi: int = 3, cost_hi: int = 20,
+                      holes: float = 0.0) -> Candidates:
+    """Small random candidates for exhaustive and cross-library checks:
+    capacities U[0, cap_hi], costs U[0, cost_hi], a fraction ``holes`` of
+    their links missing (NO_ARC)."""
+    rng = np.random.default_rng(np.random.SeedSequence(seed, spawn_key=(S, n, m, 7)))
+    u = lambda lo, hi, size: _int_uniform(rng, lo, hi, size)
+    inn, out, link = u(0, cost_hi, (m, S, n)), u(0, cost_hi, (m, S, n)), u(0, cost_hi, (m, m))
+    if holes > 0:
+        for a in (inn, out, link):
+            a[rng.random(a.shape) < holes] = NO_ARC
+    return Candidates(u(0, cap_hi, (m, S)), u(0, cost_hi, (m, S)), inn, out, link,
+                      u(0, cost_hi, m), u(0, cost_hi, m))

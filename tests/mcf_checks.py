@@ -253,3 +253,57 @@ def certify(batch, b, F, cost, node_flow, arc_flow, src_flow, snk_flow, potentia
         cut = int(cap[reach_in & ~reach_out].sum())
         assert cut == F, f"min cut {cut} != F {F}"
     return True
+
+
+def networkx_with_candidates(base, slot, cands, stages):
+    """(F, cost) of one what-if placement, built without slots: each stage
+    holds the base nodes, except that a stage receiving candidate c holds c
+    in place of the base node at ``slot``; links are looked up by the kind of
+    their two ends (base-base, base-candidate, candidate-base,
+    candidate-candidate).  networkx's max_flow_min_cost solves it."""
+    import networkx as nx
+
+    S, n = base.S, base.n
+    cap, ncost, arc, src, snk, supply = _inst(base, 0)
+    who = {k: c for c, k in enumerate(stages)}
+    nodes = []
+    for k in range(S):
+        row = [("base", i) for i in range(n) if not (i == slot and k in who)]
+        if k in who:
+            row.append(("cand", who[k]))
+        nodes.append(row)
+
+    def node_cap(k, u):
+        return int(cands.cap[u[1]][k]) if u[0] == "cand" else int(cap[k, u[1]])
+
+    def node_cost(k, u):
+        return int(cands.cost[u[1]][k]) if u[0] == "cand" else int(ncost[k, u[1]])
+
+    def link(k, u, v):
+        if u[0] == "base" and v[0] == "base":
+            return int(arc[k, u[1], v[1]])
+        if u[0] == "base":
+            return int(cands.inn[v[1]][k + 1][u[1]])
+        if v[0] == "base":
+            return int(cands.out[u[1]][k][v[1]])
+        return int(cands.link[u[1]][v[1]])
+
+    G = nx.DiGraph()
+    G.add_edge("s0", "s", capacity=supply, weight=0)
+    for u in nodes[0]:
+        G.add_edge("s", ("in", 0, u), weight=int(cands.src[u[1]]) if u[0] == "cand" else int(src[u[1]]))
+    for u in nodes[S - 1]:
+        G.add_edge(("out", S - 1, u), "t", weight=int(cands.snk[u[1]]) if u[0] == "cand" else int(snk[u[1]]))
+    for k in range(S):
+        for u in nodes[k]:
+            G.add_edge(("in", k, u), ("out", k, u), capacity=node_cap(k, u), weight=node_cost(k, u))
+    for k in range(S - 1):
+        for u in nodes[k]:
+            for v in nodes[k + 1]:
+                d = link(k, u, v)
+                if d != NO_ARC:
+                    G.add_edge(("out", k, u), ("in", k + 1, v), weight=d)
+    if "t" not in G:
+        return 0, 0
+    flow = nx.max_flow_min_cost(G, "s0", "t")
+    return int(sum(flow["s0"].values())), int(nx.cost_of_flow(G, flow))
