@@ -1,6 +1,7 @@
 """Benchmark: batched min-cost max-flow on MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 4]
+    python bench.py --whatif 1        # what-if node addition, paper setting 1
 
 A step solves one whole batch of the workload (every instance to optimality)
 with inputs already resident in HBM.  The default workload is the 7B-scale
@@ -9,6 +10,12 @@ links between consecutive stages (10 locations, supply 512).  Prints one JSON
 line: instances solved per second (the value), arc relaxations per second,
 the roofline of the solver kernel, and the CPU oracle's rate on a bounded
 sample of the same workload.
+
+With --whatif SETTING a step instead evaluates every placement of the
+paper's node-addition test (Sec. VI, handling joining nodes; settings 1-3:
+8 stages of 12 relays plus one joining position, 8 candidates, 8! = 40320
+placements): expand all placements on the device, solve them, reduce to the
+best placement.  The value is placements evaluated per second.
 """
 from __future__ import annotations
 
@@ -44,7 +51,8 @@ def measured_traffic(kernel: str, config: int, kernel_s: float):
     taken."""
     import hashlib
 
-    path = os.path.join(ROOT, "profiles", f"{kernel}_c{config}_traffic.json")
+    tag = config if isinstance(config, str) else f"c{config}"
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{tag}_traffic.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
@@ -100,12 +108,133 @@ def cpu_baseline(batch, budget_s: float, threads: int):
             "arc_scans_per_s": scans / t_used}
 
 
+def whatif_cpu_baseline(base, slot, cands, total: int, budget_s: float, threads: int):
+    """The oracle (expansion and solve) on the host cores, on a bounded prefix
+    of the placements."""
+    import oracle
+    import oracle.whatif as OW
+
+    done, t_used, chunk = 0, 0.0, 256
+    while done < total and t_used < budget_s:
+        cnt = min(chunk, total - done)
+        t0 = time.perf_counter()
+        batch = OW.expand(base, slot, cands, done, cnt)
+        r = oracle.solve(batch, nthreads=threads, flows=False, potentials=False)
+        t_used += time.perf_counter() - t0
+        done += cnt
+        used = r["threads"]
+    return {"value": done / t_used, "unit": "placements/s", "cores": used, "kind": "oracle",
+            "sample": f"first {done} of {total} placements of the same problem, expanded and solved, "
+                      f"{t_used:.1f} s wall on {used} threads"}
+
+
+def run_whatif(args):
+    """Time whole what-if evaluations: expand + solve + best placement."""
+    import numpy as np
+    import torch
+
+    from paper_2509_21221_amd import workloads as W
+    from paper_2509_21221_amd.mcf import Solver, gwtf_whatif_count
+
+    base, slot, cands = W.node_addition(args.whatif)
+    S, n = base.S, base.n
+    total = gwtf_whatif_count(S, cands.m)
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    bt = {"node_cap": t(base.node_cap), "node_cost": t(base.node_cost), "arc_cost": t(base.arc_cost),
+          "src_cost": t(base.src_cost), "snk_cost": t(base.snk_cost), "supply": t(base.supply)}
+    ct = {"cap": t(cands.cap), "cost": t(cands.cost), "in_cost": t(cands.inn), "out_cost": t(cands.out),
+          "link_cost": t(cands.link), "src_cost": t(cands.src), "snk_cost": t(cands.snk)}
+    stream = torch.cuda.current_stream(dev)
+    solver = Solver(S, n, total, device=0, stream=stream)
+    e = lambda *shape, dt=torch.int32: torch.empty(shape, dtype=dt, device=dev)
+    batch = {"node_cap": e(total, S, n), "node_cost": e(total, S, n), "arc_cost": e(total, S - 1, n, n),
+             "src_cost": e(total, n), "snk_cost": e(total, n), "supply": e(total)}
+    outs = (e(total, dt=torch.int64), e(total, dt=torch.int64), e(total))
+    best = e(3, dt=torch.int64)
+
+    def step():
+        solver.whatif_expand(bt, ct, slot, 0, total, out=batch)
+        solver.solve(batch["node_cap"], batch["node_cost"], batch["arc_cost"], batch["supply"],
+                     src_cost=batch["src_cost"], snk_cost=batch["snk_cost"], out=outs)
+        solver.whatif_best(*outs, first=0, best=best)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    # phase split of one evaluation, on the solver's stream
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    ev[0].record(stream)
+    solver.whatif_expand(bt, ct, slot, 0, total, out=batch)
+    ev[1].record(stream)
+    solver.solve(batch["node_cap"], batch["node_cost"], batch["arc_cost"], batch["supply"],
+                 src_cost=batch["src_cost"], snk_cost=batch["snk_cost"], out=outs)
+    ev[2].record(stream)
+    solver.whatif_best(*outs, first=0, best=best)
+    ev[3].record(stream)
+    torch.cuda.synchronize()
+    expand_ms, solve_ms, best_ms = (ev[i].elapsed_time(ev[i + 1]) for i in range(3))
+
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        starts[k].record(stream)
+        step()
+        ends[k].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    status = outs[2].cpu().numpy()
+    if (status != 0).any():
+        raise SystemExit(f"solver reported non-ok status on {(status != 0).sum()} placements")
+    stats = solver.stats().cpu().numpy()
+    passes = solver.passes().cpu().numpy()
+    main_pass = int(np.bincount(passes).argmax())
+    relax = int(stats[:, 2].sum()) * n + int(stats[:, 3].sum())
+    solve_s = solve_ms / 1e3
+    achieved = BYTES_PER_RELAX * relax / solve_s / 1e9
+    b = best.cpu().numpy()
+    inst_ints = 2 * S * n + (S - 1) * n * n + 2 * n + 1
+    line = {
+        "metric": "what-if placements evaluated/sec (expand + solve + best placement)",
+        "value": total * args.steps / wall,
+        "unit": "placements/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": wall / args.steps * 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "int32", "data": "synthetic (seeded generator, paper-shaped)",
+        "config": {"workload": f"node addition setting {args.whatif}: S={S} x n={n} ({n - 1} relays + 1 "
+                               f"joining position), {cands.m} candidates, {total} placements, supply "
+                               f"{int(base.supply[0])}", "placements": total, "stages": S,
+                   "nodes_per_stage": n, "seed": 0},
+        "best_placement": {"index": int(b[0]), "F": int(b[1]), "cost": int(b[2])},
+        "phase_ms": {"expand": expand_ms, "solve": solve_ms, "best": best_ms},
+        "expand_write_GBs": 4 * inst_ints * total / (expand_ms / 1e3) / 1e9,
+        "arc_relaxations_per_s": relax / solve_s,
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": measured_traffic(KERNEL_SYMBOLS.get(main_pass, "?"), f"whatif{args.whatif}",
+                                                 solve_s),
+                     "kernel": KERNELS.get(main_pass, "?") + " (one launch per step)",
+                     "kernel_ms": solve_ms},
+    }
+    if args.cpu_budget > 0:
+        threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+        threads = max(1, min(threads, os.cpu_count() or 1))
+        line["cpu_baseline"] = whatif_cpu_baseline(base, slot, cands, total, args.cpu_budget, threads)
+    solver.close()
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", type=int, default=4, choices=sorted(WORKLOADS))
+    ap.add_argument("--whatif", type=int, default=0, choices=[0, 1, 2, 3],
+                    help="time what-if node addition for this paper setting instead (0 = off)")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle time for the CPU baseline (0 = skip)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -126,6 +255,9 @@ def main():
         print(f"bench.py runs on one GPU only: this solver has no multi-GPU path "
               f"(--gpus {args.gpus} requested)", file=sys.stderr)
         sys.exit(2)
+
+    if args.whatif:
+        return run_whatif(args)
 
     import numpy as np
     import torch

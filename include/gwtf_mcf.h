@@ -126,6 +126,78 @@ gwtf_status_t gwtf_mcf_get_stats(gwtf_mcf_t *h, int32_t first, int32_t count, in
  * handle's stream; errors as for gwtf_mcf_get_stats. */
 gwtf_status_t gwtf_mcf_get_passes(gwtf_mcf_t *h, int32_t first, int32_t count, int32_t *pass);
 
+/* ---- What-if node addition (paper Sec. VI, handling joining nodes; the
+ * joining example of Sec. V-B) ----
+ *
+ * The paper places joining nodes by solving the flow problem once for every
+ * way of assigning the candidate nodes to stages and keeping the best
+ * assignment.  These calls build that batch of instances on the device
+ * (gwtf_mcf_whatif_expand), leave the solve to gwtf_mcf_solve_batch, and
+ * reduce its results to the best placement (gwtf_mcf_whatif_best).
+ *
+ * A placement sends each of m candidates to a different stage (0 <= m <= S);
+ * placements are numbered 0 .. S!/(S-m)! - 1 in lexicographic order of
+ * (stage of candidate 0, stage of candidate 1, ...).  Placement p is the
+ * base instance with, in every stage k that receives candidate c, node
+ * position `slot` replaced by c: its capacity cap[c][k], compute cost
+ * cost[c][k], links in_cost[c][k][i] from node i of stage k-1 and
+ * out_cost[c][k][j] to node j of stage k+1, link_cost[c][d] to candidate d
+ * when d sits in stage k+1, and src_cost[c] / snk_cost[c] to the data node
+ * when k is 0 / S-1.  Stages without a candidate keep the base's node at
+ * `slot` (an empty position has capacity 0). */
+typedef struct {
+    int32_t num_candidates;   /* m, 0 <= m <= S, with S!/(S-m)! < 2^63 */
+    int32_t slot;             /* node position a candidate takes, 0 <= slot < n */
+    const int32_t *cap;       /* [m][S] capacity if the candidate joins stage k (NULL iff m == 0) */
+    const int32_t *cost;      /* [m][S] compute cost if it joins stage k (NULL iff m == 0) */
+    const int32_t *in_cost;   /* [m][S][n] delay from node i of stage k-1 (row k = 0 unread);
+                                 NULL iff S == 1 or m == 0 */
+    const int32_t *out_cost;  /* [m][S][n] delay to node j of stage k+1 (row k = S-1 unread);
+                                 NULL iff S == 1 or m == 0 */
+    const int32_t *link_cost; /* [m][m] delay from candidate c to candidate d one stage later;
+                                 NULL iff S == 1 or m == 0 */
+    const int32_t *src_cost;  /* [m] data node -> candidate in stage 0; NULL = all 0 */
+    const int32_t *snk_cost;  /* [m] candidate in stage S-1 -> data node; NULL = all 0 */
+} gwtf_whatif_candidates_t;
+
+/* Caller device buffers for `count` instances in the canonical layout
+ * ([count][S][n] node_cap and node_cost, [count][S-1][n][n] arc_cost (NULL
+ * iff S == 1), [count][n] src_cost and snk_cost, [count] supply). */
+typedef struct {
+    int32_t *node_cap, *node_cost, *arc_cost, *src_cost, *snk_cost, *supply;
+} gwtf_mcf_instances_t;
+
+/* Host-only: *count = S!/(S-m)!, the number of placements of m candidates
+ * over S stages.  GWTF_ERR_INVALID_ARG if S < 1, m < 0, m > S, count is
+ * NULL, or the number does not fit in an int64. */
+gwtf_status_t gwtf_whatif_count(int32_t num_stages, int32_t num_candidates, int64_t *count);
+
+/* Writes placements [first, first + count) into `out` (instance r of `out`
+ * is placement first + r).  `base` is one instance in the batch layout of the
+ * handle's shape (batch must be 1; src_cost / snk_cost may be NULL = 0; the
+ * output fields flow_value, total_cost and status are not used).  Values are
+ * copied as they are: an invalid value reaches the solve, which reports it in
+ * that instance's status.  Requires S <= 1024 and count >= 0; first + count
+ * must not exceed the placement count (GWTF_ERR_RANGE otherwise); with
+ * count == 0 nothing is written and the `out` pointers may be NULL.  All other
+ * argument errors give GWTF_ERR_INVALID_ARG with nothing enqueued.  Enqueued
+ * on the handle's stream; `out` must not overlap any input. */
+gwtf_status_t gwtf_mcf_whatif_expand(gwtf_mcf_t *h, const gwtf_mcf_batch_t *base,
+                                     const gwtf_whatif_candidates_t *cand, int64_t first,
+                                     int32_t count, const gwtf_mcf_instances_t *out);
+
+/* Best placement among `count` solved instances (device arrays, as written
+ * by gwtf_mcf_solve_batch for an expanded batch): among instances with status
+ * GWTF_INST_OK, the largest flow value, then the smallest cost, then the
+ * smallest index.  best (device, int64[3]) receives {first + index, F, cost},
+ * or {-1, 0, 0} when no instance is OK.  With merge != 0 the call keeps the
+ * better of that and what best already holds (same order; an entry with
+ * index -1 loses), so chunks of one placement range can be reduced in turn.
+ * count >= 0; errors as for gwtf_mcf_whatif_expand. */
+gwtf_status_t gwtf_mcf_whatif_best(gwtf_mcf_t *h, int32_t count, const int64_t *flow_value,
+                                   const int64_t *total_cost, const int32_t *status, int64_t first,
+                                   int32_t merge, int64_t *best);
+
 /* Frees the handle and its workspace after draining its stream; NULL-safe. */
 void gwtf_mcf_destroy(gwtf_mcf_t *h);
 

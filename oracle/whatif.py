@@ -111,9 +111,10 @@ def expand(base, slot: int, cands, first: int = 0, count: int | None = None):
     """Placements [first, first + count) as a batch (int32 arrays in the
     canonical layout) that ``oracle.solve`` accepts."""
     S, n = int(base.S), int(base.n)
-    allp = placements(S, int(cands.m))
-    count = len(allp) - first if count is None else count
-    rows = [expand_one(base, slot, cands, allp[first + r]) for r in range(count)]
+    count = placement_count(S, int(cands.m)) - first if count is None else count
+    chosen = itertools.islice(itertools.permutations(range(S), int(cands.m)), first, first + count)
+    rows = [expand_one(base, slot, cands, stages) for stages in chosen]
+    assert len(rows) == count, "placement range outside [0, S!/(S-m)!)"
     stack = lambda key, shape: np.ascontiguousarray(
         np.array([r[key] for r in rows], np.int64).reshape((count,) + shape).astype(np.int32))
     return SimpleNamespace(

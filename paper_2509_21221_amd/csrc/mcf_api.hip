@@ -355,3 +355,111 @@ extern "C" const char *gwtf_mcf_last_error(const gwtf_mcf_t *h)
 {
     return h ? h->err.c_str() : g_create_err.c_str();
 }
+
+namespace {
+
+// S!/(S-m)! into *out; false when it does not fit in an int64.
+bool placement_count(int32_t S, int32_t m, int64_t *out)
+{
+    int64_t c = 1;
+    for (int32_t k = S - m + 1; k <= S; ++k) {
+        if (c > INT64_MAX / k) return false;
+        c *= k;
+    }
+    *out = c;
+    return true;
+}
+
+} // namespace
+
+extern "C" gwtf_status_t gwtf_whatif_count(int32_t num_stages, int32_t num_candidates, int64_t *count)
+{
+    if (!count) return fail(nullptr, GWTF_ERR_INVALID_ARG, "count is NULL");
+    if (num_stages < 1 || num_candidates < 0 || num_candidates > num_stages)
+        return fail(nullptr, GWTF_ERR_INVALID_ARG, "need S >= 1 and 0 <= m <= S");
+    if (!placement_count(num_stages, num_candidates, count))
+        return fail(nullptr, GWTF_ERR_INVALID_ARG, "S!/(S-m)! does not fit in an int64");
+    return GWTF_OK;
+}
+
+extern "C" gwtf_status_t gwtf_mcf_whatif_expand(gwtf_mcf_t *h, const gwtf_mcf_batch_t *base,
+                                                const gwtf_whatif_candidates_t *cand, int64_t first,
+                                                int32_t count, const gwtf_mcf_instances_t *out)
+{
+    if (!h) return fail(nullptr, GWTF_ERR_INVALID_ARG, "handle is NULL");
+    if (!base || !cand || !out) return fail(h, GWTF_ERR_INVALID_ARG, "base, cand or out is NULL");
+    const int S = h->shape.num_stages, n = h->shape.nodes_per_stage, m = cand->num_candidates;
+    if (S > kWhatifMaxStages) return fail(h, GWTF_ERR_INVALID_ARG, "what-if expansion needs S <= 1024");
+    if (int64_t(S - 1) * n * n >= (int64_t(1) << 31) || int64_t(S) * n >= (int64_t(1) << 31))
+        return fail(h, GWTF_ERR_INVALID_ARG, "instance too large for the what-if expansion");
+    if (base->batch != 1) return fail(h, GWTF_ERR_INVALID_ARG, "base must hold exactly one instance");
+    if (!base->node_cap || !base->node_cost || !base->supply)
+        return fail(h, GWTF_ERR_INVALID_ARG, "base pointer is NULL");
+    if ((S > 1) != (base->arc_cost != nullptr))
+        return fail(h, GWTF_ERR_INVALID_ARG, "base arc_cost must be non-NULL exactly when S > 1");
+    if (m < 0 || m > S) return fail(h, GWTF_ERR_INVALID_ARG, "num_candidates outside [0, S]");
+    if (cand->slot < 0 || cand->slot >= n) return fail(h, GWTF_ERR_INVALID_ARG, "slot outside [0, n)");
+    if ((m > 0) != (cand->cap != nullptr) || (m > 0) != (cand->cost != nullptr))
+        return fail(h, GWTF_ERR_INVALID_ARG, "candidate cap and cost must be non-NULL exactly when m > 0");
+    const bool links = S > 1 && m > 0;
+    if (links != (cand->in_cost != nullptr) || links != (cand->out_cost != nullptr) ||
+        links != (cand->link_cost != nullptr))
+        return fail(h, GWTF_ERR_INVALID_ARG,
+                    "candidate in_cost, out_cost and link_cost must be non-NULL exactly when S > 1 and m > 0");
+    if (count < 0 || first < 0) return fail(h, GWTF_ERR_INVALID_ARG, "first and count must be >= 0");
+    if (count > 0 && (!out->node_cap || !out->node_cost || !out->src_cost || !out->snk_cost || !out->supply))
+        return fail(h, GWTF_ERR_INVALID_ARG, "output pointer is NULL");
+    if (count > 0 && (S > 1) != (out->arc_cost != nullptr))
+        return fail(h, GWTF_ERR_INVALID_ARG, "output arc_cost must be non-NULL exactly when S > 1");
+    int64_t total = 0;
+    if (!placement_count(S, m, &total))
+        return fail(h, GWTF_ERR_INVALID_ARG, "S!/(S-m)! does not fit in an int64");
+    if (first > total || count > total - first)
+        return fail(h, GWTF_ERR_RANGE, "placement range outside [0, S!/(S-m)!)");
+    if (count == 0) return GWTF_OK;
+    hipError_t e = hipSetDevice(h->shape.device);
+    if (e != hipSuccess) return hip_fail(h, e, "hipSetDevice");
+    WhatifExpandParams p{};
+    p.S = S;
+    p.n = n;
+    p.m = m;
+    p.slot = cand->slot;
+    p.first = first;
+    p.cap = base->node_cap;
+    p.cost = base->node_cost;
+    p.arc = base->arc_cost;
+    p.src = base->src_cost;
+    p.snk = base->snk_cost;
+    p.supply = base->supply;
+    p.ccap = cand->cap;
+    p.ccost = cand->cost;
+    p.cin = cand->in_cost;
+    p.cout = cand->out_cost;
+    p.clink = cand->link_cost;
+    p.csrc = cand->src_cost;
+    p.csnk = cand->snk_cost;
+    p.out_cap = out->node_cap;
+    p.out_cost = out->node_cost;
+    p.out_arc = out->arc_cost;
+    p.out_src = out->src_cost;
+    p.out_snk = out->snk_cost;
+    p.out_supply = out->supply;
+    if ((e = launch_whatif_expand(p, count, h->stream)) != hipSuccess) return hip_fail(h, e, "what-if expansion launch");
+    return GWTF_OK;
+}
+
+extern "C" gwtf_status_t gwtf_mcf_whatif_best(gwtf_mcf_t *h, int32_t count, const int64_t *flow_value,
+                                              const int64_t *total_cost, const int32_t *status, int64_t first,
+                                              int32_t merge, int64_t *best)
+{
+    if (!h) return fail(nullptr, GWTF_ERR_INVALID_ARG, "handle is NULL");
+    if (!best) return fail(h, GWTF_ERR_INVALID_ARG, "best is NULL");
+    if (count < 0 || first < 0) return fail(h, GWTF_ERR_INVALID_ARG, "first and count must be >= 0");
+    if (count > 0 && (!flow_value || !total_cost || !status))
+        return fail(h, GWTF_ERR_INVALID_ARG, "flow_value, total_cost or status is NULL");
+    hipError_t e = hipSetDevice(h->shape.device);
+    if (e != hipSuccess) return hip_fail(h, e, "hipSetDevice");
+    if ((e = launch_whatif_best(count, flow_value, total_cost, status, first, merge, best, h->stream)) != hipSuccess)
+        return hip_fail(h, e, "what-if best launch");
+    return GWTF_OK;
+}

@@ -93,6 +93,19 @@ hipError_t launch_lds_pass(const SolveParams &p, int waves, size_t lds_bytes, hi
 hipError_t launch_fallback_pass(const SolveParams &p, size_t lds_bytes, hipStream_t s);
 hipError_t launch_export(const int32_t *node_flow_ws, int32_t S, int32_t n, int32_t first, int32_t count,
                          int32_t *src_flow, int32_t *snk_flow, hipStream_t s);
+// What-if expansion (mcf_whatif.hip): the base instance, the candidates
+// and the output batch, all device pointers in the canonical layouts.
+constexpr int kWhatifMaxStages = 1024;
+struct WhatifExpandParams {
+    int32_t S, n, m, slot;
+    int64_t first;
+    const int32_t *cap, *cost, *arc, *src, *snk, *supply;                 // base [1][...]
+    const int32_t *ccap, *ccost, *cin, *cout, *clink, *csrc, *csnk;       // candidates
+    int32_t *out_cap, *out_cost, *out_arc, *out_src, *out_snk, *out_supply; // [count][...]
+};
+hipError_t launch_whatif_expand(const WhatifExpandParams &p, int32_t count, hipStream_t s);
+hipError_t launch_whatif_best(int32_t count, const int64_t *F, const int64_t *cost, const int32_t *status,
+                              int64_t first, int32_t merge, int64_t *best, hipStream_t s);
 int fallback_waves();
 hipError_t set_lds_limits(size_t max_bytes);
 

@@ -2,8 +2,10 @@
 marshalling only -- every step of the solve runs in the HIP library).
 
 The functions carry the C names (``gwtf_mcf_create``, ``gwtf_mcf_solve_batch``,
-``gwtf_mcf_get_flows``, ``gwtf_mcf_get_stats``, ``gwtf_mcf_destroy``,
-``gwtf_mcf_last_error``); ``Solver`` wraps them for torch device tensors.
+``gwtf_mcf_get_flows``, ``gwtf_mcf_get_stats``, ``gwtf_mcf_get_passes``,
+``gwtf_whatif_count``, ``gwtf_mcf_whatif_expand``, ``gwtf_mcf_whatif_best``,
+``gwtf_mcf_destroy``, ``gwtf_mcf_last_error``); ``Solver`` wraps them for
+torch device tensors.
 PyTorch only provides device memory and the HIP stream.
 
 There is no fallback: if ``libgwtf_mcf.so`` is missing or cannot be loaded,
@@ -52,6 +54,19 @@ class gwtf_mcf_batch_t(ctypes.Structure):
                 ("status", ctypes.c_void_p)]
 
 
+class gwtf_whatif_candidates_t(ctypes.Structure):
+    _fields_ = [("num_candidates", ctypes.c_int32), ("slot", ctypes.c_int32),
+                ("cap", ctypes.c_void_p), ("cost", ctypes.c_void_p), ("in_cost", ctypes.c_void_p),
+                ("out_cost", ctypes.c_void_p), ("link_cost", ctypes.c_void_p),
+                ("src_cost", ctypes.c_void_p), ("snk_cost", ctypes.c_void_p)]
+
+
+class gwtf_mcf_instances_t(ctypes.Structure):
+    _fields_ = [("node_cap", ctypes.c_void_p), ("node_cost", ctypes.c_void_p),
+                ("arc_cost", ctypes.c_void_p), ("src_cost", ctypes.c_void_p),
+                ("snk_cost", ctypes.c_void_p), ("supply", ctypes.c_void_p)]
+
+
 class GwtfError(RuntimeError):
     def __init__(self, code, msg):
         super().__init__(f"{STATUS_NAMES.get(code, code)}: {msg}")
@@ -84,6 +99,14 @@ def load_library(path: str = LIB_PATH):
         lib.gwtf_mcf_get_stats.restype = ctypes.c_int
         lib.gwtf_mcf_get_passes.argtypes = [vp, i32, i32, vp]
         lib.gwtf_mcf_get_passes.restype = ctypes.c_int
+        lib.gwtf_whatif_count.argtypes = [i32, i32, ctypes.POINTER(ctypes.c_int64)]
+        lib.gwtf_whatif_count.restype = ctypes.c_int
+        lib.gwtf_mcf_whatif_expand.argtypes = [vp, ctypes.POINTER(gwtf_mcf_batch_t),
+                                               ctypes.POINTER(gwtf_whatif_candidates_t), ctypes.c_int64, i32,
+                                               ctypes.POINTER(gwtf_mcf_instances_t)]
+        lib.gwtf_mcf_whatif_expand.restype = ctypes.c_int
+        lib.gwtf_mcf_whatif_best.argtypes = [vp, i32, vp, vp, vp, ctypes.c_int64, i32, vp]
+        lib.gwtf_mcf_whatif_best.restype = ctypes.c_int
         lib.gwtf_mcf_destroy.argtypes = [vp]
         lib.gwtf_mcf_destroy.restype = None
         lib.gwtf_mcf_last_error.argtypes = [vp]
@@ -137,6 +160,35 @@ def gwtf_mcf_get_stats(handle, first: int, count: int, stats: int) -> None:
 def gwtf_mcf_get_passes(handle, first: int, count: int, passes: int) -> None:
     _check(load_library().gwtf_mcf_get_passes(ctypes.c_void_p(handle), first, count,
                                               passes or None), handle)
+
+
+def gwtf_whatif_count(num_stages: int, num_candidates: int) -> int:
+    """S!/(S-m)!: the number of placements of m candidates over S stages."""
+    out = ctypes.c_int64()
+    _check(load_library().gwtf_whatif_count(num_stages, num_candidates, ctypes.byref(out)))
+    return out.value
+
+
+def gwtf_mcf_whatif_expand(handle, base: dict, cand: dict, first: int, count: int, out: dict) -> None:
+    """``base``, ``cand`` and ``out`` map the C struct field names to device
+    addresses (0 = NULL); cand also carries num_candidates and slot."""
+    b = gwtf_mcf_batch_t(1, base.get("node_cap") or None, base.get("node_cost") or None,
+                         base.get("arc_cost") or None, base.get("src_cost") or None,
+                         base.get("snk_cost") or None, base.get("supply") or None, None, None, None)
+    c = gwtf_whatif_candidates_t(cand["num_candidates"], cand["slot"],
+                                 *(cand.get(k) or None for k in ("cap", "cost", "in_cost", "out_cost",
+                                                                  "link_cost", "src_cost", "snk_cost")))
+    o = gwtf_mcf_instances_t(*(out.get(k) or None for k in ("node_cap", "node_cost", "arc_cost", "src_cost",
+                                                             "snk_cost", "supply")))
+    _check(load_library().gwtf_mcf_whatif_expand(ctypes.c_void_p(handle), ctypes.byref(b), ctypes.byref(c),
+                                                 first, count, ctypes.byref(o)), handle)
+
+
+def gwtf_mcf_whatif_best(handle, count: int, flow_value: int, total_cost: int, status: int, first: int,
+                         merge: int, best: int) -> None:
+    _check(load_library().gwtf_mcf_whatif_best(ctypes.c_void_p(handle), count, flow_value or None,
+                                               total_cost or None, status or None, first, merge,
+                                               best or None), handle)
 
 
 def gwtf_mcf_destroy(handle) -> None:
@@ -224,6 +276,69 @@ class Solver:
         out = torch.empty(count, dtype=torch.int32, device=torch.device("cuda", self.device))
         gwtf_mcf_get_passes(self.handle, first, count, out.data_ptr())
         return out
+
+    def whatif_expand(self, base, cand, slot: int, first: int = 0, count: int | None = None, out=None):
+        """Placements [first, first + count) of ``cand`` over the base instance
+        as a batch of device tensors (keys node_cap, node_cost, arc_cost,
+        src_cost, snk_cost, supply).  ``base`` maps those keys to one
+        instance's int32 device tensors (src_cost / snk_cost optional);
+        ``cand`` maps cap [m][S], cost [m][S], in_cost and out_cost [m][S][n],
+        link_cost [m][m] and optional src_cost / snk_cost [m]."""
+        torch = self.torch
+        S, n = self.S, self.n
+        m = 0 if cand.get("cap") is None else int(cand["cap"].shape[0])
+        total = gwtf_whatif_count(S, m)
+        count = total - first if count is None else count
+        ba = {"node_cap": self._arg(base["node_cap"], (1, S, n), "node_cap"),
+              "node_cost": self._arg(base["node_cost"], (1, S, n), "node_cost"),
+              "arc_cost": self._arg(base.get("arc_cost"), (1, S - 1, n, n), "arc_cost") if S > 1 else 0,
+              "src_cost": self._arg(base.get("src_cost"), (1, n), "src_cost"),
+              "snk_cost": self._arg(base.get("snk_cost"), (1, n), "snk_cost"),
+              "supply": self._arg(base["supply"], (1,), "supply")}
+        links = S > 1 and m > 0
+        ca = {"num_candidates": m, "slot": slot,
+              "cap": self._arg(cand.get("cap"), (m, S), "cap") if m > 0 else 0,
+              "cost": self._arg(cand.get("cost"), (m, S), "cost") if m > 0 else 0,
+              "in_cost": self._arg(cand.get("in_cost"), (m, S, n), "in_cost") if links else 0,
+              "out_cost": self._arg(cand.get("out_cost"), (m, S, n), "out_cost") if links else 0,
+              "link_cost": self._arg(cand.get("link_cost"), (m, m), "link_cost") if links else 0,
+              "src_cost": self._arg(cand.get("src_cost"), (m,), "src_cost") if m > 0 else 0,
+              "snk_cost": self._arg(cand.get("snk_cost"), (m,), "snk_cost") if m > 0 else 0}
+        dev = torch.device("cuda", self.device)
+        if out is None:
+            e = lambda *shape: torch.empty(shape, dtype=torch.int32, device=dev)
+            out = {"node_cap": e(count, S, n), "node_cost": e(count, S, n),
+                   "arc_cost": e(count, S - 1, n, n) if S > 1 else None,
+                   "src_cost": e(count, n), "snk_cost": e(count, n), "supply": e(count)}
+        oa = {"node_cap": self._arg(out["node_cap"], (count, S, n), "out node_cap"),
+              "node_cost": self._arg(out["node_cost"], (count, S, n), "out node_cost"),
+              "arc_cost": self._arg(out.get("arc_cost"), (count, S - 1, n, n), "out arc_cost") if S > 1 else 0,
+              "src_cost": self._arg(out["src_cost"], (count, n), "out src_cost"),
+              "snk_cost": self._arg(out["snk_cost"], (count, n), "out snk_cost"),
+              "supply": self._arg(out["supply"], (count,), "out supply")}
+        gwtf_mcf_whatif_expand(self.handle, ba, ca, first, count, oa)
+        return out
+
+    def whatif_best(self, F, cost, status, first: int = 0, best=None, merge: bool = False):
+        """Best placement of a solved expanded batch: an int64 device tensor
+        {first + index, F, cost} ({-1, 0, 0} if no instance is OK).  With
+        ``merge`` the result is combined with what ``best`` holds."""
+        torch = self.torch
+        count = int(F.shape[0])
+        for t, dt, name in ((F, torch.int64, "F"), (cost, torch.int64, "cost"), (status, torch.int32, "status")):
+            if t.dtype != dt or not t.is_contiguous() or t.device.type != "cuda" or t.device.index != self.device \
+                    or tuple(t.shape) != (count,):
+                raise ValueError(f"{name}: need a contiguous {dt} tensor of shape ({count},) on cuda:{self.device}")
+        if best is None:
+            if merge:
+                raise ValueError("merge needs an existing best tensor")
+            best = torch.empty(3, dtype=torch.int64, device=torch.device("cuda", self.device))
+        elif best.dtype != torch.int64 or tuple(best.shape) != (3,) or not best.is_contiguous() \
+                or best.device.type != "cuda" or best.device.index != self.device:
+            raise ValueError(f"best: need a contiguous int64 tensor of shape (3,) on cuda:{self.device}")
+        gwtf_mcf_whatif_best(self.handle, count, F.data_ptr(), cost.data_ptr(), status.data_ptr(), first,
+                             int(merge), best.data_ptr())
+        return best
 
     def close(self):
         if self.handle:

@@ -15,13 +15,14 @@ HEADER = os.path.join(ROOT, "include", "gwtf_mcf.h")
 def declared_functions():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(gwtf_mcf_\w+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(gwtf_(?:mcf|whatif)_\w+)\s*\(", text)))
 
 
 def test_header_declares_the_boundary():
     names = declared_functions()
     for required in ("gwtf_mcf_create", "gwtf_mcf_solve_batch", "gwtf_mcf_get_flows",
-                     "gwtf_mcf_destroy"):
+                     "gwtf_mcf_destroy", "gwtf_whatif_count", "gwtf_mcf_whatif_expand",
+                     "gwtf_mcf_whatif_best"):
         assert required in names
 
 
@@ -57,6 +58,8 @@ def test_null_handle_calls_fail_cleanly():
     assert lib.gwtf_mcf_get_flows(None, 0, 1, None, None, None, None, None) == mcf.GWTF_ERR_INVALID_ARG
     assert lib.gwtf_mcf_get_stats(None, 0, 1, None) == mcf.GWTF_ERR_INVALID_ARG
     assert lib.gwtf_mcf_get_passes(None, 0, 1, None) == mcf.GWTF_ERR_INVALID_ARG
+    assert lib.gwtf_mcf_whatif_expand(None, None, None, 0, 1, None) == mcf.GWTF_ERR_INVALID_ARG
+    assert lib.gwtf_mcf_whatif_best(None, 1, None, None, None, 0, 0, None) == mcf.GWTF_ERR_INVALID_ARG
     lib.gwtf_mcf_destroy(None)
     out = ctypes.c_void_p(1)
     assert lib.gwtf_mcf_create(None, None, ctypes.byref(out)) == mcf.GWTF_ERR_INVALID_ARG
@@ -74,3 +77,16 @@ def test_product_path_fails_loudly_without_library(tmp_path):
             mcf.load_library(str(tmp_path / "nope.so"))
     finally:
         mcf._lib = saved
+
+
+def test_whatif_count_is_host_only():
+    """S!/(S-m)! placements, computed on the host (no device is touched)."""
+    import math
+
+    for S, m in [(1, 0), (1, 1), (4, 2), (8, 8), (12, 12), (20, 20), (64, 3)]:
+        assert mcf.gwtf_whatif_count(S, m) == math.perm(S, m)
+    for S, m in [(0, 0), (3, 4), (3, -1), (21, 21), (30, 20)]:
+        with pytest.raises(mcf.GwtfError):
+            mcf.gwtf_whatif_count(S, m)
+    lib = mcf.load_library()
+    assert lib.gwtf_whatif_count(4, 2, None) == mcf.GWTF_ERR_INVALID_ARG

@@ -1,0 +1,249 @@
+"""GPU parity of what-if node addition (paper Sec. VI, handling joining
+nodes): the HIP expansion, the unchanged batched solve and the best-placement
+reduction, all through the C ABI, against the CPU oracle.
+
+Expanded instances are integer copies and must match the oracle's bit for
+bit; (F, cost, status) of every placement and the best placement must match
+exactly.
+"""
+import ctypes
+import math
+import sys
+import time
+
+import numpy as np
+import pytest
+
+import oracle
+import oracle.whatif as OW
+from paper_2509_21221_amd import mcf
+from paper_2509_21221_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+KEYS = ("node_cap", "node_cost", "arc_cost", "src_cost", "snk_cost", "supply")
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def _t(a):
+    import torch
+
+    return torch.from_numpy(np.ascontiguousarray(a)).to(torch.device("cuda", 0))
+
+
+def base_tensors(base, with_src=True):
+    d = {"node_cap": _t(base.node_cap), "node_cost": _t(base.node_cost),
+         "arc_cost": _t(base.arc_cost) if base.S > 1 else None, "supply": _t(base.supply)}
+    if with_src:
+        d["src_cost"], d["snk_cost"] = _t(base.src_cost), _t(base.snk_cost)
+    return d
+
+
+def cand_tensors(c, with_src=True):
+    d = {"cap": _t(c.cap), "cost": _t(c.cost), "in_cost": _t(c.inn), "out_cost": _t(c.out),
+         "link_cost": _t(c.link)}
+    if with_src:
+        d["src_cost"], d["snk_cost"] = _t(c.src), _t(c.snk)
+    return d
+
+
+def gpu_whatif(base, slot, cands, first=0, count=None, with_src=True, solve=True, chunks=1):
+    """Expand (in ``chunks`` pieces), solve and reduce on the GPU; returns numpy
+    arrays of the expanded batch, F, cost, status, passes and best."""
+    import torch
+
+    S, n = base.S, base.n
+    total = math.perm(S, cands.m)
+    count = total - first if count is None else count
+    out = {}
+    with mcf.Solver(S, n, max(count, 1)) as s:
+        bt, ct = base_tensors(base, with_src), cand_tensors(cands, with_src)
+        if cands.m == 0:
+            ct = {}
+        dev = torch.device("cuda", 0)
+        e = lambda *shape: torch.empty(shape, dtype=torch.int32, device=dev)
+        batch = {"node_cap": e(count, S, n), "node_cost": e(count, S, n),
+                 "arc_cost": e(count, S - 1, n, n) if S > 1 else None,
+                 "src_cost": e(count, n), "snk_cost": e(count, n), "supply": e(count)}
+        bounds = np.linspace(0, count, chunks + 1).astype(int)
+        for a, b in zip(bounds[:-1], bounds[1:]):
+            if b > a:
+                view = {k: (None if v is None else v[a:b]) for k, v in batch.items()}
+                s.whatif_expand(bt, ct, slot, first + int(a), int(b - a), out=view)
+        if solve and count > 0:
+            F, cost, status = s.solve(batch["node_cap"], batch["node_cost"], batch["arc_cost"],
+                                      batch["supply"], src_cost=batch["src_cost"],
+                                      snk_cost=batch["snk_cost"])
+            best = s.whatif_best(F, cost, status, first)
+            merged = None
+            for a, b in zip(bounds[:-1], bounds[1:]):
+                merged = s.whatif_best(F[a:b], cost[a:b], status[a:b], first + int(a), best=merged,
+                                       merge=merged is not None)
+            out.update(F=F.cpu().numpy(), cost=cost.cpu().numpy(), status=status.cpu().numpy(),
+                       passes=s.passes().cpu().numpy(), best=tuple(int(x) for x in best.cpu().numpy()),
+                       merged=tuple(int(x) for x in merged.cpu().numpy()))
+        torch.cuda.synchronize()
+        out.update({k: (None if v is None else v.cpu().numpy()) for k, v in batch.items()})
+    return out
+
+
+def assert_same_batch(g, ref):
+    for k in KEYS:
+        if g[k] is None:
+            assert ref.S == 1 and k == "arc_cost"
+            continue
+        r = getattr(ref, k)
+        assert g[k].shape == r.shape, k
+        bad = np.argwhere(g[k] != r)
+        assert bad.size == 0, f"{k}: {len(bad)} mismatches, first at {bad[:3].tolist()}"
+
+
+def _case(S, n, m, slot, occupied, holes, seed):
+    base = W.random_small(1, S, n, seed=100 + seed, supply_hi=10, holes=holes)
+    if not occupied:
+        base.node_cap[0][:, slot] = 0
+    return base, W.random_candidates(S, n, m, seed=seed, holes=holes)
+
+
+EXPAND_CASES = [
+    # S, n, m, slot, occupied, holes, with_src, first, count
+    (1, 3, 1, 0, False, 0.0, True, 0, None),
+    (1, 3, 0, 2, True, 0.0, True, 0, None),
+    (2, 5, 2, 4, False, 0.2, False, 0, None),
+    (3, 4, 3, 1, True, 0.3, True, 0, None),
+    (4, 6, 2, 5, False, 0.0, True, 3, 5),
+    (5, 7, 5, 3, False, 0.1, True, 0, None),
+    (6, 70, 3, 69, False, 0.0, True, 7, 40),
+    (70, 3, 2, 1, False, 0.0, True, 0, None),
+    (130, 2, 1, 0, True, 0.0, False, 0, None),
+    (12, 9, 12, 8, False, 0.0, True, 30_000_000, 700),
+]
+
+
+@pytest.mark.parametrize("S,n,m,slot,occupied,holes,with_src,first,count", EXPAND_CASES)
+def test_expand_bit_exact(S, n, m, slot, occupied, holes, with_src, first, count):
+    base, cands = _case(S, n, m, slot, occupied, holes, seed=S * 7 + n)
+    if not with_src:
+        base.src_cost[:] = 0
+        base.snk_cost[:] = 0
+        cands.src[:] = 0
+        cands.snk[:] = 0
+    say("expand", S, n, m, slot, first, count)
+    g = gpu_whatif(base, slot, cands, first, count, with_src=with_src, solve=False, chunks=3)
+    ref = OW.expand(base, slot, cands, first, count)
+    assert_same_batch(g, ref)
+
+
+@pytest.mark.parametrize("S,n,m,slot,occupied,holes", [
+    (2, 3, 2, 2, False, 0.0), (3, 4, 3, 0, False, 0.2), (4, 5, 3, 4, True, 0.1),
+    (5, 6, 5, 5, False, 0.0), (4, 20, 4, 19, False, 0.0), (3, 70, 2, 69, False, 0.0),
+])
+def test_whatif_parity_small(S, n, m, slot, occupied, holes):
+    base, cands = _case(S, n, m, slot, occupied, holes, seed=S * 11 + n)
+    say("whatif", S, n, m, slot)
+    g = gpu_whatif(base, slot, cands, chunks=3)
+    ref = OW.whatif(base, slot, cands)
+    assert (g["status"] == ref["status"]).all()
+    bad = np.flatnonzero((g["F"] != ref["F"]) | (g["cost"] != ref["cost"]))
+    assert bad.size == 0, f"{bad.size} placements differ, first {bad[:5]}"
+    assert g["best"] == ref["best"] == g["merged"]
+
+
+def test_paper_join_example_on_gpu():
+    """Sec. V-B: the joining node goes to stage 1 (throughput 2 -> 3), the
+    next one to stage 2; each round's winner becomes the next base by
+    expanding only the best placement."""
+    import json
+    import os
+
+    d = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "whatif_paper_join.json")))
+    S, n = d["S"], d["n"]
+    base = W.Batch(S, n, np.asarray([d["node_cap"]], np.int32), np.asarray([d["node_cost"]], np.int32),
+                   np.full((1, S - 1, n, n), d["arc_cost"], np.int32), np.full((1, n), d["src_cost"], np.int32),
+                   np.full((1, n), d["snk_cost"], np.int32), np.asarray([d["supply"]], np.int32))
+    full = lambda shape: np.full(shape, d["candidate"]["cost"], np.int32)
+    cand = W.Candidates(np.full((1, S), d["candidate"]["cap"], np.int32), full((1, S)), full((1, S, n)),
+                        full((1, S, n)), full((1, 1)), full(1), full(1))
+    for rnd in d["rounds"]:
+        g = gpu_whatif(base, rnd["slot"], cand)
+        assert g["F"].tolist() == rnd["expect_F"]
+        assert g["best"][0] == rnd["expect_best"]
+        nxt = gpu_whatif(base, rnd["slot"], cand, first=g["best"][0], count=1, solve=False)
+        base = W.Batch(S, n, *(np.ascontiguousarray(nxt[k]) for k in KEYS))
+
+
+def test_bad_candidates_are_reported_and_skipped():
+    S, n = 3, 4
+    base, cands = _case(S, n, 3, 3, False, 0.0, seed=5)
+    cands.cap[1, 0] = -1  # candidate 1 is invalid in stage 0 only
+    g = gpu_whatif(base, 3, cands)
+    ref = OW.whatif(base, 3, cands)
+    assert (g["status"] == ref["status"]).all() and (g["status"] == 1).sum() == 2
+    assert (g["F"] == ref["F"]).all() and (g["cost"] == ref["cost"]).all()
+    assert g["best"] == ref["best"] and ref["best"][0] >= 0
+    cands.cap[:] = -1
+    g = gpu_whatif(base, 3, cands)
+    assert (g["status"] == 1).all() and g["best"] == (-1, 0, 0) == g["merged"]
+
+
+def test_no_candidates_gives_the_base():
+    base, cands = _case(4, 5, 0, 2, True, 0.1, seed=9)
+    g = gpu_whatif(base, 2, cands)
+    assert_same_batch(g, base)
+    r = oracle.solve(base, flows=False, potentials=False)
+    assert (g["F"][0], g["cost"][0], g["best"]) == (r["F"][0], r["cost"][0], (0, r["F"][0], r["cost"][0]))
+
+
+def test_argument_errors():
+    S, n = 3, 4
+    base, cands = _case(S, n, 2, 1, False, 0.0, seed=2)
+    with mcf.Solver(S, n, 8) as s:
+        bt, ct = base_tensors(base), cand_tensors(cands)
+        with pytest.raises(mcf.GwtfError) as e:
+            s.whatif_expand(bt, ct, 1, first=5, count=2)  # 6 placements
+        assert e.value.code == mcf.GWTF_ERR_RANGE
+        with pytest.raises(mcf.GwtfError) as e:
+            s.whatif_expand(bt, ct, n, first=0, count=1)
+        assert e.value.code == mcf.GWTF_ERR_INVALID_ARG
+        big = W.random_candidates(S, n, S + 1, seed=1)
+        with pytest.raises(mcf.GwtfError) as e:
+            s.whatif_expand(bt, cand_tensors(big), 0, first=0, count=1)
+        assert e.value.code == mcf.GWTF_ERR_INVALID_ARG
+        out = s.whatif_expand(bt, ct, 1, first=0, count=0)
+        assert out["node_cap"].shape[0] == 0
+        # a NULL required candidate array is rejected by the library itself
+        lib = mcf.load_library()
+        b = mcf.gwtf_mcf_batch_t(1, bt["node_cap"].data_ptr(), bt["node_cost"].data_ptr(),
+                                 bt["arc_cost"].data_ptr(), None, None, bt["supply"].data_ptr(), None, None, None)
+        c = mcf.gwtf_whatif_candidates_t(2, 1, ct["cap"].data_ptr(), ct["cost"].data_ptr(), None, None, None,
+                                         None, None)
+        o = mcf.gwtf_mcf_instances_t()
+        assert lib.gwtf_mcf_whatif_expand(ctypes.c_void_p(s.handle), ctypes.byref(b), ctypes.byref(c), 0, 1,
+                                          ctypes.byref(o)) == mcf.GWTF_ERR_INVALID_ARG
+
+
+def test_node_addition_setting1_full():
+    """The paper's node-addition setting 1 (8 stages of 12 relays, 8
+    candidates): all 8! = 40320 placements, in the launch configuration the
+    benchmark times, against the oracle on every placement."""
+    base, slot, cands = W.node_addition(1)
+    t0 = time.time()
+    g = gpu_whatif(base, slot, cands)
+    say("gpu whatif done", time.time() - t0)
+    assert (g["passes"] == mcf.GWTF_PASS_LDS).all()
+    ref_batch = OW.expand(base, slot, cands)
+    say("oracle expand done", time.time() - t0)
+    assert_same_batch(g, ref_batch)
+    r = oracle.solve(ref_batch, flows=False, potentials=False)
+    say("oracle solve done", time.time() - t0)
+    assert (g["status"] == r["status"]).all() and (g["status"] == 0).all()
+    bad = np.flatnonzero((g["F"] != r["F"]) | (g["cost"] != r["cost"]))
+    assert bad.size == 0, f"{bad.size} placements differ, first {bad[:5]}"
+    assert g["best"] == OW.best(r["F"], r["cost"], r["status"]) == g["merged"]
+    # supply binds before the join: every placement keeps F and none costs more
+    r0 = oracle.solve(base, flows=False, potentials=False)
+    assert r0["F"][0] == base.supply[0]
+    assert (g["F"] == r0["F"][0]).all() and (g["cost"] <= r0["cost"][0]).all()
