@@ -389,3 +389,84 @@ def random_candidates(S: int, n: int, m: int, seed: int, cap_hi: int = 3, cost_h
             a[rng.random(a.shape) < holes] = NO_ARC
     return Candidates(u(0, cap_hi, (m, S)), u(0, cost_hi, (m, S)), inn, out, link,
                       u(0, cost_hi, m), u(0, cost_hi, m))
+
+
+@dataclass
+class LocatedBatch:
+    """A batch whose link delays are latencies between node locations (the
+    paper's testbed of Sec. VI places every node at one of a few geographic
+    locations).  All int32, C-contiguous:
+
+        node_cap, node_cost  [B][S][n]
+        location             [B][S][n]   in [0, L)
+        latency              [B][L][L]   >= 0: delay between two locations
+        src_cost, snk_cost   [B][n]
+        supply               [B]
+
+    The link from node i of stage k to node j of stage k+1 has delay
+    latency[b][location[b][k][i]][location[b][k+1][j]]."""
+
+    S: int
+    n: int
+    L: int
+    node_cap: np.ndarray
+    node_cost: np.ndarray
+    location: np.ndarray
+    latency: np.ndarray
+    src_cost: np.ndarray
+    snk_cost: np.ndarray
+    supply: np.ndarray
+    name: str = ""
+
+    @property
+    def B(self) -> int:
+        return int(self.supply.shape[0])
+
+    def subset(self, idx) -> "LocatedBatch":
+        idx = np.asarray(idx, dtype=np.int64)
+        take = lambda a: np.ascontiguousarray(a[idx])
+        return LocatedBatch(self.S, self.n, self.L, take(self.node_cap), take(self.node_cost),
+                            take(self.location), take(self.latency), take(self.src_cost),
+                            take(self.snk_cost), take(self.supply), name=self.name)
+
+
+def located(preset: int, B: int | None = None, first: int = 0) -> LocatedBatch:
+    """The location-latency presets (2, 4 and 5) in located form: the same
+    random draws as CONFIGS[preset], so the implied link delays equal that
+    preset's arc_cost arrays element for element."""
+    S, n, cap_hi, supply, default_B = {2: (8, 8, 8, 64, 16384), 4: (32, 64, 8, 512, 256),
+                                       5: (64, 512, 16, 4096, 1)}[preset]
+    B = default_B if B is None else B
+    L = NUM_LOCATIONS
+    out = LocatedBatch(S, n, L, np.zeros((B, S, n), np.int32), np.zeros((B, S, n), np.int32),
+                       np.zeros((B, S, n), np.int32), np.zeros((B, L, L), np.int32),
+                       np.zeros((B, n), np.int32), np.zeros((B, n), np.int32),
+                       np.full(B, supply, np.int32), name=f"located preset {preset}")
+    scratch = _empty(1, S, n, "")
+    for b in range(B):
+        loc, lat = _location_instance(_rng(preset, first + b), S, n, cap_hi, scratch, 0)
+        out.node_cap[b] = scratch.node_cap[0]
+        out.node_cost[b] = scratch.node_cost[0]
+        out.location[b] = loc
+        out.latency[b] = lat
+    return out
+
+
+def random_located(B: int, S: int, n: int, L: int, seed: int, cap_hi: int = 4, cost_hi: int = 30,
+                   supply_hi: int = 12) -> LocatedBatch:
+    """Small random located instances: locations U[0, L-1], latencies
+    U[0, cost_hi] (not symmetric), capacities U[0, cap_hi]."""
+    out = LocatedBatch(S, n, L, np.zeros((B, S, n), np.int32), np.zeros((B, S, n), np.int32),
+                       np.zeros((B, S, n), np.int32), np.zeros((B, L, L), np.int32),
+                       np.zeros((B, n), np.int32), np.zeros((B, n), np.int32),
+                       np.zeros(B, np.int32), name=f"random located S={S} n={n} L={L}")
+    for b in range(B):
+        rng = np.random.default_rng(np.random.SeedSequence(seed, spawn_key=(S, n, L, b)))
+        out.node_cap[b] = _int_uniform(rng, 0, cap_hi, (S, n))
+        out.node_cost[b] = _int_uniform(rng, 0, cost_hi, (S, n))
+        out.location[b] = _int_uniform(rng, 0, L - 1, (S, n))
+        out.latency[b] = _int_uniform(rng, 0, cost_hi, (L, L))
+        out.src_cost[b] = _int_uniform(rng, 0, cost_hi, n)
+        out.snk_cost[b] = _int_uniform(rng, 0, cost_hi, n)
+        out.supply[b] = int(rng.integers(0, supply_hi + 1))
+    return out

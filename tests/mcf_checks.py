@@ -307,3 +307,32 @@ def networkx_with_candidates(base, slot, cands, stages):
         return 0, 0
     flow = nx.max_flow_min_cost(G, "s0", "t")
     return int(sum(flow["s0"].values())), int(nx.cost_of_flow(G, flow))
+
+
+def networkx_located_hubs(lb, b):
+    """(F, cost) of located instance b on a network with one hub vertex per
+    stage boundary and location: exit (k, i) -> hub (k, location of i) at
+    cost 0, hub (k, a) -> entry (k+1, j) at latency[a][location of j].  Every
+    link is uncapacitated, so a path exit -> hub -> entry costs exactly the
+    direct link and the optimum equals the direct network's."""
+    import networkx as nx
+
+    S, n = lb.S, lb.n
+    cap, ncost = lb.node_cap[b].astype(int), lb.node_cost[b].astype(int)
+    loc, lat = lb.location[b], lb.latency[b]
+    G = nx.DiGraph()
+    G.add_edge("s0", "s", capacity=int(lb.supply[b]), weight=0)
+    for i in range(n):
+        G.add_edge("s", ("in", 0, i), weight=int(lb.src_cost[b][i]))
+        G.add_edge(("out", S - 1, i), "t", weight=int(lb.snk_cost[b][i]))
+    for k in range(S):
+        for i in range(n):
+            G.add_edge(("in", k, i), ("out", k, i), capacity=int(cap[k, i]), weight=int(ncost[k, i]))
+    for k in range(S - 1):
+        for i in range(n):
+            G.add_edge(("out", k, i), ("hub", k, int(loc[k, i])), weight=0)
+        for a in set(int(x) for x in loc[k]):
+            for j in range(n):
+                G.add_edge(("hub", k, a), ("in", k + 1, j), weight=int(lat[a, loc[k + 1, j]]))
+    flow = nx.max_flow_min_cost(G, "s0", "t")
+    return int(sum(flow["s0"].values())), int(nx.cost_of_flow(G, flow))
