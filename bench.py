@@ -2,6 +2,7 @@
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 4]
     python bench.py --whatif 1        # what-if node addition, paper setting 1
+    python bench.py --config 5 --located   # link delays as location latencies
 
 A step solves one whole batch of the workload (every instance to optimality)
 with inputs already resident in HBM.  The default workload is the 7B-scale
@@ -16,6 +17,12 @@ paper's node-addition test (Sec. VI, handling joining nodes; settings 1-3:
 8 stages of 12 relays plus one joining position, 8 candidates, 8! = 40320
 placements): expand all placements on the device, solve them, reduce to the
 best placement.  The value is placements evaluated per second.
+
+With --located the same preset (2, 4 or 5) is passed in located form (each
+node's location and the latency matrix instead of the n x n delays) to
+gwtf_mcf_solve_located; the 64 x 512 instance then runs the grid pass with
+location-factored relaxation.  That line reports its relaxation operations,
+not the dense links they stand for.
 """
 from __future__ import annotations
 
@@ -90,14 +97,16 @@ def cpu_baseline(batch, budget_s: float, threads: int):
     import numpy as np
 
     import oracle
+    import oracle.located
 
+    solve = oracle.located.solve if hasattr(batch, "location") else oracle.solve
     done, t_used, scans = 0, 0.0, 0
     chunk = max(1, threads)
     while done < batch.B and t_used < budget_s:
         idx = list(range(done, min(batch.B, done + chunk)))
         sub = batch.subset(idx)
         t0 = time.perf_counter()
-        r = oracle.solve(sub, nthreads=threads, flows=False, potentials=False)
+        r = solve(sub, nthreads=threads, flows=False, potentials=False)
         t_used += time.perf_counter() - t0
         scans += int(np.sum(r["arc_scans"]))
         done += len(idx)
@@ -235,6 +244,8 @@ def main():
     ap.add_argument("--config", type=int, default=4, choices=sorted(WORKLOADS))
     ap.add_argument("--whatif", type=int, default=0, choices=[0, 1, 2, 3],
                     help="time what-if node addition for this paper setting instead (0 = off)")
+    ap.add_argument("--located", action="store_true",
+                    help="pass the preset (2, 4 or 5) in located form to gwtf_mcf_solve_located")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle time for the CPU baseline (0 = skip)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -265,12 +276,18 @@ def main():
     from paper_2509_21221_amd import workloads as W
     from paper_2509_21221_amd.mcf import Solver
 
-    batch = W.CONFIGS[args.config]()
+    if args.located and args.config not in (2, 4, 5):
+        raise SystemExit("--located applies to the location-latency presets 2, 4 and 5")
+    batch = W.located(args.config) if args.located else W.CONFIGS[args.config]()
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
     t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
-    inputs = (t(batch.node_cap), t(batch.node_cost), t(batch.arc_cost) if batch.S > 1 else None,
-              t(batch.supply), t(batch.src_cost), t(batch.snk_cost))
+    if args.located:
+        inputs = (t(batch.node_cap), t(batch.node_cost), t(batch.location), t(batch.latency),
+                  t(batch.supply), t(batch.src_cost), t(batch.snk_cost))
+    else:
+        inputs = (t(batch.node_cap), t(batch.node_cost), t(batch.arc_cost) if batch.S > 1 else None,
+                  t(batch.supply), t(batch.src_cost), t(batch.snk_cost))
     stream = torch.cuda.current_stream(dev)
     solver = Solver(batch.S, batch.n, batch.B, device=0, stream=stream)
     outs = (torch.empty(batch.B, dtype=torch.int64, device=dev),
@@ -278,7 +295,10 @@ def main():
             torch.empty(batch.B, dtype=torch.int32, device=dev))
 
     def step():
-        solver.solve(*inputs[:4], src_cost=inputs[4], snk_cost=inputs[5], out=outs)
+        if args.located:
+            solver.solve_located(*inputs[:5], src_cost=inputs[5], snk_cost=inputs[6], out=outs)
+        else:
+            solver.solve(*inputs[:4], src_cost=inputs[4], snk_cost=inputs[5], out=outs)
 
     for _ in range(args.warmup):
         step()
@@ -314,8 +334,9 @@ def main():
         "ms_per_step": wall / args.steps * 1e3,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "int32", "data": "synthetic (seeded generator, paper-shaped)",
-        "config": {"workload": WORKLOADS[args.config], "instances": batch.B, "stages": batch.S,
-                   "nodes_per_stage": batch.n, "seed": 0},
+        "config": {"workload": WORKLOADS[args.config] + (", located form (node locations + latency matrix)"
+                                                          if args.located else ""),
+                   "instances": batch.B, "stages": batch.S, "nodes_per_stage": batch.n, "seed": 0},
         "arc_relaxations_per_s": relax / kernel_s,
         "dense_link_relaxations_per_s": dense_relax / kernel_s,
         "augmentations_per_instance": float(stats[:, 0].mean()),
@@ -332,6 +353,11 @@ def main():
                      "instances_per_pass": {KERNELS[p]: int((passes == p).sum()) for p in np.unique(passes)},
                      "kernel_ms": kernel_s * 1e3},
     }
+    if args.located:
+        line["metric"] = "MCMF instances solved/sec, located form (+ relaxation operations/sec)"
+        line["dense_link_relaxations_per_s"] = None
+        line["roofline"]["traffic"] = measured_traffic(KERNEL_SYMBOLS.get(main_pass, "?"),
+                                                       f"c{args.config}_located", kernel_s)
     if args.cpu_budget > 0 and args.config == 5:
         line["cpu_baseline"] = stored_oracle_baseline(args.config)
     elif args.cpu_budget > 0:

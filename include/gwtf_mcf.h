@@ -126,6 +126,44 @@ gwtf_status_t gwtf_mcf_get_stats(gwtf_mcf_t *h, int32_t first, int32_t count, in
  * handle's stream; errors as for gwtf_mcf_get_stats. */
 gwtf_status_t gwtf_mcf_get_passes(gwtf_mcf_t *h, int32_t first, int32_t count, int32_t *pass);
 
+/* ---- Location-factored instances (paper Sec. VI testbed: every node sits at
+ * one of a few geographic locations, and Eq. 1's link term is the latency
+ * between the two nodes' locations) ----
+ *
+ * A located batch stands for the ordinary batch whose link from node i of
+ * stage k to node j of stage k+1 has delay
+ * latency[b][location[b][k][i]][location[b][k+1][j]]; the result is exactly
+ * that batch's (gwtf_mcf_solve_batch semantics, every link present).  The
+ * grid pass (64 < n <= 512) relaxes the links in factored form: per
+ * location, the best label among the previous stage's nodes there, then per
+ * node one candidate per location, L operations instead of n.  Other shapes
+ * expand the delays into library workspace on the device and run the
+ * ordinary passes. */
+typedef struct {
+    int32_t batch;            /* B, 1 <= B <= max_batch */
+    int32_t num_locations;    /* L, 1 <= L <= 32 */
+    const int32_t *node_cap;  /* [B][S][n] >= 0 */
+    const int32_t *node_cost; /* [B][S][n] >= 0 */
+    const int32_t *location;  /* [B][S][n] in [0, L) */
+    const int32_t *latency;   /* [B][L][L] >= 0: [a][c] = delay from location a to location c */
+    const int32_t *src_cost;  /* [B][n] or NULL = 0 */
+    const int32_t *snk_cost;  /* [B][n] or NULL = 0 */
+    const int32_t *supply;    /* [B] >= 0 */
+    int64_t *flow_value;      /* [B] out */
+    int64_t *total_cost;      /* [B] out */
+    int32_t *status;          /* [B] out; with S > 1, a location outside [0, L) or a negative
+                                 latency gives GWTF_INST_BAD_INPUT (S == 1 reads neither) */
+} gwtf_mcf_located_batch_t;
+
+/* Solves a located batch; argument errors and status as for
+ * gwtf_mcf_solve_batch, and gwtf_mcf_get_flows / get_stats / get_passes then
+ * refer to it (for instances of the factored grid pass, stats column 2
+ * counts the factored relaxation operations divided by n).  The first call
+ * on a handle with S > 1 allocates max_batch * (S-1) * n * n int32 of
+ * workspace for the expanded delays, which every pass but the factored one
+ * reads (GWTF_ERR_OUT_OF_MEMORY if that fails). */
+gwtf_status_t gwtf_mcf_solve_located(gwtf_mcf_t *h, const gwtf_mcf_located_batch_t *b);
+
 /* ---- What-if node addition (paper Sec. VI, handling joining nodes; the
  * joining example of Sec. V-B) ----
  *

@@ -11,8 +11,9 @@ A located instance stands for the ordinary layered instance whose link from
 node i of stage k to node j of stage k+1 has delay
 latency[location[k][i]][location[k+1][j]].  ``to_dense`` writes that
 instance out element by element; ``solve`` hands it to the oracle's solver,
-so the optimum is Eq. 2's (Sec. V-A) by definition.  An out-of-range
-location or a negative latency makes the instance invalid (status 1).
+so the optimum is Eq. 2's (Sec. V-A) by definition.  With S > 1 an
+out-of-range location or a negative latency makes the instance invalid
+(status 1); with one stage there are no links and neither is read.
 
 parity: pinned by a network with one hub vertex per (stage boundary,
 location) built and solved by networkx (equal optima because every link is
@@ -35,7 +36,8 @@ def to_dense(lb):
     bad = np.zeros(B, bool)
     for b in range(B):
         loc, lat = lb.location[b], lb.latency[b]
-        bad[b] = bool((loc < 0).any() or (loc >= L).any() or (lat < 0).any())
+        # with one stage there are no links, and neither array is read
+        bad[b] = S > 1 and bool((loc < 0).any() or (loc >= L).any() or (lat < 0).any())
         if bad[b]:
             continue
         for k in range(S - 1):

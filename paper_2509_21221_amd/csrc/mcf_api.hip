@@ -36,6 +36,7 @@ struct gwtf_mcf {
     uint32_t *g_ex = nullptr, *g_en = nullptr, *g_ring = nullptr;
     unsigned long long *g_ring_key = nullptr;
     int32_t *g_pred = nullptr, *g_path = nullptr, *g_ctrl = nullptr;
+    int32_t *dense_arc = nullptr; // located batches: implied link delays, allocated on first use
     int32_t solved = 0; // batch size of the last successful solve (0 = none)
 };
 
@@ -85,6 +86,8 @@ void free_ws(gwtf_mcf_t *h)
     (void)hipFree(h->g_ctrl);
     (void)hipFree(h->g_ring);
     (void)hipFree(h->g_ring_key);
+    (void)hipFree(h->dense_arc);
+    h->dense_arc = nullptr;
     h->route = h->node_flow = h->arc_flow = h->pot = nullptr;
     h->stats = nullptr;
     h->state = nullptr;
@@ -186,33 +189,14 @@ extern "C" gwtf_status_t gwtf_mcf_create(const gwtf_mcf_shape_t *shape, void *hi
     return GWTF_OK;
 }
 
-extern "C" gwtf_status_t gwtf_mcf_solve_batch(gwtf_mcf_t *h, const gwtf_mcf_batch_t *b)
-{
-    if (!h) return fail(nullptr, GWTF_ERR_INVALID_ARG, "handle is NULL");
-    if (!b) return fail(h, GWTF_ERR_INVALID_ARG, "batch is NULL");
-    const int S = h->shape.num_stages, n = h->shape.nodes_per_stage;
-    if (b->batch < 1 || b->batch > h->shape.max_batch)
-        return fail(h, GWTF_ERR_INVALID_ARG, "batch outside [1, max_batch]");
-    if (!b->node_cap || !b->node_cost || !b->supply || !b->flow_value || !b->total_cost || !b->status)
-        return fail(h, GWTF_ERR_INVALID_ARG, "required pointer is NULL");
-    if ((S > 1) != (b->arc_cost != nullptr))
-        return fail(h, GWTF_ERR_INVALID_ARG, "arc_cost must be non-NULL exactly when S > 1");
-    hipError_t e = hipSetDevice(h->shape.device);
-    if (e != hipSuccess) return hip_fail(h, e, "hipSetDevice");
+namespace {
 
-    SolveParams p{};
-    p.B = b->batch;
-    p.S = S;
-    p.n = n;
-    p.cap = b->node_cap;
-    p.ncost = b->node_cost;
-    p.acost = b->arc_cost;
-    p.src = b->src_cost;
-    p.snk = b->snk_cost;
-    p.supply = b->supply;
-    p.F_out = b->flow_value;
-    p.cost_out = b->total_cost;
-    p.status_out = b->status;
+// Runs the solver passes for one batch (p describes it; loc/lat non-NULL
+// selects the location-factored grid pass for shapes that use the grid).
+gwtf_status_t run_passes(gwtf_mcf_t *h, SolveParams &p, const int32_t *loc, const int32_t *lat, int32_t L)
+{
+    const int S = h->shape.num_stages, n = h->shape.nodes_per_stage;
+    hipError_t e;
     p.route = h->route;
     p.node_flow = h->node_flow;
     p.arc_flow = h->arc_flow;
@@ -247,7 +231,10 @@ extern "C" gwtf_status_t gwtf_mcf_solve_batch(gwtf_mcf_t *h, const gwtf_mcf_batc
         gp.ring = h->g_ring;
         gp.ring_key = h->g_ring_key;
         gp.ring_slots = grid_ring_slots(S);
-        for (int i = 0; i < b->batch; ++i) {
+        gp.loc = loc;
+        gp.lat = lat;
+        gp.L = L;
+        for (int i = 0; i < p.B; ++i) {
             gp.instance = i;
             if ((e = launch_grid_pass(gp, h->grid_lds, h->stream)) != hipSuccess)
                 return hip_fail(h, e, "grid solver launch");
@@ -277,9 +264,82 @@ extern "C" gwtf_status_t gwtf_mcf_solve_batch(gwtf_mcf_t *h, const gwtf_mcf_batc
         if ((e = launch_fallback_pass(p, lds, h->stream)) != hipSuccess)
             return hip_fail(h, e, "fallback solver launch");
     }
-    h->solved = b->batch;
+    h->solved = p.B;
     h->err.clear();
     return GWTF_OK;
+}
+
+} // namespace
+
+extern "C" gwtf_status_t gwtf_mcf_solve_batch(gwtf_mcf_t *h, const gwtf_mcf_batch_t *b)
+{
+    if (!h) return fail(nullptr, GWTF_ERR_INVALID_ARG, "handle is NULL");
+    if (!b) return fail(h, GWTF_ERR_INVALID_ARG, "batch is NULL");
+    const int S = h->shape.num_stages, n = h->shape.nodes_per_stage;
+    if (b->batch < 1 || b->batch > h->shape.max_batch)
+        return fail(h, GWTF_ERR_INVALID_ARG, "batch outside [1, max_batch]");
+    if (!b->node_cap || !b->node_cost || !b->supply || !b->flow_value || !b->total_cost || !b->status)
+        return fail(h, GWTF_ERR_INVALID_ARG, "required pointer is NULL");
+    if ((S > 1) != (b->arc_cost != nullptr))
+        return fail(h, GWTF_ERR_INVALID_ARG, "arc_cost must be non-NULL exactly when S > 1");
+    hipError_t e = hipSetDevice(h->shape.device);
+    if (e != hipSuccess) return hip_fail(h, e, "hipSetDevice");
+
+    SolveParams p{};
+    p.B = b->batch;
+    p.S = S;
+    p.n = n;
+    p.cap = b->node_cap;
+    p.ncost = b->node_cost;
+    p.acost = b->arc_cost;
+    p.src = b->src_cost;
+    p.snk = b->snk_cost;
+    p.supply = b->supply;
+    p.F_out = b->flow_value;
+    p.cost_out = b->total_cost;
+    p.status_out = b->status;
+    return run_passes(h, p, nullptr, nullptr, 0);
+}
+
+extern "C" gwtf_status_t gwtf_mcf_solve_located(gwtf_mcf_t *h, const gwtf_mcf_located_batch_t *b)
+{
+    if (!h) return fail(nullptr, GWTF_ERR_INVALID_ARG, "handle is NULL");
+    if (!b) return fail(h, GWTF_ERR_INVALID_ARG, "batch is NULL");
+    const int S = h->shape.num_stages, n = h->shape.nodes_per_stage, L = b->num_locations;
+    if (b->batch < 1 || b->batch > h->shape.max_batch)
+        return fail(h, GWTF_ERR_INVALID_ARG, "batch outside [1, max_batch]");
+    if (L < 1 || L > kGridMaxLocations) return fail(h, GWTF_ERR_INVALID_ARG, "num_locations outside [1, 32]");
+    if (!b->node_cap || !b->node_cost || !b->location || !b->latency || !b->supply || !b->flow_value ||
+        !b->total_cost || !b->status)
+        return fail(h, GWTF_ERR_INVALID_ARG, "required pointer is NULL");
+    hipError_t e = hipSetDevice(h->shape.device);
+    if (e != hipSuccess) return hip_fail(h, e, "hipSetDevice");
+    const size_t na = size_t(std::max(S - 1, 0)) * n * n;
+    if (S > 1 && !h->dense_arc) {
+        if ((e = hipMalloc((void **)&h->dense_arc, sizeof(int32_t) * na * h->shape.max_batch)) != hipSuccess) {
+            h->dense_arc = nullptr;
+            return fail(h, GWTF_ERR_OUT_OF_MEMORY, std::string("hipMalloc located workspace: ") + hipGetErrorString(e));
+        }
+    }
+    // The implied dense delays serve every pass but the factored grid pass
+    // (the fallback pass included), so they are always written.
+    if ((e = launch_located_expand(b->batch, S, n, L, b->location, b->latency, h->dense_arc, h->stream)) != hipSuccess)
+        return hip_fail(h, e, "located expansion launch");
+
+    SolveParams p{};
+    p.B = b->batch;
+    p.S = S;
+    p.n = n;
+    p.cap = b->node_cap;
+    p.ncost = b->node_cost;
+    p.acost = S > 1 ? h->dense_arc : nullptr;
+    p.src = b->src_cost;
+    p.snk = b->snk_cost;
+    p.supply = b->supply;
+    p.F_out = b->flow_value;
+    p.cost_out = b->total_cost;
+    p.status_out = b->status;
+    return run_passes(h, p, b->location, b->latency, L);
 }
 
 extern "C" gwtf_status_t gwtf_mcf_get_flows(gwtf_mcf_t *h, int32_t first, int32_t count, int32_t *node_flow,

@@ -23,7 +23,14 @@ struct GridParams {
     int32_t *pred;      // [S*n] entry predecessor (low 16 bits) and exit predecessor (high)
     int32_t *path;      // [2*S*n + 8] arc codes of the augmenting path
     int32_t *ctrl;      // [kGridCtrlInts], cleared before each launch
+    // Location-factored links (NULL loc = dense link costs): the link from
+    // node i of stage k to node j of stage k+1 costs
+    // lat[loc[k][i]][loc[k+1][j]].
+    const int32_t *loc; // [B][S][n] in [0, L)
+    const int32_t *lat; // [B][L][L]
+    int32_t L;          // 1 <= L <= kGridMaxLocations
 };
+constexpr int kGridMaxLocations = 32;
 inline int grid_ring_slots(int S) { return S + 8; }
 size_t grid_pass_big_bytes(int S, int n);
 size_t grid_pass_lds_bytes(int S, int n, int64_t list_slots);

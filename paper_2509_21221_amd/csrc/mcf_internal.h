@@ -106,6 +106,10 @@ struct WhatifExpandParams {
 hipError_t launch_whatif_expand(const WhatifExpandParams &p, int32_t count, hipStream_t s);
 hipError_t launch_whatif_best(int32_t count, const int64_t *F, const int64_t *cost, const int32_t *status,
                               int64_t first, int32_t merge, int64_t *best, hipStream_t s);
+// Located instances (mcf_located.hip): the implied dense link delays
+// arc[b][k][i][j] = lat[b][loc[b][k][i]][loc[b][k+1][j]], -2 where invalid.
+hipError_t launch_located_expand(int32_t B, int32_t S, int32_t n, int32_t L, const int32_t *loc,
+                                 const int32_t *lat, int32_t *arc, hipStream_t s);
 int fallback_waves();
 hipError_t set_lds_limits(size_t max_bytes);
 

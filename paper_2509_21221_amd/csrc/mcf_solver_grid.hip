@@ -138,7 +138,7 @@ struct GridBarrier {
     __device__ bool sync(int *ok_lds, int *flag_lds) { return sync(false, ok_lds, flag_lds); }
 };
 
-__global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams gp)
+template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams gp)
 {
     const SolveParams &p = gp.base;
     const int b = gp.instance;
@@ -159,6 +159,16 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
     // links) uses it for the staged predecessors instead.
     uint16_t *cost16 = reinterpret_cast<uint16_t *>(smem);
     int *all_pred = reinterpret_cast<int *>(smem); // [SN]: entry pred low 16 bits, exit pred high
+    // Location-factored links use the same area (workgroups with incoming
+    // links only): locations of stage k-1's nodes and of the owned nodes,
+    // the latency matrix, and per location the best key of the rows that
+    // dropped in the current iteration.
+    constexpr bool located = kLocated;
+    const int L = located ? gp.L : 0;
+    int *rowloc = reinterpret_cast<int *>(smem);
+    int *colloc = rowloc + n;
+    int *latl = colloc + kGridNB;
+    unsigned long long *mkey = reinterpret_cast<unsigned long long *>(smem + align16(4 * (size_t(n) + kGridNB + L * L)));
     size_t o = align16(gp.big_bytes);
     auto take = [&](size_t bytes) {
         unsigned char *at = smem + o;
@@ -235,7 +245,41 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
             gpot[4 + 2 * q] = 0;
         }
     }
-    if (has_prev) {
+    if (located && S > 1) {
+        // A location outside [0, L) or a negative latency makes the instance
+        // invalid; each workgroup checks its owned nodes, workgroup 0 the
+        // latency matrix.  The cost bound counts the latencies of location
+        // pairs that some link of this block uses.
+        const int32_t *gl = gp.loc + size_t(b) * SN;
+        const int32_t *gt = gp.lat + size_t(b) * L * L;
+        if (tid < nown) {
+            const int a = gl[k * n + j0 + tid];
+            bad |= (a < 0) | (a >= L);
+        }
+        if (g == 0)
+            for (int e = tid; e < L * L; e += kGridThreads) bad |= gt[e] < 0;
+        if (has_prev) {
+            __shared__ unsigned rowmask, colmask;
+            if (tid == 0) rowmask = colmask = 0u;
+            __syncthreads();
+            for (int i = tid; i < n; i += kGridThreads) {
+                const int a = gl[(k - 1) * n + i];
+                const bool okl = a >= 0 && a < L;
+                rowloc[i] = okl ? a : 0;
+                if (okl) atomicOr(&rowmask, 1u << a);
+            }
+            if (tid < kGridNB) {
+                const int a = tid < nown ? gl[k * n + j0 + tid] : -1;
+                const bool okl = a >= 0 && a < L;
+                colloc[tid] = okl ? a : 0;
+                if (okl) atomicOr(&colmask, 1u << a);
+            }
+            for (int e = tid; e < L * L; e += kGridThreads) latl[e] = gt[e];
+            __syncthreads();
+            for (int e = tid; e < L * L; e += kGridThreads)
+                if (((rowmask >> (e / L)) & 1u) && ((colmask >> (e % L)) & 1u)) mx = max(mx, latl[e]);
+        }
+    } else if (has_prev) {
         const int32_t *layer = gac + size_t(k - 1) * n * n;
         for (int e = tid; e < n * kGridNB; e += kGridThreads) {
             const int i = e / kGridNB, c = e % kGridNB;
@@ -338,6 +382,7 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
             uint64_t final_key = ~0ull;
             bool converged = false;
             for (int t = 1; t <= 4 * V + 8; ++t) {
+                if (located && has_prev && tid < L) mkey[tid] = ~0ull;
                 const uint32_t *ex_f = gp.ex + size_t(t & 1) * SN + size_t(has_prev ? k - 1 : 0) * n;
                 const uint32_t *en_b = gp.en + size_t((t - 1) & 1) * SN + size_t(has_next ? k + 1 : 0) * n;
                 uint32_t *ex_out = gp.ex + size_t(t & 1) * SN;
@@ -416,12 +461,29 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
                 // the compacted list (which then holds the packed keys).
                 const bool packed = uint32_t(maxd) < kPackLimit;
                 const bool dense = packed && 2 * nrows > n;
-                if (dropped) rowlist[base + __popcll(m & ((1ull << lane) - 1ull))] = packed ? int(rowkey[tid]) : tid;
+                if (located) {
+                    // fold the dropped rows into their location's best key
+                    if (dropped) atomicMin(&mkey[rowloc[tid]], (unsigned long long)pack_key(dnew, tid));
+                } else if (dropped) {
+                    rowlist[base + __popcll(m & ((1ull << lane) - 1ull))] = packed ? int(rowkey[tid]) : tid;
+                }
                 __syncthreads();
 
                 // links into this block's entries, from the rows that dropped
                 uint64_t key = ~0ull;
-                if (col < nown && nrows > 0) {
+                if (located) {
+                    // one candidate per location: its best row plus the latency
+                    // to this column's location (a quarter of the locations each)
+                    if (col < nown && nrows > 0) {
+                        const int cl = colloc[col];
+                        const int chunk = (L + kGridRowGroups - 1) / kGridRowGroups;
+                        const int lo = min(L, rgrp * chunk), hi = min(L, lo + chunk);
+                        for (int a = lo; a < hi; ++a) {
+                            const unsigned long long mk = mkey[a];
+                            if (mk != ~0ull) key = min(key, (uint64_t)mk + (uint64_t(uint32_t(latl[a * L + cl])) << 32));
+                        }
+                    }
+                } else if (col < nown && nrows > 0) {
                     // this thread's share: a quarter of the rows (dense) or of the list
                     const int span = dense ? n : nrows;
                     const int chunk = (((span + kGridRowGroups - 1) / kGridRowGroups) + 3) & ~3;
@@ -554,7 +616,8 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
                     }
                     sh_key = ~0ull;
                     sh_changed = 0;
-                    my_relax += (long long)nrows * nown;
+                    my_relax += located ? (nrows > 0 ? (long long)nrows + (long long)nown * L : 0)
+                                        : (long long)nrows * nown;
                 }
             }
             if (timed_out) break;
@@ -729,7 +792,9 @@ __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams 
                         } else {
                             lpart[hi] = int16_t(j);
                             lamt[hi] = delta;
-                            lcost[hi] = gac[size_t(q) * n + j];
+                            lcost[hi] = located ? gp.lat[(size_t(b) * L + gp.loc[size_t(b) * SN + q]) * L +
+                                                         gp.loc[size_t(b) * SN + (k + 1) * n + j]]
+                                                : gac[size_t(q) * n + j];
                             llen[c] = hi + 1 - lo;
                         }
                         st(&gaf[size_t(q) * n + j], now);
@@ -828,16 +893,20 @@ int grid_pass_slices(int n) { return (n + kGridNB - 1) / kGridNB; }
 
 int grid_pass_blocks_per_cu(size_t lds_bytes)
 {
-    // Raising the dynamic-LDS ceiling is not needed on every runtime; a
-    // refusal is harmless but must not linger for a later launch check.
-    if (hipFuncSetAttribute(reinterpret_cast<const void *>(solve_grid_kernel),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, int(lds_bytes)) != hipSuccess)
-        (void)hipGetLastError();
-    int per_cu = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(solve_grid_kernel),
-                                                     kGridThreads, lds_bytes) != hipSuccess) {
-        (void)hipGetLastError();
-        return 0;
+    // Both variants (dense and location-factored links) must fit; raising
+    // the dynamic-LDS ceiling is not needed on every runtime, and a refusal
+    // is harmless but must not linger for a later launch check.
+    int per_cu = 1 << 30;
+    for (const void *f : {reinterpret_cast<const void *>(solve_grid_kernel<false>),
+                          reinterpret_cast<const void *>(solve_grid_kernel<true>)}) {
+        if (hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, int(lds_bytes)) != hipSuccess)
+            (void)hipGetLastError();
+        int here = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&here, f, kGridThreads, lds_bytes) != hipSuccess) {
+            (void)hipGetLastError();
+            return 0;
+        }
+        per_cu = std::min(per_cu, here);
     }
     return per_cu;
 }
@@ -849,8 +918,9 @@ hipError_t launch_grid_pass(const GridParams &gp, size_t lds_bytes, hipStream_t 
     if (e != hipSuccess) return e;
     GridParams arg = gp;
     void *args[] = {&arg};
-    return hipLaunchCooperativeKernel(reinterpret_cast<const void *>(solve_grid_kernel),
-                                      dim3(unsigned(gp.base.S * gp.slices)), dim3(kGridThreads), args,
+    const void *f = gp.loc ? reinterpret_cast<const void *>(solve_grid_kernel<true>)
+                           : reinterpret_cast<const void *>(solve_grid_kernel<false>);
+    return hipLaunchCooperativeKernel(f, dim3(unsigned(gp.base.S * gp.slices)), dim3(kGridThreads), args,
                                       unsigned(lds_bytes), s);
 }
 

@@ -3,7 +3,7 @@ marshalling only -- every step of the solve runs in the HIP library).
 
 The functions carry the C names (``gwtf_mcf_create``, ``gwtf_mcf_solve_batch``,
 ``gwtf_mcf_get_flows``, ``gwtf_mcf_get_stats``, ``gwtf_mcf_get_passes``,
-``gwtf_whatif_count``, ``gwtf_mcf_whatif_expand``, ``gwtf_mcf_whatif_best``,
+``gwtf_mcf_solve_located``, ``gwtf_whatif_count``, ``gwtf_mcf_whatif_expand``, ``gwtf_mcf_whatif_best``,
 ``gwtf_mcf_destroy``, ``gwtf_mcf_last_error``); ``Solver`` wraps them for
 torch device tensors.
 PyTorch only provides device memory and the HIP stream.
@@ -54,6 +54,15 @@ class gwtf_mcf_batch_t(ctypes.Structure):
                 ("status", ctypes.c_void_p)]
 
 
+class gwtf_mcf_located_batch_t(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("num_locations", ctypes.c_int32),
+                ("node_cap", ctypes.c_void_p), ("node_cost", ctypes.c_void_p),
+                ("location", ctypes.c_void_p), ("latency", ctypes.c_void_p),
+                ("src_cost", ctypes.c_void_p), ("snk_cost", ctypes.c_void_p),
+                ("supply", ctypes.c_void_p), ("flow_value", ctypes.c_void_p),
+                ("total_cost", ctypes.c_void_p), ("status", ctypes.c_void_p)]
+
+
 class gwtf_whatif_candidates_t(ctypes.Structure):
     _fields_ = [("num_candidates", ctypes.c_int32), ("slot", ctypes.c_int32),
                 ("cap", ctypes.c_void_p), ("cost", ctypes.c_void_p), ("in_cost", ctypes.c_void_p),
@@ -99,6 +108,8 @@ def load_library(path: str = LIB_PATH):
         lib.gwtf_mcf_get_stats.restype = ctypes.c_int
         lib.gwtf_mcf_get_passes.argtypes = [vp, i32, i32, vp]
         lib.gwtf_mcf_get_passes.restype = ctypes.c_int
+        lib.gwtf_mcf_solve_located.argtypes = [vp, ctypes.POINTER(gwtf_mcf_located_batch_t)]
+        lib.gwtf_mcf_solve_located.restype = ctypes.c_int
         lib.gwtf_whatif_count.argtypes = [i32, i32, ctypes.POINTER(ctypes.c_int64)]
         lib.gwtf_whatif_count.restype = ctypes.c_int
         lib.gwtf_mcf_whatif_expand.argtypes = [vp, ctypes.POINTER(gwtf_mcf_batch_t),
@@ -143,6 +154,16 @@ def gwtf_mcf_solve_batch(handle, batch: int, node_cap: int, node_cost: int, arc_
                          src_cost or None, snk_cost or None, supply or None, flow_value or None,
                          total_cost or None, status or None)
     _check(load_library().gwtf_mcf_solve_batch(ctypes.c_void_p(handle), ctypes.byref(b)), handle)
+
+
+def gwtf_mcf_solve_located(handle, batch: int, num_locations: int, node_cap: int, node_cost: int,
+                           location: int, latency: int, src_cost: int, snk_cost: int, supply: int,
+                           flow_value: int, total_cost: int, status: int) -> None:
+    """All arguments after ``num_locations`` are device addresses (0 = NULL)."""
+    b = gwtf_mcf_located_batch_t(batch, num_locations, node_cap or None, node_cost or None,
+                                 location or None, latency or None, src_cost or None, snk_cost or None,
+                                 supply or None, flow_value or None, total_cost or None, status or None)
+    _check(load_library().gwtf_mcf_solve_located(ctypes.c_void_p(handle), ctypes.byref(b)), handle)
 
 
 def gwtf_mcf_get_flows(handle, first: int, count: int, node_flow: int = 0, arc_flow: int = 0,
@@ -246,6 +267,28 @@ class Solver:
                    torch.empty(B, dtype=torch.int32, device=dev))
         F, cost, status = out
         gwtf_mcf_solve_batch(self.handle, B, *args, F.data_ptr(), cost.data_ptr(), status.data_ptr())
+        self.last_batch = B
+        return F, cost, status
+
+    def solve_located(self, node_cap, node_cost, location, latency, supply, src_cost=None, snk_cost=None,
+                      out=None):
+        """Located batch: [B][S][n] capacities, compute costs and locations,
+        [B][L][L] latencies, [B] supply, optional [B][n] data-node delays."""
+        torch = self.torch
+        S, n = self.S, self.n
+        B = int(supply.shape[0])
+        L = int(latency.shape[1]) if latency.dim() == 3 else -1
+        args = [self._arg(node_cap, (B, S, n), "node_cap"), self._arg(node_cost, (B, S, n), "node_cost"),
+                self._arg(location, (B, S, n), "location"), self._arg(latency, (B, L, L), "latency"),
+                self._arg(src_cost, (B, n), "src_cost"), self._arg(snk_cost, (B, n), "snk_cost"),
+                self._arg(supply, (B,), "supply")]
+        dev = torch.device("cuda", self.device)
+        if out is None:
+            out = (torch.empty(B, dtype=torch.int64, device=dev),
+                   torch.empty(B, dtype=torch.int64, device=dev),
+                   torch.empty(B, dtype=torch.int32, device=dev))
+        F, cost, status = out
+        gwtf_mcf_solve_located(self.handle, B, L, *args, F.data_ptr(), cost.data_ptr(), status.data_ptr())
         self.last_batch = B
         return F, cost, status
 

@@ -111,3 +111,11 @@ def test_located_pins_reject_mutant(name):
     text = open(OL.__file__).read()
     assert text.count(before) == 1, f"mutation anchor for {name} not unique"
     assert not _located_pins_pass(_variant(text.replace(before, after), name))
+
+
+def test_single_stage_reads_no_location():
+    lb = W.random_located(2, 1, 3, 2, seed=2)
+    lb.location[0][0, 0] = 7
+    lb.latency[1][0, 1] = -3
+    r = OL.solve(lb, flows=False, potentials=False)
+    assert r["status"].tolist() == [0, 0]
