@@ -75,8 +75,9 @@ def measured_traffic(kernel: str, config: int, kernel_s: float):
 
 
 KERNELS = {1: "solve_pipe_kernel", 2: "solve_kernel (LDS state)", 3: "solve_grid_kernel",
-           4: "solve_kernel (global-memory state)"}
-KERNEL_SYMBOLS = {1: "solve_pipe_kernel", 2: "solve_kernel_lds", 3: "solve_grid_kernel", 4: "solve_kernel_global"}
+           4: "solve_kernel (global-memory state)", 5: "solve_small_kernel (four instances per wave)"}
+KERNEL_SYMBOLS = {1: "solve_pipe_kernel", 2: "solve_kernel_lds", 3: "solve_grid_kernel", 4: "solve_kernel_global",
+                  5: "solve_small_kernel"}
 
 
 def stored_oracle_baseline(config: int):

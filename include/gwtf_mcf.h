@@ -55,7 +55,8 @@ enum {
     GWTF_PASS_REGISTER = 1, /* one workgroup, link costs in registers: 16 < n <= 64, S <= 32 */
     GWTF_PASS_LDS = 2,      /* one workgroup, instance state in LDS: n <= 64 */
     GWTF_PASS_GRID = 3,     /* one instance over S * ceil(n/128) co-resident workgroups: 64 < n <= 512 */
-    GWTF_PASS_GLOBAL = 4    /* one workgroup, instance state in device memory: any shape */
+    GWTF_PASS_GLOBAL = 4,   /* one workgroup, instance state in device memory: any shape */
+    GWTF_PASS_PACKED = 5    /* four instances per wave: S <= 8, n <= 16, supply <= 255, costs <= 2047 */
 };
 
 /* arc_cost entry meaning "these two nodes share no link". */
@@ -122,7 +123,8 @@ gwtf_status_t gwtf_mcf_get_stats(gwtf_mcf_t *h, int32_t first, int32_t count, in
 /* Which solver pass produced each instance of the last solve, into a caller
  * device buffer pass[count] (int32, GWTF_PASS_*).  The pass follows from the
  * handle's shape, except that an instance whose link costs exceed 65534 or
- * whose flow lists outgrow LDS moves to GWTF_PASS_GLOBAL.  Enqueued on the
+ * whose flow lists outgrow LDS, or one outside GWTF_PASS_PACKED's bounds,
+ * moves to GWTF_PASS_GLOBAL.  Enqueued on the
  * handle's stream; errors as for gwtf_mcf_get_stats. */
 gwtf_status_t gwtf_mcf_get_passes(gwtf_mcf_t *h, int32_t first, int32_t count, int32_t *pass);
 

@@ -8,6 +8,7 @@
 #include "mcf_grid.h"
 #include "mcf_internal.h"
 #include "mcf_pipe.h"
+#include "mcf_small.h"
 
 #include <algorithm>
 #include <cstdio>
@@ -212,7 +213,14 @@ gwtf_status_t run_passes(gwtf_mcf_t *h, SolveParams &p, const int32_t *loc, cons
     const int64_t pipe_slots = (n > 16 && pipe_pass_fits(S, n)) ? pipe_pass_slots(S, h->lds_max) : 0;
     const int waves = lds_waves(n);
     const int64_t slots = pipe_slots > 0 ? 0 : lds_slots(S, n, waves, h->lds_max);
-    if (h->grid) {
+    if (small_pass_fits(S, n)) {
+        // Four instances per wave; instances outside the packed bounds go to
+        // the fallback pass.
+        p.list_slots = 0;
+        p.route_all = 0;
+        if ((e = launch_small_pass(p, h->stream)) != hipSuccess) return hip_fail(h, e, "packed solver launch");
+        need_fallback = true;
+    } else if (h->grid) {
         // One cooperative launch per instance; instances whose link costs
         // need more than 16 bits or whose flow lists outgrow LDS go to the
         // fallback pass.

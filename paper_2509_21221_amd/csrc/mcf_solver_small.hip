@@ -1,0 +1,468 @@
+// Packed pass for small instances: four instances per wave, for at most 8
+// stages of at most 16 nodes (the node-addition batches of paper Sec. VI and
+// the 4 x 4 / 8 x 8 presets).
+//
+// Same method as the other passes (successive shortest paths with Johnson
+// potentials on the node-split stage graph, paper Sec. V-A Eq. 2); what
+// differs is the mapping.  One wave = four 16-lane rows (the DPP row of
+// CDNA), one instance per row, lane j of a row = node j of every stage:
+//
+//  * Keys.  A vertex label is kept as key = label << 5 | code, where code
+//    names the predecessor arc: for an entry, 0..15 = the link from that
+//    exit of the previous stage, 16 = the reverse compute arc, 17 = the
+//    data node; for an exit, 0..15 = the reverse link from that entry of the
+//    next stage, 16 = the compute arc.  Finite keys stay below 2^30 (labels
+//    below 2^25); unreached vertices hold kKeyInf = 2^31 | 31, and a missing
+//    link costs 2^30, so no sum or difference of a key and a cost wraps and
+//    none that involves an unreached key or a missing link lands in the
+//    finite range.  A key is replaced only by one with a strictly smaller
+//    label, which keeps the predecessors a tree.
+//  * Forward relaxation.  The incoming link costs of a stage sit in vector
+//    registers (cost << 5, column j in lane j, one register per row); the
+//    previous stage's exit keys reach lane j through DPP row broadcasts
+//    fused into the adds, so a dense 16 x 16 relaxation is 16 broadcast-adds
+//    and 8 three-way minima per stage.
+//  * Reverse links (links carrying flow) are pulled at the exit's lane from
+//    the next stage's entry keys, over the exit's row of link costs (a copy
+//    in LDS) and a 16-bit mask of the links with flow.
+//  * Rounds: a forward sweep over the stages, then a backward sweep, until
+//    a backward sweep changes nothing in any of the wave's instances.
+//  * After each search: potentials (device workspace), then each row walks
+//    its own path twice (bottleneck, then apply) over the node flows and the
+//    per-link flows kept in LDS.
+//
+// Instances outside the pass's bounds (supply above 255, a cost above 2047,
+// labels that could reach 2^25) are routed to the fallback pass.
+#include "mcf_device.h"
+#include "mcf_small.h"
+
+namespace gwtf {
+namespace {
+
+using namespace dev;
+
+constexpr int kRows = 4;                    // instances per wave
+constexpr uint32_t kKeyInf = 0x80000000u | 31u;
+constexpr uint32_t kFiniteLimit = 0x40000000u; // keys at or above are unreached
+constexpr uint32_t kNoLink = 0x40000000u;      // cost << 5 of a missing link
+constexpr uint32_t kCodeSplit = 16, kCodeSrc = 17;
+constexpr int kMaxCost = 2047;
+constexpr int kMaxSupply = 255;
+constexpr int64_t kSmallLabelLimit = (int64_t(1) << 25) - (int64_t(1) << 16);
+
+// The largest key a strictly better candidate must stay below.
+__device__ __forceinline__ uint32_t lim(uint32_t key) { return min(key & ~31u, kFiniteLimit); }
+
+template <int I> __device__ __forceinline__ uint32_t row_bcast(uint32_t x)
+{
+    return uint32_t(__builtin_amdgcn_update_dpp(0, int(x), 0x150 + I, 0xf, 0xf, false));
+}
+
+// min over the 16 rows i of (key of exit i with code i) + cost(i -> this lane)
+template <int I> struct Relax {
+    static __device__ __forceinline__ void run(uint32_t xr, const uint32_t (&c)[16], uint32_t &best)
+    {
+        best = min(best, row_bcast<I>(xr) + c[I]);
+        Relax<I + 1>::run(xr, c, best);
+    }
+};
+template <> struct Relax<16> {
+    static __device__ __forceinline__ void run(uint32_t, const uint32_t (&)[16], uint32_t &) {}
+};
+
+// min over the 16 entries j of the next stage with flow on (this lane -> j):
+// (key of entry j with code j) - cost(this lane -> j)
+template <int J> struct Pull {
+    static __device__ __forceinline__ void run(uint32_t yr, const uint32_t (&c)[8], uint32_t nomask, uint32_t &best)
+    {
+        const uint32_t w = c[J >> 1];
+        const uint32_t c5 = (J & 1) ? (w >> 16) : (w & 0xffffu);
+        // no flow on this link: force the candidate out of the finite range
+        const uint32_t off = uint32_t(int32_t(nomask << (31 - J)) >> 31) & 0xc0000000u;
+        best = min(best, (row_bcast<J>(yr) - c5) | off);
+        Pull<J + 1>::run(yr, c, nomask, best);
+    }
+};
+template <> struct Pull<16> {
+    static __device__ __forceinline__ void run(uint32_t, const uint32_t (&)[8], uint32_t, uint32_t &) {}
+};
+
+// min over the 16 lanes of a row, in every lane of the row
+__device__ __forceinline__ uint32_t row_min(uint32_t v)
+{
+    v = min(v, uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0xb1, 0xf, 0xf, false)));  // quad_perm [1,0,3,2]
+    v = min(v, uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x4e, 0xf, 0xf, false)));  // quad_perm [2,3,0,1]
+    v = min(v, uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x141, 0xf, 0xf, false))); // row_half_mirror
+    v = min(v, uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x140, 0xf, 0xf, false))); // row_mirror
+    return v;
+}
+// OR over the whole wave
+__device__ __forceinline__ uint32_t row_or_wave(uint32_t v)
+{
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v |= uint32_t(__shfl_xor(int(v), off));
+    return v;
+}
+__device__ __forceinline__ int row_max_i(int v)
+{
+    v = max(v, __builtin_amdgcn_update_dpp(0, v, 0xb1, 0xf, 0xf, false));
+    v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x4e, 0xf, 0xf, false));
+    v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x141, 0xf, 0xf, false));
+    v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x140, 0xf, 0xf, false));
+    return v;
+}
+
+// LDS of one wave, laid out for the largest stage count so that every
+// offset is a constant: node words (flow | capacity << 8 | compute cost <<
+// 16), per exit the mask of its links with flow, per link its flow, and per
+// exit its row of link costs (cost << 5).
+template <int MAXS> struct SmallLayout {
+    static constexpr size_t node = 0;
+    static constexpr size_t mask = node + 4 * MAXS * 64;
+    static constexpr size_t lflow = mask + 4 * MAXS * 64;
+    static constexpr size_t lcost = lflow + size_t(MAXS - 1) * kRows * 256;
+    static constexpr size_t total = lcost + 2 * size_t(MAXS - 1) * kRows * 256;
+};
+
+template <int MAXS>
+__global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
+{
+    const int S = p.S, n = p.n, SN = S * n, V = 2 * SN + 3;
+    const int lane = threadIdx.x, g = lane >> 4, j = lane & 15;
+    const int b = blockIdx.x * kRows + g;
+    const bool inst = b < p.B;      // this row holds an instance
+    const bool node = inst && j < n; // this lane is a real node
+    extern __shared__ __align__(16) unsigned char smem[];
+    using Ly = SmallLayout<MAXS>;
+    uint32_t *nodew = reinterpret_cast<uint32_t *>(smem + Ly::node);  // [S][64]
+    uint32_t *lmask = reinterpret_cast<uint32_t *>(smem + Ly::mask);  // [S][64]: exit's links with flow
+    uint8_t *lflow = smem + Ly::lflow;                                // [S-1][4][16][16]: (k, i) -> (k+1, j)
+    uint16_t *lcost = reinterpret_cast<uint16_t *>(smem + Ly::lcost); // [S-1][4][16][16]
+    auto lidx = [&](int k, int i, int jj) { return ((k * kRows + g) * 16 + i) * 16 + jj; };
+
+    const int supply = inst ? p.supply[b] : 0;
+    const int32_t *gcap = p.cap + size_t(b) * SN;
+    const int32_t *gnc = p.ncost + size_t(b) * SN;
+    const int32_t *gac = S > 1 ? p.acost + size_t(b) * (S - 1) * n * n : nullptr;
+    int32_t *gpot = p.pot + size_t(b) * V;
+
+    // ---------------- ingest + validate ----------------
+    int bad = supply < 0, mx = 0;
+    uint32_t cin[MAXS][16]; // [k][i]: cost << 5 of link (k-1, i) -> (k, j), k >= 1
+#pragma unroll
+    for (int k = 0; k < MAXS; ++k) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) cin[k][r] = 0;
+        if (k >= S) continue;
+        const int q = k * n + j;
+        const int cp = node ? gcap[q] : 0, w = node ? gnc[q] : 0;
+        bad |= (cp < 0) | (w < 0);
+        mx = max(mx, w);
+        const int ec = min(max(cp, 0), max(supply, 0));
+        nodew[k * 64 + lane] = uint32_t(min(ec, kMaxSupply)) << 8 | uint32_t(min(max(w, 0), kMaxCost)) << 16;
+        lmask[k * 64 + lane] = 0;
+    }
+    // link costs: each row's n x n block of a stage pair, read with
+    // consecutive lanes on consecutive elements, into the row-major LDS copy
+    for (int k = 0; k + 1 < S; ++k) {
+        for (int e = j; e < 256; e += 16) {
+            const int i = e >> 4, jj = e & 15;
+            int a = 0;
+            if (inst && i < n && jj < n) a = gac[size_t(k) * n * n + size_t(i) * n + jj];
+            bad |= a < -1;
+            mx = max(mx, a);
+            // a missing link never carries flow, so its LDS copy is never read
+            lcost[lidx(k, i, jj)] = a < 0 ? 0xffffu : uint16_t(uint32_t(min(a, kMaxCost)) << 5);
+            lflow[lidx(k, i, jj)] = 0;
+        }
+    }
+    __syncthreads();
+    // columns into registers: lane j holds the costs of the links into node j
+#pragma unroll
+    for (int k = 1; k < MAXS; ++k) {
+        if (k >= S) break;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const uint32_t c5 = lcost[lidx(k - 1, r, j)];
+            cin[k][r] = c5 == 0xffffu ? kNoLink : c5;
+        }
+    }
+    int srcc = node && p.src ? p.src[size_t(b) * n + j] : 0;
+    int snkc = node && p.snk ? p.snk[size_t(b) * n + j] : 0;
+    bad |= (srcc < 0) | (snkc < 0);
+    mx = max(mx, max(srcc, snkc));
+    if (inst)
+        for (int q = j; q < V; q += 16) gpot[q] = 0;
+    bad = row_max_i(bad);
+    mx = row_max_i(mx);
+    int status = 0;
+    if (bad) status = 1;
+    else if (int64_t(V) * mx >= kLabelBound) status = 2;
+    const bool fits = supply <= kMaxSupply && mx <= kMaxCost && int64_t(V) * mx < kSmallLabelLimit;
+    const bool mine = inst && (status != 0 || fits); // this pass owns the instance
+    if (inst && j == 0) p.route[b] = mine ? kRouteSmall : kRouteFallback;
+    const uint32_t src5 = uint32_t(min(max(srcc, 0), kMaxCost)) << 5, snk5 = uint32_t(min(max(snkc, 0), kMaxCost)) << 5;
+
+    // ---------------- successive shortest paths ----------------
+    long long F = 0, cost = 0, augs = 0, rounds = 0, rows_relaxed = 0, pulls = 0;
+    int pit = 0;
+    bool active = mine && status == 0 && supply > 0; // this row still searches
+    uint64_t tick = wall_clock64(), clk_fwd = 0, clk_bwd = 0, clk_aug = 0, clk_other = 0;
+    uint32_t din[MAXS], dout[MAXS];
+    while (__any(active)) {
+        // labels of a fresh search
+#pragma unroll
+        for (int k = 0; k < MAXS; ++k) {
+            din[k] = (k == 0 && active && j < n) ? (src5 | kCodeSrc) : kKeyInf;
+            dout[k] = kKeyInf;
+        }
+        clk_other += lap(tick);
+        int round_count = 0;
+        bool fault = false;
+        for (;;) {
+            // -------- forward sweep --------
+#pragma unroll
+            for (int k = 0; k < MAXS; ++k) {
+                if (k >= S) break;
+                const uint32_t nw = nodew[k * 64 + lane];
+                const uint32_t fl = nw & 255u, ec = (nw >> 8) & 255u, nc5 = ((nw >> 16) & 2047u) << 5;
+                uint32_t di = din[k], dq = dout[k];
+                if (k >= 1) {
+                    const uint32_t xr = (dout[k - 1] & ~31u) | uint32_t(j);
+                    uint32_t best = kKeyInf;
+                    Relax<0>::run(xr, cin[k], best);
+                    di = best < lim(di) ? best : di;
+                }
+                if (fl > 0) {
+                    const uint32_t cand = ((dq & ~31u) - nc5) | kCodeSplit;
+                    di = cand < lim(di) ? cand : di;
+                }
+                if (fl < ec) {
+                    const uint32_t cand = ((di & ~31u) + nc5) | kCodeSplit;
+                    dq = cand < lim(dq) ? cand : dq;
+                }
+                din[k] = di;
+                dout[k] = dq;
+            }
+            rows_relaxed += S - 1;
+            clk_fwd += lap(tick);
+            // -------- backward sweep --------
+            bool chg = false;
+#pragma unroll
+            for (int kk = MAXS - 1; kk >= 0; --kk) {
+                if (kk >= S) continue;
+                const int k = kk;
+                const uint32_t nw = nodew[k * 64 + lane];
+                const uint32_t fl = nw & 255u, nc5 = ((nw >> 16) & 2047u) << 5;
+                uint32_t di = din[k], dq = dout[k];
+                // links with flow out of this exit, read here each time (values
+                // derived from it must not be kept live across the rounds)
+                const uint32_t lm =
+                    k + 1 < S ? __hip_atomic_load(&lmask[k * 64 + lane], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) : 0u;
+                if (k + 1 < S && __any(lm != 0u)) {
+                    // this exit's row of link costs
+                    uint32_t cr[8];
+                    const uint32_t *row = reinterpret_cast<const uint32_t *>(&lcost[lidx(k, j, 0)]);
+#pragma unroll
+                    for (int r = 0; r < 8; ++r) cr[r] = __hip_atomic_load(row + r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+                    const uint32_t yr = (din[k + 1] & ~31u) | uint32_t(j);
+                    uint32_t best = kKeyInf;
+                    Pull<0>::run(yr, cr, ~lm, best);
+                    pulls += __popc(lm);
+                    dq = best < lim(dq) ? best : dq;
+                }
+                if (fl > 0) {
+                    const uint32_t cand = ((dq & ~31u) - nc5) | kCodeSplit;
+                    di = cand < lim(di) ? cand : di;
+                }
+                chg |= (di != din[k]) | (dq != dout[k]);
+                din[k] = di;
+                dout[k] = dq;
+            }
+            clk_bwd += lap(tick);
+            ++rounds;
+            if (!__any(chg)) break;
+            // Bellman-Ford settles within |V| rounds without a negative cycle
+            if (++round_count > V) {
+                fault = true;
+                break;
+            }
+        }
+        if (fault) {
+            if (active) status = kStatusInternal;
+            active = false;
+            break;
+        }
+
+        // -------- sink, potentials --------
+        uint32_t tk = kKeyInf;
+#pragma unroll
+        for (int k = 0; k < MAXS; ++k)
+            if (k == S - 1 && j < n) tk = ((dout[k] & ~31u) + snk5) | uint32_t(j);
+        tk = row_min(tk);
+        const bool aug = active && tk < kFiniteLimit;
+        if (active && !aug) active = false; // sink unreachable: the flow is maximum
+        const int Dt = int(tk >> 5), predt = int(tk & 31u);
+        if (aug && j < n) {
+            const int dred = Dt - pit;
+#pragma unroll
+            for (int k = 0; k < MAXS; ++k) {
+                if (k >= S) break;
+                const int q = k * n + j;
+                const int li = din[k] < kFiniteLimit ? int(din[k] >> 5) : INT32_MAX;
+                const int lo = dout[k] < kFiniteLimit ? int(dout[k] >> 5) : INT32_MAX;
+                gpot[3 + 2 * q] = min(li, gpot[3 + 2 * q] + dred);
+                gpot[4 + 2 * q] = min(lo, gpot[4 + 2 * q] + dred);
+            }
+        }
+
+        // -------- path: bottleneck, then apply (each row its own) --------
+        // Keys of vertex (k, v): the lane v of this row, stage k, selected by
+        // value since k differs between rows.
+        auto key_at = [&](int k, int v, bool exit) {
+            uint32_t x = kKeyInf;
+#pragma unroll
+            for (int kk = 0; kk < MAXS; ++kk)
+                if (kk == k) x = exit ? dout[kk] : din[kk];
+            return uint32_t(__shfl(int(x), (g << 4) | v));
+        };
+        int delta = aug ? supply - int(F) : 0;
+        bool bad_walk = false;
+        for (int pass = 0; pass < 2; ++pass) {
+            int k = S - 1, v = predt;
+            bool at_exit = true, walking = aug && delta > 0;
+            for (int steps = 0; __any(walking); ++steps) {
+                // every lane takes part in the cross-lane reads
+                const uint32_t key = key_at(k, v, at_exit);
+                if (!walking) continue;
+                if (steps > 2 * S * 16 + 4) {
+                    bad_walk = true;
+                    walking = false;
+                    continue;
+                }
+                const uint32_t code = key & 31u;
+                if (at_exit) {
+                    if (code == kCodeSplit) {
+                        const int at = k * 64 + (g << 4) + v;
+                        const uint32_t nw = nodew[at];
+                        if (pass == 0) delta = min(delta, int((nw >> 8) & 255u) - int(nw & 255u));
+                        else if (j == 0) nodew[at] = nw + uint32_t(delta);
+                        at_exit = false;
+                    } else if (code < 16 && k + 1 < S) {
+                        const int e = lidx(k, v, int(code));
+                        const int f = lflow[e];
+                        if (pass == 0) delta = min(delta, f);
+                        else if (j == 0) {
+                            lflow[e] = uint8_t(f - delta);
+                            if (f - delta == 0) lmask[k * 64 + (g << 4) + v] &= ~(1u << code);
+                        }
+                        k = k + 1;
+                        v = int(code);
+                        at_exit = false;
+                    } else {
+                        bad_walk = true;
+                        walking = false;
+                    }
+                } else {
+                    if (code == kCodeSrc && k == 0) {
+                        walking = false;
+                    } else if (code == kCodeSplit) {
+                        const int at = k * 64 + (g << 4) + v;
+                        const uint32_t nw = nodew[at];
+                        if (pass == 0) delta = min(delta, int(nw & 255u));
+                        else if (j == 0) nodew[at] = nw - uint32_t(delta);
+                        at_exit = true;
+                    } else if (code < 16 && k >= 1) {
+                        if (pass == 1 && j == 0) {
+                            const int e = lidx(k - 1, int(code), v);
+                            const int f = lflow[e] + delta;
+                            lflow[e] = uint8_t(f);
+                            lmask[(k - 1) * 64 + (g << 4) + int(code)] |= 1u << v;
+                        }
+                        k = k - 1;
+                        v = int(code);
+                        at_exit = true;
+                    } else {
+                        bad_walk = true;
+                        walking = false;
+                    }
+                }
+            }
+            if (pass == 0 && aug && !bad_walk && delta <= 0) bad_walk = true;
+            if (__any(bad_walk)) {
+                // a fault in any row: those rows stop with an internal status
+                if (bad_walk && active) status = kStatusInternal;
+                if (bad_walk) active = false;
+                if (pass == 0) delta = bad_walk ? 0 : delta;
+            }
+        }
+        if (aug && !bad_walk) {
+            F += delta;
+            cost += (long long)delta * Dt;
+            ++augs;
+            pit = Dt;
+            if (F >= supply) active = false;
+        }
+        clk_aug += lap(tick);
+    }
+
+    // ---------------- export ----------------
+    if (!mine) return; // the fallback pass writes this instance
+    const bool ok = status == 0;
+    const size_t na = size_t(S > 1 ? S - 1 : 0) * n * n;
+    int32_t *nf = p.node_flow + size_t(b) * SN;
+    int32_t *af = p.arc_flow + size_t(b) * na;
+    if (j < n) {
+#pragma unroll
+        for (int k = 0; k < MAXS; ++k) {
+            if (k >= S) break;
+            const int q = k * n + j;
+            nf[q] = ok ? int(nodew[k * 64 + lane] & 255u) : 0;
+            if (!ok) {
+                gpot[3 + 2 * q] = 0;
+                gpot[4 + 2 * q] = 0;
+            }
+            if (k + 1 < S)
+                for (int i = 0; i < n; ++i) af[size_t(k) * n * n + size_t(i) * n + j] = ok ? lflow[lidx(k, i, j)] : 0;
+        }
+    }
+    if (j == 0) {
+        gpot[0] = 0;
+        gpot[1] = 0;
+        gpot[2] = ok ? pit : 0;
+        p.F_out[b] = ok ? F : 0;
+        p.cost_out[b] = ok ? cost : 0;
+        p.status_out[b] = status;
+        int64_t *s = p.stats + size_t(b) * kStatsPerInstance;
+        s[0] = augs;
+        s[1] = rounds;
+        s[2] = rows_relaxed * n;
+        s[3] = pulls;
+        const double ns_per_tick = 1e6 / double(p.clock_khz > 0 ? p.clock_khz : 100000);
+        s[4] = int64_t(double(clk_fwd) * ns_per_tick);
+        s[5] = int64_t(double(clk_bwd) * ns_per_tick);
+        s[6] = int64_t(double(clk_aug) * ns_per_tick);
+        s[7] = int64_t(double(clk_other) * ns_per_tick);
+        s[8] = 0;
+        s[9] = 0;
+    }
+}
+
+} // namespace
+
+bool small_pass_fits(int S, int n) { return S >= 1 && S <= kSmallMaxStages && n <= 16; }
+
+size_t small_pass_lds_bytes(int S)
+{
+    (void)S;
+    return SmallLayout<kSmallMaxStages>::total;
+}
+
+hipError_t launch_small_pass(const SolveParams &p, hipStream_t s)
+{
+    const unsigned blocks = unsigned((p.B + kRows - 1) / kRows);
+    hipLaunchKernelGGL((solve_small_kernel<kSmallMaxStages>), dim3(blocks), dim3(64), small_pass_lds_bytes(p.S), s, p);
+    return hipGetLastError();
+}
+
+} // namespace gwtf

@@ -35,6 +35,7 @@ GWTF_PASS_REGISTER = 1
 GWTF_PASS_LDS = 2
 GWTF_PASS_GRID = 3
 GWTF_PASS_GLOBAL = 4
+GWTF_PASS_PACKED = 5
 
 STATUS_NAMES = {0: "GWTF_OK", 1: "GWTF_ERR_INVALID_ARG", 2: "GWTF_ERR_OUT_OF_MEMORY",
                 3: "GWTF_ERR_DEVICE", 4: "GWTF_ERR_NOT_SOLVED", 5: "GWTF_ERR_RANGE"}

@@ -45,7 +45,7 @@ def test_header_constants_match_binding():
     for name, value in [("GWTF_OK", 0), ("GWTF_ERR_INVALID_ARG", 1), ("GWTF_ERR_OUT_OF_MEMORY", 2),
                         ("GWTF_ERR_DEVICE", 3), ("GWTF_ERR_NOT_SOLVED", 4), ("GWTF_ERR_RANGE", 5),
                         ("GWTF_INST_OK", 0), ("GWTF_INST_BAD_INPUT", 1), ("GWTF_INST_OVERFLOW", 2),
-                        ("GWTF_PASS_REGISTER", 1), ("GWTF_PASS_LDS", 2), ("GWTF_PASS_GRID", 3),
+                        ("GWTF_PASS_REGISTER", 1), ("GWTF_PASS_LDS", 2), ("GWTF_PASS_GRID", 3), ("GWTF_PASS_PACKED", 5),
                         ("GWTF_PASS_GLOBAL", 4)]:
         assert re.search(rf"\b{name}\s*=\s*{value}\b", text), name
         assert getattr(mcf, name) == value

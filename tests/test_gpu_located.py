@@ -64,13 +64,14 @@ def check(lb, g, ref, certify=None):
 
 
 @pytest.mark.parametrize("S,n,L,B,expect_pass", [
-    (3, 6, 3, 24, mcf.GWTF_PASS_LDS),
+    (3, 6, 3, 24, mcf.GWTF_PASS_PACKED),
+    (10, 6, 3, 8, mcf.GWTF_PASS_LDS),
     (4, 24, 5, 12, mcf.GWTF_PASS_REGISTER),
     (3, 80, 7, 4, mcf.GWTF_PASS_GRID),
     (2, 130, 32, 3, mcf.GWTF_PASS_GRID),
     (5, 200, 10, 2, mcf.GWTF_PASS_GRID),
     (1, 100, 4, 3, mcf.GWTF_PASS_GRID),
-    (2, 1, 1, 8, mcf.GWTF_PASS_LDS),
+    (2, 1, 1, 8, mcf.GWTF_PASS_PACKED),
 ])
 def test_random_located(S, n, L, B, expect_pass):
     lb = W.random_located(B, S, n, L, seed=21, supply_hi=40)

@@ -160,6 +160,45 @@ def test_grid_pass_routing_and_status():
                   g["src_flow"][b], g["snk_flow"][b], g["potential"][b])
 
 
+@pytest.mark.parametrize("S,n,B,holes,zero", [
+    (1, 1, 5, 0.0, 0.0), (2, 16, 7, 0.2, 0.1), (8, 16, 33, 0.1, 0.1), (8, 13, 64, 0.0, 0.0),
+    (5, 9, 10, 0.3, 0.2), (3, 4, 1, 0.0, 0.0), (7, 11, 6, 0.0, 0.3),
+])
+def test_packed_pass_shapes(S, n, B, holes, zero):
+    """Shapes served by the packed pass (S <= 8, n <= 16): four instances per
+    wave, batches that leave a wave partly empty, missing links, deleted
+    nodes."""
+    batch = W.random_small(B, S, n, seed=31, cap_hi=9, cost_hi=400, supply_hi=4 * n + 8,
+                           holes=holes, zero_cap=zero)
+    say("packed", S, n, B)
+    g = gpu_solve(batch)
+    compare(batch, g, oracle.solve(batch))
+    assert (g["passes"] == mcf.GWTF_PASS_PACKED).all()
+
+
+def test_packed_pass_routing_and_status():
+    """Instances outside the packed bounds (supply above 255, a cost above
+    2047) move to the global pass; bad input and label overflow are reported
+    by the packed pass itself."""
+    batch = W.random_small(9, 4, 8, seed=37, cap_hi=9, cost_hi=400, supply_hi=40)
+    batch.supply[1] = 256
+    batch.arc_cost[2, 1, 3, 4] = 2048
+    batch.node_cost[3, 2, 2] = 5000
+    batch.src_cost[4, 0] = 3000
+    batch.node_cap[5, 1, 1] = -3
+    batch.node_cost[6, 0, 0] = 2 ** 27    # (2Sn+3) * max cost >= 2^29
+    say("packed routing")
+    g = gpu_solve(batch)
+    assert g["status"].tolist() == [0, 0, 0, 0, 0, 1, 2, 0, 0]
+    assert g["passes"].tolist() == [5, 4, 4, 4, 4, 5, 5, 5, 5]
+    keep = [0, 1, 2, 3, 4, 7, 8]
+    ref = oracle.solve(batch.subset(keep))
+    assert (g["F"][keep] == ref["F"]).all() and (g["cost"][keep] == ref["cost"]).all()
+    for b in keep:
+        C.certify(batch, b, int(g["F"][b]), int(g["cost"][b]), g["node_flow"][b], g["arc_flow"][b],
+                  g["src_flow"][b], g["snk_flow"][b], g["potential"][b])
+
+
 def test_lists_outgrow_lds_use_fallback():
     """Capacities of 64 make every exit vertex reserve 64 flow-list slots,
     more than LDS holds at this shape, so the global-memory pass runs."""

@@ -233,7 +233,7 @@ def test_node_addition_setting1_full():
     t0 = time.time()
     g = gpu_whatif(base, slot, cands)
     say("gpu whatif done", time.time() - t0)
-    assert (g["passes"] == mcf.GWTF_PASS_LDS).all()
+    assert (g["passes"] == mcf.GWTF_PASS_PACKED).all()
     ref_batch = OW.expand(base, slot, cands)
     say("oracle expand done", time.time() - t0)
     assert_same_batch(g, ref_batch)
