@@ -96,13 +96,6 @@ __device__ __forceinline__ uint32_t row_min(uint32_t v)
     v = min(v, uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x140, 0xf, 0xf, false))); // row_mirror
     return v;
 }
-// OR over the whole wave
-__device__ __forceinline__ uint32_t row_or_wave(uint32_t v)
-{
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v |= uint32_t(__shfl_xor(int(v), off));
-    return v;
-}
 __device__ __forceinline__ int row_max_i(int v)
 {
     v = max(v, __builtin_amdgcn_update_dpp(0, v, 0xb1, 0xf, 0xf, false));
@@ -114,12 +107,15 @@ __device__ __forceinline__ int row_max_i(int v)
 
 // LDS of one wave, laid out for the largest stage count so that every
 // offset is a constant: node words (flow | capacity << 8 | compute cost <<
-// 16), per exit the mask of its links with flow, per link its flow, and per
-// exit its row of link costs (cost << 5).
+// 16), per exit the mask of its links with flow (16 bits, two exits per
+// word), per vertex its predecessor code and that arc's residual for the
+// path walk, per link its flow, and per exit its row of link costs (cost <<
+// 5).
 template <int MAXS> struct SmallLayout {
     static constexpr size_t node = 0;
-    static constexpr size_t mask = node + 4 * MAXS * 64;
-    static constexpr size_t lflow = mask + 4 * MAXS * 64;
+    static constexpr size_t mask = node + 4 * MAXS * 64;     // 16 bits per exit
+    static constexpr size_t walk = mask + 2 * MAXS * 64;     // per vertex: pred code | residual << 5
+    static constexpr size_t lflow = walk + 2 * 2 * MAXS * 64;
     static constexpr size_t lcost = lflow + size_t(MAXS - 1) * kRows * 256;
     static constexpr size_t total = lcost + 2 * size_t(MAXS - 1) * kRows * 256;
 };
@@ -135,7 +131,8 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
     extern __shared__ __align__(16) unsigned char smem[];
     using Ly = SmallLayout<MAXS>;
     uint32_t *nodew = reinterpret_cast<uint32_t *>(smem + Ly::node);  // [S][64]
-    uint32_t *lmask = reinterpret_cast<uint32_t *>(smem + Ly::mask);  // [S][64]: exit's links with flow
+    uint32_t *lmask = reinterpret_cast<uint32_t *>(smem + Ly::mask);  // [S][32]: two exits' links with flow
+    uint16_t *wstage = reinterpret_cast<uint16_t *>(smem + Ly::walk); // [S][2][64]: entry, exit
     uint8_t *lflow = smem + Ly::lflow;                                // [S-1][4][16][16]: (k, i) -> (k+1, j)
     uint16_t *lcost = reinterpret_cast<uint16_t *>(smem + Ly::lcost); // [S-1][4][16][16]
     auto lidx = [&](int k, int i, int jj) { return ((k * kRows + g) * 16 + i) * 16 + jj; };
@@ -160,7 +157,7 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
         mx = max(mx, w);
         const int ec = min(max(cp, 0), max(supply, 0));
         nodew[k * 64 + lane] = uint32_t(min(ec, kMaxSupply)) << 8 | uint32_t(min(max(w, 0), kMaxCost)) << 16;
-        lmask[k * 64 + lane] = 0;
+        if ((lane & 1) == 0) lmask[k * 32 + (lane >> 1)] = 0;
     }
     // link costs: each row's n x n block of a stage pair, read with
     // consecutive lanes on consecutive elements, into the row-major LDS copy
@@ -191,8 +188,6 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
     int snkc = node && p.snk ? p.snk[size_t(b) * n + j] : 0;
     bad |= (srcc < 0) | (snkc < 0);
     mx = max(mx, max(srcc, snkc));
-    if (inst)
-        for (int q = j; q < V; q += 16) gpot[q] = 0;
     bad = row_max_i(bad);
     mx = row_max_i(mx);
     int status = 0;
@@ -209,6 +204,9 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
     bool active = mine && status == 0 && supply > 0; // this row still searches
     uint64_t tick = wall_clock64(), clk_fwd = 0, clk_bwd = 0, clk_aug = 0, clk_other = 0;
     uint32_t din[MAXS], dout[MAXS];
+    int pin[MAXS], pout[MAXS]; // potentials of this lane's entries and exits
+#pragma unroll
+    for (int k = 0; k < MAXS; ++k) pin[k] = pout[k] = 0;
     while (__any(active)) {
         // labels of a fresh search
 #pragma unroll
@@ -219,6 +217,10 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
         clk_other += lap(tick);
         int round_count = 0;
         bool fault = false;
+        // Stages whose exit (entry) keys changed in some lane since the next
+        // (previous) stage last read them: a relaxation or a pull whose input
+        // is unchanged cannot improve anything and is skipped.
+        uint32_t new_out = ~0u, new_in = ~0u;
         for (;;) {
             // -------- forward sweep --------
 #pragma unroll
@@ -227,11 +229,13 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
                 const uint32_t nw = nodew[k * 64 + lane];
                 const uint32_t fl = nw & 255u, ec = (nw >> 8) & 255u, nc5 = ((nw >> 16) & 2047u) << 5;
                 uint32_t di = din[k], dq = dout[k];
-                if (k >= 1) {
+                if (k >= 1 && ((new_out >> (k - 1)) & 1u)) {
+                    new_out &= ~(1u << (k - 1));
                     const uint32_t xr = (dout[k - 1] & ~31u) | uint32_t(j);
                     uint32_t best = kKeyInf;
                     Relax<0>::run(xr, cin[k], best);
                     di = best < lim(di) ? best : di;
+                    ++rows_relaxed;
                 }
                 if (fl > 0) {
                     const uint32_t cand = ((dq & ~31u) - nc5) | kCodeSplit;
@@ -241,10 +245,11 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
                     const uint32_t cand = ((di & ~31u) + nc5) | kCodeSplit;
                     dq = cand < lim(dq) ? cand : dq;
                 }
+                if (__any(di != din[k])) new_in |= 1u << k;
+                if (__any(dq != dout[k])) new_out |= 1u << k;
                 din[k] = di;
                 dout[k] = dq;
             }
-            rows_relaxed += S - 1;
             clk_fwd += lap(tick);
             // -------- backward sweep --------
             bool chg = false;
@@ -258,8 +263,11 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
                 // links with flow out of this exit, read here each time (values
                 // derived from it must not be kept live across the rounds)
                 const uint32_t lm =
-                    k + 1 < S ? __hip_atomic_load(&lmask[k * 64 + lane], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) : 0u;
-                if (k + 1 < S && __any(lm != 0u)) {
+                    k + 1 < S ? (__hip_atomic_load(&lmask[k * 32 + (lane >> 1)], __ATOMIC_RELAXED,
+                                                   __HIP_MEMORY_SCOPE_WORKGROUP) >> (16 * (lane & 1))) & 0xffffu
+                              : 0u;
+                if (k + 1 < S && ((new_in >> (k + 1)) & 1u) && __any(lm != 0u)) {
+                    new_in &= ~(1u << (k + 1));
                     // this exit's row of link costs
                     uint32_t cr[8];
                     const uint32_t *row = reinterpret_cast<const uint32_t *>(&lcost[lidx(k, j, 0)]);
@@ -276,6 +284,8 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
                     di = cand < lim(di) ? cand : di;
                 }
                 chg |= (di != din[k]) | (dq != dout[k]);
+                if (__any(di != din[k])) new_in |= 1u << k;
+                if (__any(dq != dout[k])) new_out |= 1u << k;
                 din[k] = di;
                 dout[k] = dq;
             }
@@ -307,93 +317,128 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
             const int dred = Dt - pit;
 #pragma unroll
             for (int k = 0; k < MAXS; ++k) {
-                if (k >= S) break;
-                const int q = k * n + j;
                 const int li = din[k] < kFiniteLimit ? int(din[k] >> 5) : INT32_MAX;
                 const int lo = dout[k] < kFiniteLimit ? int(dout[k] >> 5) : INT32_MAX;
-                gpot[3 + 2 * q] = min(li, gpot[3 + 2 * q] + dred);
-                gpot[4 + 2 * q] = min(lo, gpot[4 + 2 * q] + dred);
+                pin[k] = min(li, pin[k] + dred);
+                pout[k] = min(lo, pout[k] + dred);
             }
         }
 
         // -------- path: bottleneck, then apply (each row its own) --------
-        // Keys of vertex (k, v): the lane v of this row, stage k, selected by
-        // value since k differs between rows.
-        auto key_at = [&](int k, int v, bool exit) {
-            uint32_t x = kKeyInf;
+        // Each vertex's predecessor code and the residual of that arc (255 =
+        // unbounded or above the supply bound) go to LDS; one lane of the row
+        // then needs a single read per step.
+        if (__any(aug)) {
 #pragma unroll
-            for (int kk = 0; kk < MAXS; ++kk)
-                if (kk == k) x = exit ? dout[kk] : din[kk];
-            return uint32_t(__shfl(int(x), (g << 4) | v));
-        };
+            for (int k = 0; k < MAXS; ++k) {
+                if (k >= S) break;
+                const uint32_t nw = nodew[k * 64 + lane];
+                const uint32_t fl = nw & 255u, ec = (nw >> 8) & 255u;
+                const uint32_t ci = din[k] & 31u, co = dout[k] & 31u;
+                const uint32_t ri = ci == kCodeSplit ? fl : 255u;
+                uint32_t ro = 255u;
+                if (co == kCodeSplit) ro = ec - fl;
+                else if (co < 16 && k + 1 < S) ro = lflow[lidx(k, j, int(co))];
+                wstage[(2 * k) * 64 + lane] = uint16_t(ci | ri << 5);
+                wstage[(2 * k + 1) * 64 + lane] = uint16_t(co | ro << 5);
+            }
+        }
+        // The walk takes the bottleneck and records each arc (type | stage <<
+        // 2 | node << 6 | other << 10) in lane step % 16 of the row: slot 0
+        // takes the current block of 16 steps and the slots shift up after
+        // each block.  Then all recorded arcs are applied at once.  A simple
+        // path touches each node word and link byte once; the link masks of
+        // an exit are updated atomically.
+        constexpr int kSlots = (2 * MAXS * 16 + 5 + 15) / 16;
+        constexpr uint32_t kNoArcRec = ~0u;
+        uint32_t rec[kSlots];
+#pragma unroll
+        for (int r = 0; r < kSlots; ++r) rec[r] = kNoArcRec;
         int delta = aug ? supply - int(F) : 0;
         bool bad_walk = false;
-        for (int pass = 0; pass < 2; ++pass) {
+        {
             int k = S - 1, v = predt;
             bool at_exit = true, walking = aug && delta > 0;
             for (int steps = 0; __any(walking); ++steps) {
-                // every lane takes part in the cross-lane reads
-                const uint32_t key = key_at(k, v, at_exit);
-                if (!walking) continue;
-                if (steps > 2 * S * 16 + 4) {
-                    bad_walk = true;
-                    walking = false;
-                    continue;
+                if (walking) {
+                    if (steps > 2 * S * 16 + 4) {
+                        bad_walk = true;
+                        walking = false;
+                    }
                 }
-                const uint32_t code = key & 31u;
-                if (at_exit) {
-                    if (code == kCodeSplit) {
-                        const int at = k * 64 + (g << 4) + v;
-                        const uint32_t nw = nodew[at];
-                        if (pass == 0) delta = min(delta, int((nw >> 8) & 255u) - int(nw & 255u));
-                        else if (j == 0) nodew[at] = nw + uint32_t(delta);
-                        at_exit = false;
-                    } else if (code < 16 && k + 1 < S) {
-                        const int e = lidx(k, v, int(code));
-                        const int f = lflow[e];
-                        if (pass == 0) delta = min(delta, f);
-                        else if (j == 0) {
-                            lflow[e] = uint8_t(f - delta);
-                            if (f - delta == 0) lmask[k * 64 + (g << 4) + v] &= ~(1u << code);
+                uint32_t arc = ~0u; // type: 0 compute, 1 reverse compute, 2 link, 3 reverse link
+                if (walking) {
+                    const uint32_t w = wstage[(2 * k + (at_exit ? 1 : 0)) * 64 + (g << 4) + v];
+                    const uint32_t code = w & 31u;
+                    delta = min(delta, int(w >> 5));
+                    if (at_exit) {
+                        if (code == kCodeSplit) {
+                            arc = 0u | uint32_t(k) << 2 | uint32_t(v) << 6;
+                            at_exit = false;
+                        } else if (code < 16 && k + 1 < S) {
+                            arc = 3u | uint32_t(k) << 2 | uint32_t(v) << 6 | code << 10;
+                            k = k + 1;
+                            v = int(code);
+                            at_exit = false;
+                        } else {
+                            bad_walk = true;
+                            walking = false;
                         }
-                        k = k + 1;
-                        v = int(code);
-                        at_exit = false;
                     } else {
-                        bad_walk = true;
-                        walking = false;
-                    }
-                } else {
-                    if (code == kCodeSrc && k == 0) {
-                        walking = false;
-                    } else if (code == kCodeSplit) {
-                        const int at = k * 64 + (g << 4) + v;
-                        const uint32_t nw = nodew[at];
-                        if (pass == 0) delta = min(delta, int(nw & 255u));
-                        else if (j == 0) nodew[at] = nw - uint32_t(delta);
-                        at_exit = true;
-                    } else if (code < 16 && k >= 1) {
-                        if (pass == 1 && j == 0) {
-                            const int e = lidx(k - 1, int(code), v);
-                            const int f = lflow[e] + delta;
-                            lflow[e] = uint8_t(f);
-                            lmask[(k - 1) * 64 + (g << 4) + int(code)] |= 1u << v;
+                        if (code == kCodeSrc && k == 0) {
+                            walking = false;
+                        } else if (code == kCodeSplit) {
+                            arc = 1u | uint32_t(k) << 2 | uint32_t(v) << 6;
+                            at_exit = true;
+                        } else if (code < 16 && k >= 1) {
+                            // link (k-1, code) -> (k, v): unbounded
+                            arc = 2u | uint32_t(k - 1) << 2 | code << 6 | uint32_t(v) << 10;
+                            k = k - 1;
+                            v = int(code);
+                            at_exit = true;
+                        } else {
+                            bad_walk = true;
+                            walking = false;
                         }
-                        k = k - 1;
-                        v = int(code);
-                        at_exit = true;
-                    } else {
-                        bad_walk = true;
-                        walking = false;
                     }
+                }
+                if (arc != ~0u && j == (steps & 15)) rec[0] = arc;
+                if ((steps & 15) == 15) { // steps is the same in every lane
+#pragma unroll
+                    for (int r = kSlots - 1; r > 0; --r) rec[r] = rec[r - 1];
+                    rec[0] = kNoArcRec;
                 }
             }
-            if (pass == 0 && aug && !bad_walk && delta <= 0) bad_walk = true;
-            if (__any(bad_walk)) {
-                // a fault in any row: those rows stop with an internal status
-                if (bad_walk && active) status = kStatusInternal;
-                if (bad_walk) active = false;
-                if (pass == 0) delta = bad_walk ? 0 : delta;
+        }
+        if (aug && !bad_walk && delta <= 0) bad_walk = true;
+        if (bad_walk && active) status = kStatusInternal;
+        if (bad_walk) active = false;
+        {
+            const bool apply = aug && !bad_walk;
+            // the shifts run for the whole wave, so a row's blocks may sit in
+            // any slot: every slot holding an arc is applied
+#pragma unroll
+            for (int r = 0; r < kSlots; ++r) {
+                const uint32_t arc = rec[r];
+                if (!apply || arc == kNoArcRec) continue;
+                const int type = int(arc & 3u), k = int((arc >> 2) & 15u), a = int((arc >> 6) & 15u),
+                          c = int((arc >> 10) & 15u);
+                if (type == 0) {
+                    atomicAdd(&nodew[k * 64 + (g << 4) + a], uint32_t(delta));
+                } else if (type == 1) {
+                    atomicSub(&nodew[k * 64 + (g << 4) + a], uint32_t(delta));
+                } else if (type == 2) {
+                    const int e = lidx(k, a, c);
+                    lflow[e] = uint8_t(lflow[e] + delta);
+                    const int x = (g << 4) + a;
+                    atomicOr(&lmask[k * 32 + (x >> 1)], 1u << (c + 16 * (x & 1)));
+                } else {
+                    const int e = lidx(k, a, c);
+                    const int left = lflow[e] - delta;
+                    lflow[e] = uint8_t(left);
+                    const int x = (g << 4) + a;
+                    if (left == 0) atomicAnd(&lmask[k * 32 + (x >> 1)], ~(1u << (c + 16 * (x & 1))));
+                }
             }
         }
         if (aug && !bad_walk) {
@@ -418,10 +463,8 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
             if (k >= S) break;
             const int q = k * n + j;
             nf[q] = ok ? int(nodew[k * 64 + lane] & 255u) : 0;
-            if (!ok) {
-                gpot[3 + 2 * q] = 0;
-                gpot[4 + 2 * q] = 0;
-            }
+            gpot[3 + 2 * q] = ok ? pin[k] : 0;
+            gpot[4 + 2 * q] = ok ? pout[k] : 0;
             if (k + 1 < S)
                 for (int i = 0; i < n; ++i) af[size_t(k) * n * n + size_t(i) * n + j] = ok ? lflow[lidx(k, i, j)] : 0;
         }
@@ -436,7 +479,7 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
         int64_t *s = p.stats + size_t(b) * kStatsPerInstance;
         s[0] = augs;
         s[1] = rounds;
-        s[2] = rows_relaxed * n;
+        s[2] = rows_relaxed * n; // relaxed stage blocks x n rows of n links
         s[3] = pulls;
         const double ns_per_tick = 1e6 / double(p.clock_khz > 0 ? p.clock_khz : 100000);
         s[4] = int64_t(double(clk_fwd) * ns_per_tick);
