@@ -9,7 +9,7 @@ namespace gwtf {
 
 constexpr int kSmallMaxStages = 8;
 bool small_pass_fits(int S, int n);
-size_t small_pass_lds_bytes(int S);
+size_t small_pass_lds_bytes(int S, int n);
 hipError_t launch_small_pass(const SolveParams &p, hipStream_t s);
 
 } // namespace gwtf

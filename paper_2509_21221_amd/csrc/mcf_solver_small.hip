@@ -23,8 +23,9 @@
 //    fused into the adds, so a dense 16 x 16 relaxation is 16 broadcast-adds
 //    and 8 three-way minima per stage.
 //  * Reverse links (links carrying flow) are pulled at the exit's lane from
-//    the next stage's entry keys, over the exit's row of link costs (a copy
-//    in LDS) and a 16-bit mask of the links with flow.
+//    the next stage's entry keys, one partner per pass over the set bits of
+//    the exit's 16-bit mask of links with flow (cross-lane read of the
+//    partner's key, link cost from the exit's row of costs in LDS).
 //  * Rounds: a forward sweep over the stages, then a backward sweep, until
 //    a backward sweep changes nothing in any of the wave's instances.
 //  * After each search: potentials (device workspace), then each row walks
@@ -70,23 +71,6 @@ template <> struct Relax<16> {
     static __device__ __forceinline__ void run(uint32_t, const uint32_t (&)[16], uint32_t &) {}
 };
 
-// min over the 16 entries j of the next stage with flow on (this lane -> j):
-// (key of entry j with code j) - cost(this lane -> j)
-template <int J> struct Pull {
-    static __device__ __forceinline__ void run(uint32_t yr, const uint32_t (&c)[8], uint32_t nomask, uint32_t &best)
-    {
-        const uint32_t w = c[J >> 1];
-        const uint32_t c5 = (J & 1) ? (w >> 16) : (w & 0xffffu);
-        // no flow on this link: force the candidate out of the finite range
-        const uint32_t off = uint32_t(int32_t(nomask << (31 - J)) >> 31) & 0xc0000000u;
-        best = min(best, (row_bcast<J>(yr) - c5) | off);
-        Pull<J + 1>::run(yr, c, nomask, best);
-    }
-};
-template <> struct Pull<16> {
-    static __device__ __forceinline__ void run(uint32_t, const uint32_t (&)[8], uint32_t, uint32_t &) {}
-};
-
 // min over the 16 lanes of a row, in every lane of the row
 __device__ __forceinline__ uint32_t row_min(uint32_t v)
 {
@@ -105,19 +89,19 @@ __device__ __forceinline__ int row_max_i(int v)
     return v;
 }
 
-// LDS of one wave, laid out for the largest stage count so that every
-// offset is a constant: node words (flow | capacity << 8 | compute cost <<
-// 16), per exit the mask of its links with flow (16 bits, two exits per
-// word), per vertex its predecessor code and that arc's residual for the
-// path walk, per link its flow, and per exit its row of link costs (cost <<
-// 5).
+// LDS of one wave: node words (flow | capacity << 8 | compute cost << 16),
+// per exit the mask of its links with flow (16 bits, two exits per word),
+// per vertex its predecessor code and that arc's residual for the path walk
+// (all laid out for the largest stage count, so their offsets are
+// constants), then per link its flow and per exit its row of link costs
+// (cost << 5), n x n per stage pair and row.
 template <int MAXS> struct SmallLayout {
     static constexpr size_t node = 0;
     static constexpr size_t mask = node + 4 * MAXS * 64;     // 16 bits per exit
     static constexpr size_t walk = mask + 2 * MAXS * 64;     // per vertex: pred code | residual << 5
     static constexpr size_t lflow = walk + 2 * 2 * MAXS * 64;
-    static constexpr size_t lcost = lflow + size_t(MAXS - 1) * kRows * 256;
-    static constexpr size_t total = lcost + 2 * size_t(MAXS - 1) * kRows * 256;
+    static __host__ __device__ size_t lcost(int n) { return lflow + align16(size_t(MAXS - 1) * kRows * n * n); }
+    static __host__ __device__ size_t total(int n) { return lcost(n) + align16(2 * size_t(MAXS - 1) * kRows * n * n); }
 };
 
 template <int MAXS>
@@ -133,9 +117,9 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
     uint32_t *nodew = reinterpret_cast<uint32_t *>(smem + Ly::node);  // [S][64]
     uint32_t *lmask = reinterpret_cast<uint32_t *>(smem + Ly::mask);  // [S][32]: two exits' links with flow
     uint16_t *wstage = reinterpret_cast<uint16_t *>(smem + Ly::walk); // [S][2][64]: entry, exit
-    uint8_t *lflow = smem + Ly::lflow;                                // [S-1][4][16][16]: (k, i) -> (k+1, j)
-    uint16_t *lcost = reinterpret_cast<uint16_t *>(smem + Ly::lcost); // [S-1][4][16][16]
-    auto lidx = [&](int k, int i, int jj) { return ((k * kRows + g) * 16 + i) * 16 + jj; };
+    uint8_t *lflow = smem + Ly::lflow;                                   // [S-1][4][n][n]: (k, i) -> (k+1, j)
+    uint16_t *lcost = reinterpret_cast<uint16_t *>(smem + Ly::lcost(n)); // [S-1][4][n][n]
+    auto lidx = [&](int k, int i, int jj) { return ((k * kRows + g) * n + i) * n + jj; };
 
     const int supply = inst ? p.supply[b] : 0;
     const int32_t *gcap = p.cap + size_t(b) * SN;
@@ -162,10 +146,9 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
     // link costs: each row's n x n block of a stage pair, read with
     // consecutive lanes on consecutive elements, into the row-major LDS copy
     for (int k = 0; k + 1 < S; ++k) {
-        for (int e = j; e < 256; e += 16) {
-            const int i = e >> 4, jj = e & 15;
-            int a = 0;
-            if (inst && i < n && jj < n) a = gac[size_t(k) * n * n + size_t(i) * n + jj];
+        for (int e = j; e < n * n; e += 16) {
+            const int i = e / n, jj = e - i * n;
+            const int a = inst ? gac[size_t(k) * n * n + size_t(e)] : 0;
             bad |= a < -1;
             mx = max(mx, a);
             // a missing link never carries flow, so its LDS copy is never read
@@ -180,7 +163,9 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
         if (k >= S) break;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-            const uint32_t c5 = lcost[lidx(k - 1, r, j)];
+            // rows and columns beyond n are padding: cost 0, never improving
+            // anything since those exits stay unreached
+            const uint32_t c5 = (r < n && j < n) ? lcost[lidx(k - 1, r, j)] : 0u;
             cin[k][r] = c5 == 0xffffu ? kNoLink : c5;
         }
     }
@@ -268,14 +253,23 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
                               : 0u;
                 if (k + 1 < S && ((new_in >> (k + 1)) & 1u) && __any(lm != 0u)) {
                     new_in &= ~(1u << (k + 1));
-                    // this exit's row of link costs
-                    uint32_t cr[8];
-                    const uint32_t *row = reinterpret_cast<const uint32_t *>(&lcost[lidx(k, j, 0)]);
-#pragma unroll
-                    for (int r = 0; r < 8; ++r) cr[r] = __hip_atomic_load(row + r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+                    // one partner per pass: the lowest remaining link with flow
                     const uint32_t yr = (din[k + 1] & ~31u) | uint32_t(j);
                     uint32_t best = kKeyInf;
-                    Pull<0>::run(yr, cr, ~lm, best);
+                    uint32_t rem = lm;
+                    while (__any(rem != 0u)) {
+                        const bool have = rem != 0u;
+                        const int jj = have ? __builtin_ctz(rem) : 0;
+                        rem &= rem - 1u;
+                        const uint32_t yj = uint32_t(__shfl(int(yr), (g << 4) | jj));
+                        // only a real exit with a partner reads its cost (rows of
+                        // padding lanes lie outside the n x n block)
+                        if (have) {
+                            const uint32_t c5 =
+                                __hip_atomic_load(&lcost[lidx(k, j, jj)], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+                            best = min(best, yj - c5);
+                        }
+                    }
                     pulls += __popc(lm);
                     dq = best < lim(dq) ? best : dq;
                 }
@@ -338,7 +332,7 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
                 const uint32_t ri = ci == kCodeSplit ? fl : 255u;
                 uint32_t ro = 255u;
                 if (co == kCodeSplit) ro = ec - fl;
-                else if (co < 16 && k + 1 < S) ro = lflow[lidx(k, j, int(co))];
+                else if (co < 16 && k + 1 < S && j < n) ro = lflow[lidx(k, j, int(co))];
                 wstage[(2 * k) * 64 + lane] = uint16_t(ci | ri << 5);
                 wstage[(2 * k + 1) * 64 + lane] = uint16_t(co | ro << 5);
             }
@@ -356,10 +350,12 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
         for (int r = 0; r < kSlots; ++r) rec[r] = kNoArcRec;
         int delta = aug ? supply - int(F) : 0;
         bool bad_walk = false;
+        int wave_steps = 0; // iterations of the walk loop (the same in every lane)
         {
             int k = S - 1, v = predt;
             bool at_exit = true, walking = aug && delta > 0;
             for (int steps = 0; __any(walking); ++steps) {
+                wave_steps = steps + 1;
                 if (walking) {
                     if (steps > 2 * S * 16 + 4) {
                         bad_walk = true;
@@ -415,10 +411,13 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
         if (bad_walk) active = false;
         {
             const bool apply = aug && !bad_walk;
-            // the shifts run for the whole wave, so a row's blocks may sit in
-            // any slot: every slot holding an arc is applied
+            // the shifts run for the whole wave, after the record of steps
+            // 15, 31, ...: every row's arcs sit in the first
+            // floor(wave_steps / 16) + 1 slots
+            const int used = (wave_steps >> 4) + 1;
 #pragma unroll
             for (int r = 0; r < kSlots; ++r) {
+                if (r >= used) continue;
                 const uint32_t arc = rec[r];
                 if (!apply || arc == kNoArcRec) continue;
                 const int type = int(arc & 3u), k = int((arc >> 2) & 15u), a = int((arc >> 6) & 15u),
@@ -495,16 +494,17 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
 
 bool small_pass_fits(int S, int n) { return S >= 1 && S <= kSmallMaxStages && n <= 16; }
 
-size_t small_pass_lds_bytes(int S)
+size_t small_pass_lds_bytes(int S, int n)
 {
     (void)S;
-    return SmallLayout<kSmallMaxStages>::total;
+    return SmallLayout<kSmallMaxStages>::total(n);
 }
 
 hipError_t launch_small_pass(const SolveParams &p, hipStream_t s)
 {
     const unsigned blocks = unsigned((p.B + kRows - 1) / kRows);
-    hipLaunchKernelGGL((solve_small_kernel<kSmallMaxStages>), dim3(blocks), dim3(64), small_pass_lds_bytes(p.S), s, p);
+    hipLaunchKernelGGL((solve_small_kernel<kSmallMaxStages>), dim3(blocks), dim3(64), small_pass_lds_bytes(p.S, p.n), s,
+                       p);
     return hipGetLastError();
 }
 
