@@ -85,6 +85,17 @@ __device__ __forceinline__ uint64_t pack_key(int label, int idx)
 }
 __device__ __forceinline__ int key_label(uint64_t key) { return int(uint32_t(key >> 32)) - kBias; }
 
+__device__ __forceinline__ uint64_t wave_min_u64(uint64_t v)
+{
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        const uint32_t lo = __shfl_xor(uint32_t(v), off), hi = __shfl_xor(uint32_t(v >> 32), off);
+        const uint64_t o = (uint64_t(hi) << 32) | lo;
+        v = o < v ? o : v;
+    }
+    return v;
+}
+
 // Device-coherent accesses for data shared between workgroups.
 template <typename T> __device__ __forceinline__ T ld(const T *p)
 {
@@ -544,6 +555,7 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                 __syncthreads();
 
                 // compute arcs and reverse links of the owned nodes
+                uint64_t skey = ~0ull;
                 if (tid < nown) {
                     const int c = tid, q = k * n + j0 + c;
                     uint64_t kb = red[c];
@@ -590,7 +602,13 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                     st(&ex_out[q], (uint32_t(dq) << 2) | tag_f);
                     st(&en_out[q], (uint32_t(di) << 2) | tag_f);
                     if ((di != di0) | (dq != dq0)) sh_changed = 1;
-                    if (k == S - 1 && dq < kInf) atomicMin(&sh_key, (unsigned long long)pack_key(dq + snkc[c], j0 + c));
+                    if (k == S - 1 && dq < kInf) skey = pack_key(dq + snkc[c], j0 + c);
+                }
+                // the sink's best key: per wave first (the owner threads fill
+                // waves 0 and 1), then one LDS atomic per wave
+                if (k == S - 1 && tid < kGridNB) {
+                    skey = wave_min_u64(skey);
+                    if (lane == 0 && skey != ~0ull) atomicMin(&sh_key, (unsigned long long)skey);
                 }
                 __syncthreads();
                 // Count this workgroup into iteration t.  The last one in
