@@ -42,7 +42,6 @@ namespace {
 
 using namespace dev;
 
-constexpr int kRows = 4;                    // instances per wave
 constexpr uint32_t kKeyInf = 0x80000000u | 31u;
 constexpr uint32_t kFiniteLimit = 0x40000000u; // keys at or above are unreached
 constexpr uint32_t kNoLink = 0x40000000u;      // cost << 5 of a missing link
@@ -54,38 +53,51 @@ constexpr int64_t kSmallLabelLimit = (int64_t(1) << 25) - (int64_t(1) << 16);
 // The largest key a strictly better candidate must stay below.
 __device__ __forceinline__ uint32_t lim(uint32_t key) { return min(key & ~31u, kFiniteLimit); }
 
-template <int I> __device__ __forceinline__ uint32_t row_bcast(uint32_t x)
+// Lane I of this lane's group of G lanes: for G = 16 one DPP row broadcast;
+// for G = 8 the two halves of a row take lanes I and 8 + I through
+// bank-masked broadcasts.
+template <int G, int I> __device__ __forceinline__ uint32_t group_bcast(uint32_t x)
 {
-    return uint32_t(__builtin_amdgcn_update_dpp(0, int(x), 0x150 + I, 0xf, 0xf, false));
+    if constexpr (G == 16) {
+        return uint32_t(__builtin_amdgcn_update_dpp(0, int(x), 0x150 + I, 0xf, 0xf, false));
+    } else {
+        static_assert(G == 8, "groups of 8 or 16 lanes");
+        const int lo = __builtin_amdgcn_update_dpp(0, int(x), 0x150 + I, 0xf, 0x3, false);
+        return uint32_t(__builtin_amdgcn_update_dpp(lo, int(x), 0x158 + I, 0xf, 0xc, false));
+    }
 }
 
-// min over the 16 rows i of (key of exit i with code i) + cost(i -> this lane)
-template <int I> struct Relax {
-    static __device__ __forceinline__ void run(uint32_t xr, const uint32_t (&c)[16], uint32_t &best)
+// min over the G rows i of (key of exit i with code i) + cost(i -> this lane)
+template <int G, int I> struct Relax {
+    static __device__ __forceinline__ void run(uint32_t xr, const uint32_t (&c)[G], uint32_t &best)
     {
-        best = min(best, row_bcast<I>(xr) + c[I]);
-        Relax<I + 1>::run(xr, c, best);
+        best = min(best, group_bcast<G, I>(xr) + c[I]);
+        Relax<G, I + 1>::run(xr, c, best);
     }
 };
-template <> struct Relax<16> {
+template <> struct Relax<16, 16> {
     static __device__ __forceinline__ void run(uint32_t, const uint32_t (&)[16], uint32_t &) {}
 };
+template <> struct Relax<8, 8> {
+    static __device__ __forceinline__ void run(uint32_t, const uint32_t (&)[8], uint32_t &) {}
+};
 
-// min over the 16 lanes of a row, in every lane of the row
-__device__ __forceinline__ uint32_t row_min(uint32_t v)
+// min over the G lanes of a group, in every lane of the group
+template <int G> __device__ __forceinline__ uint32_t group_min(uint32_t v)
 {
     v = min(v, uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0xb1, 0xf, 0xf, false)));  // quad_perm [1,0,3,2]
     v = min(v, uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x4e, 0xf, 0xf, false)));  // quad_perm [2,3,0,1]
     v = min(v, uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x141, 0xf, 0xf, false))); // row_half_mirror
-    v = min(v, uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x140, 0xf, 0xf, false))); // row_mirror
+    if constexpr (G == 16)
+        v = min(v, uint32_t(__builtin_amdgcn_update_dpp(0, int(v), 0x140, 0xf, 0xf, false))); // row_mirror
     return v;
 }
-__device__ __forceinline__ int row_max_i(int v)
+template <int G> __device__ __forceinline__ int group_max(int v)
 {
     v = max(v, __builtin_amdgcn_update_dpp(0, v, 0xb1, 0xf, 0xf, false));
     v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x4e, 0xf, 0xf, false));
     v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x141, 0xf, 0xf, false));
-    v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x140, 0xf, 0xf, false));
+    if constexpr (G == 16) v = max(v, __builtin_amdgcn_update_dpp(0, v, 0x140, 0xf, 0xf, false));
     return v;
 }
 
@@ -95,25 +107,26 @@ __device__ __forceinline__ int row_max_i(int v)
 // (all laid out for the largest stage count, so their offsets are
 // constants), then per link its flow and per exit its row of link costs
 // (cost << 5), n x n per stage pair and row.
-template <int MAXS> struct SmallLayout {
+template <int MAXS, int ROWS> struct SmallLayout {
     static constexpr size_t node = 0;
     static constexpr size_t mask = node + 4 * MAXS * 64;     // 16 bits per exit
     static constexpr size_t walk = mask + 2 * MAXS * 64;     // per vertex: pred code | residual << 5
     static constexpr size_t lflow = walk + 2 * 2 * MAXS * 64;
-    static __host__ __device__ size_t lcost(int n) { return lflow + align16(size_t(MAXS - 1) * kRows * n * n); }
-    static __host__ __device__ size_t total(int n) { return lcost(n) + align16(2 * size_t(MAXS - 1) * kRows * n * n); }
+    static __host__ __device__ size_t lcost(int n) { return lflow + align16(size_t(MAXS - 1) * ROWS * n * n); }
+    static __host__ __device__ size_t total(int n) { return lcost(n) + align16(2 * size_t(MAXS - 1) * ROWS * n * n); }
 };
 
-template <int MAXS>
+template <int MAXS, int G>
 __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
 {
+    constexpr int kRows = 64 / G; // instances per wave
     const int S = p.S, n = p.n, SN = S * n, V = 2 * SN + 3;
-    const int lane = threadIdx.x, g = lane >> 4, j = lane & 15;
+    const int lane = threadIdx.x, g = lane / G, j = lane % G, gb = g * G; // gb: first lane of the group
     const int b = blockIdx.x * kRows + g;
     const bool inst = b < p.B;      // this row holds an instance
     const bool node = inst && j < n; // this lane is a real node
     extern __shared__ __align__(16) unsigned char smem[];
-    using Ly = SmallLayout<MAXS>;
+    using Ly = SmallLayout<MAXS, kRows>;
     uint32_t *nodew = reinterpret_cast<uint32_t *>(smem + Ly::node);  // [S][64]
     uint32_t *lmask = reinterpret_cast<uint32_t *>(smem + Ly::mask);  // [S][32]: two exits' links with flow
     uint16_t *wstage = reinterpret_cast<uint16_t *>(smem + Ly::walk); // [S][2][64]: entry, exit
@@ -129,11 +142,11 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
 
     // ---------------- ingest + validate ----------------
     int bad = supply < 0, mx = 0;
-    uint32_t cin[MAXS][16]; // [k][i]: cost << 5 of link (k-1, i) -> (k, j), k >= 1
+    uint32_t cin[MAXS][G]; // [k][i]: cost << 5 of link (k-1, i) -> (k, j), k >= 1
 #pragma unroll
     for (int k = 0; k < MAXS; ++k) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) cin[k][r] = 0;
+        for (int r = 0; r < G; ++r) cin[k][r] = 0;
         if (k >= S) continue;
         const int q = k * n + j;
         const int cp = node ? gcap[q] : 0, w = node ? gnc[q] : 0;
@@ -146,7 +159,7 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
     // link costs: each row's n x n block of a stage pair, read with
     // consecutive lanes on consecutive elements, into the row-major LDS copy
     for (int k = 0; k + 1 < S; ++k) {
-        for (int e = j; e < n * n; e += 16) {
+        for (int e = j; e < n * n; e += G) {
             const int i = e / n, jj = e - i * n;
             const int a = inst ? gac[size_t(k) * n * n + size_t(e)] : 0;
             bad |= a < -1;
@@ -162,7 +175,7 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
     for (int k = 1; k < MAXS; ++k) {
         if (k >= S) break;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
+        for (int r = 0; r < G; ++r) {
             // rows and columns beyond n are padding: cost 0, never improving
             // anything since those exits stay unreached
             const uint32_t c5 = (r < n && j < n) ? lcost[lidx(k - 1, r, j)] : 0u;
@@ -173,8 +186,8 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
     int snkc = node && p.snk ? p.snk[size_t(b) * n + j] : 0;
     bad |= (srcc < 0) | (snkc < 0);
     mx = max(mx, max(srcc, snkc));
-    bad = row_max_i(bad);
-    mx = row_max_i(mx);
+    bad = group_max<G>(bad);
+    mx = group_max<G>(mx);
     int status = 0;
     if (bad) status = 1;
     else if (int64_t(V) * mx >= kLabelBound) status = 2;
@@ -218,7 +231,7 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
                     new_out &= ~(1u << (k - 1));
                     const uint32_t xr = (dout[k - 1] & ~31u) | uint32_t(j);
                     uint32_t best = kKeyInf;
-                    Relax<0>::run(xr, cin[k], best);
+                    Relax<G, 0>::run(xr, cin[k], best);
                     di = best < lim(di) ? best : di;
                     ++rows_relaxed;
                 }
@@ -261,7 +274,7 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
                         const bool have = rem != 0u;
                         const int jj = have ? __builtin_ctz(rem) : 0;
                         rem &= rem - 1u;
-                        const uint32_t yj = uint32_t(__shfl(int(yr), (g << 4) | jj));
+                        const uint32_t yj = uint32_t(__shfl(int(yr), gb + jj));
                         // only a real exit with a partner reads its cost (rows of
                         // padding lanes lie outside the n x n block)
                         if (have) {
@@ -303,7 +316,7 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
 #pragma unroll
         for (int k = 0; k < MAXS; ++k)
             if (k == S - 1 && j < n) tk = ((dout[k] & ~31u) + snk5) | uint32_t(j);
-        tk = row_min(tk);
+        tk = group_min<G>(tk);
         const bool aug = active && tk < kFiniteLimit;
         if (active && !aug) active = false; // sink unreachable: the flow is maximum
         const int Dt = int(tk >> 5), predt = int(tk & 31u);
@@ -343,7 +356,7 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
         // each block.  Then all recorded arcs are applied at once.  A simple
         // path touches each node word and link byte once; the link masks of
         // an exit are updated atomically.
-        constexpr int kSlots = (2 * MAXS * 16 + 5 + 15) / 16;
+        constexpr int kSlots = (2 * MAXS * G + 5 + G - 1) / G;
         constexpr uint32_t kNoArcRec = ~0u;
         uint32_t rec[kSlots];
 #pragma unroll
@@ -357,14 +370,14 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
             for (int steps = 0; __any(walking); ++steps) {
                 wave_steps = steps + 1;
                 if (walking) {
-                    if (steps > 2 * S * 16 + 4) {
+                    if (steps > 2 * S * G + 4) {
                         bad_walk = true;
                         walking = false;
                     }
                 }
                 uint32_t arc = ~0u; // type: 0 compute, 1 reverse compute, 2 link, 3 reverse link
                 if (walking) {
-                    const uint32_t w = wstage[(2 * k + (at_exit ? 1 : 0)) * 64 + (g << 4) + v];
+                    const uint32_t w = wstage[(2 * k + (at_exit ? 1 : 0)) * 64 + gb + v];
                     const uint32_t code = w & 31u;
                     delta = min(delta, int(w >> 5));
                     if (at_exit) {
@@ -398,8 +411,8 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
                         }
                     }
                 }
-                if (arc != ~0u && j == (steps & 15)) rec[0] = arc;
-                if ((steps & 15) == 15) { // steps is the same in every lane
+                if (arc != ~0u && j == steps % G) rec[0] = arc;
+                if (steps % G == G - 1) { // steps is the same in every lane
 #pragma unroll
                     for (int r = kSlots - 1; r > 0; --r) rec[r] = rec[r - 1];
                     rec[0] = kNoArcRec;
@@ -412,9 +425,9 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
         {
             const bool apply = aug && !bad_walk;
             // the shifts run for the whole wave, after the record of steps
-            // 15, 31, ...: every row's arcs sit in the first
-            // floor(wave_steps / 16) + 1 slots
-            const int used = (wave_steps >> 4) + 1;
+            // G - 1, 2G - 1, ...: every row's arcs sit in the first
+            // floor(wave_steps / G) + 1 slots
+            const int used = wave_steps / G + 1;
 #pragma unroll
             for (int r = 0; r < kSlots; ++r) {
                 if (r >= used) continue;
@@ -423,19 +436,19 @@ __global__ __launch_bounds__(64, 2) void solve_small_kernel(SolveParams p)
                 const int type = int(arc & 3u), k = int((arc >> 2) & 15u), a = int((arc >> 6) & 15u),
                           c = int((arc >> 10) & 15u);
                 if (type == 0) {
-                    atomicAdd(&nodew[k * 64 + (g << 4) + a], uint32_t(delta));
+                    atomicAdd(&nodew[k * 64 + gb + a], uint32_t(delta));
                 } else if (type == 1) {
-                    atomicSub(&nodew[k * 64 + (g << 4) + a], uint32_t(delta));
+                    atomicSub(&nodew[k * 64 + gb + a], uint32_t(delta));
                 } else if (type == 2) {
                     const int e = lidx(k, a, c);
                     lflow[e] = uint8_t(lflow[e] + delta);
-                    const int x = (g << 4) + a;
+                    const int x = gb + a;
                     atomicOr(&lmask[k * 32 + (x >> 1)], 1u << (c + 16 * (x & 1)));
                 } else {
                     const int e = lidx(k, a, c);
                     const int left = lflow[e] - delta;
                     lflow[e] = uint8_t(left);
-                    const int x = (g << 4) + a;
+                    const int x = gb + a;
                     if (left == 0) atomicAnd(&lmask[k * 32 + (x >> 1)], ~(1u << (c + 16 * (x & 1))));
                 }
             }
@@ -497,14 +510,20 @@ bool small_pass_fits(int S, int n) { return S >= 1 && S <= kSmallMaxStages && n 
 size_t small_pass_lds_bytes(int S, int n)
 {
     (void)S;
-    return SmallLayout<kSmallMaxStages>::total(n);
+    return n <= 8 ? SmallLayout<kSmallMaxStages, 8>::total(n) : SmallLayout<kSmallMaxStages, 4>::total(n);
 }
 
 hipError_t launch_small_pass(const SolveParams &p, hipStream_t s)
 {
-    const unsigned blocks = unsigned((p.B + kRows - 1) / kRows);
-    hipLaunchKernelGGL((solve_small_kernel<kSmallMaxStages>), dim3(blocks), dim3(64), small_pass_lds_bytes(p.S, p.n), s,
-                       p);
+    if (p.n <= 8) {
+        const unsigned blocks = unsigned((p.B + 7) / 8);
+        hipLaunchKernelGGL((solve_small_kernel<kSmallMaxStages, 8>), dim3(blocks), dim3(64),
+                           small_pass_lds_bytes(p.S, p.n), s, p);
+    } else {
+        const unsigned blocks = unsigned((p.B + 3) / 4);
+        hipLaunchKernelGGL((solve_small_kernel<kSmallMaxStages, 16>), dim3(blocks), dim3(64),
+                           small_pass_lds_bytes(p.S, p.n), s, p);
+    }
     return hipGetLastError();
 }
 

@@ -163,11 +163,12 @@ def test_grid_pass_routing_and_status():
 @pytest.mark.parametrize("S,n,B,holes,zero", [
     (1, 1, 5, 0.0, 0.0), (2, 16, 7, 0.2, 0.1), (8, 16, 33, 0.1, 0.1), (8, 13, 64, 0.0, 0.0),
     (5, 9, 10, 0.3, 0.2), (3, 4, 1, 0.0, 0.0), (7, 11, 6, 0.0, 0.3),
+    (8, 8, 37, 0.2, 0.1), (6, 7, 9, 0.0, 0.2), (4, 2, 13, 0.3, 0.0), (8, 5, 70, 0.1, 0.1),
 ])
 def test_packed_pass_shapes(S, n, B, holes, zero):
     """Shapes served by the packed pass (S <= 8, n <= 16): four instances per
-    wave, batches that leave a wave partly empty, missing links, deleted
-    nodes."""
+    wave (eight when n <= 8), batches that leave a wave partly empty, missing
+    links, deleted nodes."""
     batch = W.random_small(B, S, n, seed=31, cap_hi=9, cost_hi=400, supply_hi=4 * n + 8,
                            holes=holes, zero_cap=zero)
     say("packed", S, n, B)
