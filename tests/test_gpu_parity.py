@@ -200,6 +200,20 @@ def test_packed_pass_routing_and_status():
                   g["src_flow"][b], g["snk_flow"][b], g["potential"][b])
 
 
+def test_packed_pass_bounds():
+    """Supply 255 and a cost of 2047 are the largest the packed pass keeps
+    (flows in 8 bits, costs shifted by 5 in 16 bits); parity at the bounds."""
+    batch = W.random_small(12, 6, 10, seed=41, cap_hi=60, cost_hi=2047, supply_hi=255)
+    batch.supply[:] = 255
+    batch.node_cost[:, 0, 0] = 2047
+    batch.arc_cost[:, 2, 3, 4] = 2047
+    batch.src_cost[:, 1] = 2047
+    say("packed bounds")
+    g = gpu_solve(batch)
+    compare(batch, g, oracle.solve(batch))
+    assert (g["passes"] == mcf.GWTF_PASS_PACKED).all()
+
+
 def test_lists_outgrow_lds_use_fallback():
     """Capacities of 64 make every exit vertex reserve 64 flow-list slots,
     more than LDS holds at this shape, so the global-memory pass runs."""
