@@ -283,6 +283,20 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
     if (status == 0) {
         while (F < supply) {
             // ---- labels of a fresh search; mailboxes hold iteration 0 ----
+            // The flow lists change only between searches: each exit's list
+            // and the wave's longest list per stage are read once here.
+            int lst_lo[P], lst_len[P], lst_max[P];
+#pragma unroll
+            for (int s = 0; s < P; ++s) {
+                const int q = (k0 + s) * 64 + lane;
+                const bool own = k0 + s <= klast && k0 + s + 1 < S;
+                lst_lo[s] = own ? int(loff[q]) : 0;
+                lst_len[s] = own && jv ? int(llen[q]) : 0;
+                int m = lst_len[s];
+#pragma unroll
+                for (int off = 32; off > 0; off >>= 1) m = max(m, __shfl_xor(m, off));
+                lst_max[s] = __builtin_amdgcn_readfirstlane(m);
+            }
 #pragma unroll
             for (int s = 0; s < P; ++s) {
                 const int k = k0 + s;
@@ -395,11 +409,7 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
                         const bool ydr = Y < seeny[s];
                         seeny[s] = ydr ? Y : seeny[s];
                         if (k + 1 < S && __ballot(ydr) != 0) {
-                            const int lo = loff[q], len = jv ? llen[q] : 0;
-                            int maxlen = len;
-#pragma unroll
-                            for (int off = 32; off > 0; off >>= 1) maxlen = max(maxlen, __shfl_xor(maxlen, off));
-                            maxlen = __builtin_amdgcn_readfirstlane(maxlen);
+                            const int lo = lst_lo[s], len = lst_len[s], maxlen = lst_max[s];
                             for (int e = 0; e < maxlen; e += 4) {
                                 uint32_t ent[4];
 #pragma unroll
