@@ -17,6 +17,9 @@ constexpr int64_t kLabelBound = int64_t(1) << 29;
 // Route codes in the workspace: an instance waiting for the fallback pass,
 // or the pass that finished it (the public GWTF_PASS_* values).
 enum : int32_t { kRouteFallback = -1, kRouteReg = 1, kRouteLds = 2, kRouteGrid = 3, kRouteGlobal = 4, kRouteSmall = 5 };
+// between the two launches of the pipelined pass only: the unscaled variant
+// solves the instance
+constexpr int32_t kRoutePipeWide = 6;
 
 // Kernel arguments shared by both solver passes.
 struct SolveParams {

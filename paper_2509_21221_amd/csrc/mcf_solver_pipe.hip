@@ -45,6 +45,16 @@ constexpr int kRing = 32; // iterations in flight across the waves: fewer than t
 constexpr int kSpinLimit = 1 << 22;
 constexpr uint32_t kNoArc16 = 0xffff;
 constexpr int kBias = 1 << 30;
+// Keyed relaxation: a link candidate is the key label * 64 + row, so one
+// unsigned min keeps the smallest label and, among equal labels, the first
+// row.  Link costs are then stored times 64 (at most kKeyMaxCost), and an
+// unreached row broadcasts kKeyNone, which no real key reaches.
+constexpr int kKeyMaxCost = 1023;
+constexpr uint32_t kKeyNone = 0xffff0000u;
+__host__ __device__ constexpr bool keyed_fits(int64_t V, int64_t maxc)
+{
+    return maxc <= kKeyMaxCost && (V + 1) * maxc * 64 + 63 < int64_t(kKeyNone);
+}
 
 enum : int { kArcSplitFwd = 0, kArcSplitRev = 1, kArcLinkFwd = 2, kArcLinkRev = 3 };
 
@@ -129,11 +139,13 @@ __device__ __forceinline__ int mailbox_wait(const uint32_t *mb, uint32_t par, co
     }
 }
 
-template <int W, int P>
+template <int W, int P, bool kKeyed>
 __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
 {
     constexpr int NT = 64 * W;
     const int b = blockIdx.x;
+    // the unscaled variant runs after the keyed one, on the instances it passed on
+    if (!kKeyed && p.route[b] != kRoutePipeWide) return;
     const int S = p.S, n = p.n, SN = S * n, V = 2 * SN + 3;
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -199,8 +211,10 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
                     wide |= (a0 > 65534) | (a1 > 65534);
                     hole |= (jv & (2 * r < n) & (a0 < 0)) | (jv & (2 * r + 1 < n) & (a1 < 0));
                     mx = max(mx, max(a0, a1));
-                    const uint32_t c0 = a0 < 0 ? kNoArc16 : uint32_t(min(a0, 65535));
-                    const uint32_t c1 = a1 < 0 ? kNoArc16 : uint32_t(min(a1, 65535));
+                    // keyed: costs above kKeyMaxCost send the instance on, so
+                    // the clamp only keeps the stored word in range
+                    const uint32_t c0 = a0 < 0 ? kNoArc16 : kKeyed ? uint32_t(min(a0, kKeyMaxCost)) << 6 : uint32_t(min(a0, 65535));
+                    const uint32_t c1 = a1 < 0 ? kNoArc16 : kKeyed ? uint32_t(min(a1, kKeyMaxCost)) << 6 : uint32_t(min(a1, 65535));
                     v[r] = c0 | (c1 << 16);
                 }
             }
@@ -272,6 +286,12 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
         // 16-bit link costs or LDS lists do not fit: the fallback pass
         // solves this instance.
         if (tid == 0) p.route[b] = kRouteFallback;
+        return;
+    }
+    if (kKeyed && status == 0 && !keyed_fits(V, ps.maxc)) {
+        // costs above kKeyMaxCost or labels too long for the keys: the
+        // unscaled variant solves this instance
+        if (tid == 0) p.route[b] = kRoutePipeWide;
         return;
     }
 
@@ -359,22 +379,59 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
                             const uint64_t mask = __ballot(dr);
                             rows += __popcll(mask);
                             // rows that dropped, two per cost register, in row order
-                            if (mask) {
+                            if (mask && kKeyed) {
+                                // every row of a group with a dropped row: a row
+                                // that did not drop was relaxed with the same label
+                                // before, so its key cannot beat the current label
+                                const uint32_t xk = X < kInf ? (uint32_t(X) << 6) | uint32_t(lane) : kKeyNone;
+                                uint32_t key = kKeyNone;
                                 if (!((holes >> s) & 1u)) {
+                                    const uint32_t mlo = uint32_t(mask), mhi = uint32_t(mask >> 32);
 #pragma unroll
-                                    for (int r2 = 0; r2 < 32; ++r2) {
-                                        const uint32_t bits = uint32_t(mask >> (2 * r2)) & 3u;
-                                        if (bits) {
-                                            const uint32_t wd = lw[s][r2];
-                                            if (bits & 1u) {
-                                                const int cand = __builtin_amdgcn_readlane(X, 2 * r2) + int(wd & 0xffffu);
-                                                pi = cand < di ? 2 * r2 : pi;
-                                                di = min(di, cand);
+                                    for (int g = 0; g < 8; ++g) {
+                                        const uint32_t half = g < 4 ? mlo : mhi;
+                                        if (half & (0xffu << (8 * (g & 3)))) {
+#pragma unroll
+                                            for (int r = 8 * g; r < 8 * g + 8; r += 2) {
+                                                const uint32_t wd = lw[s][r >> 1];
+                                                const uint32_t a = __builtin_amdgcn_readlane(xk, r) + (wd & 0xffffu);
+                                                const uint32_t c = __builtin_amdgcn_readlane(xk, r + 1) + (wd >> 16);
+                                                key = min(key, min(a, c));
                                             }
-                                            if (bits & 2u) {
-                                                const int cand = __builtin_amdgcn_readlane(X, 2 * r2 + 1) + int(wd >> 16);
-                                                pi = cand < di ? 2 * r2 + 1 : pi;
-                                                di = min(di, cand);
+                                        }
+                                    }
+                                } else {
+                                    // some links are missing (cost 0xffff): skip them
+                                    uint64_t m = mask;
+                                    while (m) {
+                                        const int r = __builtin_ctzll(m);
+                                        m &= m - 1;
+                                        const uint32_t c = (lw[s][r >> 1] >> (16 * (r & 1))) & 0xffffu;
+                                        const uint32_t cand = __builtin_amdgcn_readlane(xk, r) + c;
+                                        key = c != kNoArc16 ? min(key, cand) : key;
+                                    }
+                                }
+                                if (key < kKeyNone && int(key >> 6) < di) {
+                                    di = int(key >> 6);
+                                    pi = int(key & 63u);
+                                }
+                            } else if (mask) {
+                                if (!((holes >> s) & 1u)) {
+                                    // one scalar test per group of 8 rows, then one
+                                    // bit test per row of a group that has any
+                                    const uint32_t mlo = uint32_t(mask), mhi = uint32_t(mask >> 32);
+#pragma unroll
+                                    for (int g = 0; g < 8; ++g) {
+                                        const uint32_t half = g < 4 ? mlo : mhi;
+                                        if (half & (0xffu << (8 * (g & 3)))) {
+#pragma unroll
+                                            for (int r = 8 * g; r < 8 * g + 8; ++r) {
+                                                if (half & (1u << (r & 31))) {
+                                                    const uint32_t wd = lw[s][r >> 1];
+                                                    const int cand = __builtin_amdgcn_readlane(X, r) + int((r & 1) ? wd >> 16 : wd & 0xffffu);
+                                                    pi = cand < di ? r : pi;
+                                                    di = min(di, cand);
+                                                }
                                             }
                                         }
                                     }
@@ -712,9 +769,17 @@ hipError_t launch_pipe_pass(const SolveParams &p, hipStream_t s)
     int W, P;
     pipe_shape(p.S, W, P);
     const size_t lds = pipe_layout(p.S, W, p.list_slots).total;
-    if (W == 8) hipLaunchKernelGGL((solve_pipe_kernel<8, 1>), dim3(p.B), dim3(512), lds, s, p);
-    else if (P == 1) hipLaunchKernelGGL((solve_pipe_kernel<16, 1>), dim3(p.B), dim3(1024), lds, s, p);
-    else hipLaunchKernelGGL((solve_pipe_kernel<16, 2>), dim3(p.B), dim3(1024), lds, s, p);
+    // keyed variant first; the unscaled one takes the instances it passed on
+    if (W == 8) {
+        hipLaunchKernelGGL((solve_pipe_kernel<8, 1, true>), dim3(p.B), dim3(512), lds, s, p);
+        hipLaunchKernelGGL((solve_pipe_kernel<8, 1, false>), dim3(p.B), dim3(512), lds, s, p);
+    } else if (P == 1) {
+        hipLaunchKernelGGL((solve_pipe_kernel<16, 1, true>), dim3(p.B), dim3(1024), lds, s, p);
+        hipLaunchKernelGGL((solve_pipe_kernel<16, 1, false>), dim3(p.B), dim3(1024), lds, s, p);
+    } else {
+        hipLaunchKernelGGL((solve_pipe_kernel<16, 2, true>), dim3(p.B), dim3(1024), lds, s, p);
+        hipLaunchKernelGGL((solve_pipe_kernel<16, 2, false>), dim3(p.B), dim3(1024), lds, s, p);
+    }
     return hipGetLastError();
 }
 

@@ -319,6 +319,37 @@ def test_register_pass_routes_wide_costs():
     compare(batch, g, oracle.solve(batch))
 
 
+@pytest.mark.parametrize("S,n,holes", [(3, 40, 0.0), (32, 64, 0.0), (9, 64, 0.2)])
+def test_register_pass_unscaled_costs(S, n, holes):
+    """Costs above 1023 do not fit the keyed relaxation (labels times 64 plus
+    the row in 32 bits, costs times 64 in 16): the unscaled variant of the
+    register pass solves these instances."""
+    batch = W.random_small(8, S, n, seed=43, cap_hi=6, cost_hi=6000, supply_hi=4 * n, holes=holes)
+    say("register pass unscaled", S, n)
+    g = gpu_solve(batch)
+    compare(batch, g, oracle.solve(batch))
+    assert (g["passes"] == mcf.GWTF_PASS_REGISTER).all()
+
+
+def test_register_pass_keyed_and_unscaled_in_one_batch():
+    """One batch split over both variants of the register pass and the
+    fallback: the keyed variant keeps instances whose costs are at most 1023
+    (a link, a compute and a data-node cost at exactly 1023 included)."""
+    batch = W.config4(8)
+    batch.arc_cost[1, 3, 5, 7] = 1023
+    batch.node_cost[1, 4, 9] = 1023
+    batch.snk_cost[1, 2] = 1023
+    batch.arc_cost[2, 0, 0, 1] = 1024   # link cost over the keyed limit
+    batch.node_cost[4, 31, 63] = 4000   # compute cost over it
+    batch.src_cost[5, 0] = 1500         # data-node cost over it
+    batch.arc_cost[6, 7, 2, 2] = 70000  # over 16 bits: the fallback pass
+    say("register pass keyed / unscaled / fallback")
+    g = gpu_solve(batch)
+    compare(batch, g, oracle.solve(batch))
+    assert (g["passes"][[0, 1, 2, 3, 4, 5, 7]] == mcf.GWTF_PASS_REGISTER).all()
+    assert g["passes"][6] != mcf.GWTF_PASS_REGISTER
+
+
 def test_config5_full_against_stored_oracle():
     """The single 64 x 512 instance: (F, cost) equal to the stored oracle
     optimum, the closed-form flow value, and the returned flow certified."""
