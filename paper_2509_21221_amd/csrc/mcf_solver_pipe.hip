@@ -19,9 +19,12 @@
 //    mailboxes whose words carry the iteration's parity, and the reader waits
 //    on the words themselves.  All waves run concurrently on different
 //    stages, without workgroup barriers.
-//  * Convergence is counted per iteration on a ring of LDS counters: the last
-//    wave to finish an iteration in which no label changed anywhere publishes
-//    the sink's key and a stop word.
+//  * Convergence travels with the labels: each exit-mailbox word of
+//    iteration t also carries whether any stage up to that wave's last one
+//    changed a label in iteration t, so the wave that owns the last stage
+//    learns it for the whole pipeline and, when nothing changed, publishes
+//    the sink's key and a stop word; the other waves leave on that word
+//    while they wait for a mailbox.
 //  * After convergence: potentials (kept in the device workspace), then lane
 //    0 of wave 0 walks the path over predecessors staged in LDS and takes the
 //    bottleneck from the LDS node flows and flow lists; every wave applies
@@ -41,7 +44,6 @@ namespace {
 
 using namespace dev;
 
-constexpr int kRing = 32; // iterations in flight across the waves: fewer than the waves
 constexpr int kSpinLimit = 1 << 22;
 constexpr uint32_t kNoArc16 = 0xffff;
 constexpr int kBias = 1 << 30;
@@ -107,8 +109,6 @@ __device__ __forceinline__ int pred_out(int pp) { return pp >> 16; }
 __device__ __forceinline__ int pred_pack(int pi, int po) { return (pi & 0xffff) | (po << 16); }
 
 struct PipeShared {
-    unsigned ring[kRing];
-    unsigned long long ring_key[kRing];
     unsigned long long final_key;
     int stop;  // iteration at which the search converged; 0 while it runs
     int fault; // a wait ran out, an iteration bound was exceeded, or a self-check failed
@@ -118,22 +118,22 @@ struct PipeShared {
     long long rows, pulls, steps;
 };
 
-// Waits until all 64 words of a mailbox carry parity `par`; returns this
-// lane's label.  Sets why to 1 if the search stopped meanwhile, 2 if the
+// Waits until all 64 words of a mailbox carry parity `par` in bit 0; returns
+// this lane's word.  Sets why to 1 if the search stopped meanwhile, 2 if the
 // wait ran out.
-__device__ __forceinline__ int mailbox_wait(const uint32_t *mb, uint32_t par, const int *stop, int &why)
+__device__ __forceinline__ uint32_t mailbox_wait(const uint32_t *mb, uint32_t par, const int *stop, int &why)
 {
     const int lane = threadIdx.x & 63;
     for (int spins = 0;; ++spins) {
         const uint32_t v = lds_ld(&mb[lane]);
-        if (__all((v & 1u) == par)) return int(v >> 1);
+        if (__all((v & 1u) == par)) return v;
         if (lds_ld(stop) != 0) {
             why = 1;
-            return kInf;
+            return ~0u;
         }
         if (spins > kSpinLimit) {
             why = 2;
-            return kInf;
+            return ~0u;
         }
         __builtin_amdgcn_s_sleep(4);
     }
@@ -149,7 +149,6 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
     const int S = p.S, n = p.n, SN = S * n, V = 2 * SN + 3;
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int nw = (S + P - 1) / P;       // waves that own stages
     const int k0 = w * P;                 // this wave's first stage
     const int klast = min(S, k0 + P) - 1; // and last (k0 > klast for idle waves)
     const bool jv = lane < n;
@@ -157,7 +156,7 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
     extern __shared__ __align__(16) unsigned char smem[];
     __shared__ PipeShared ps;
     const PipeLayout L = pipe_layout(S, W, p.list_slots);
-    uint32_t *exmb = reinterpret_cast<uint32_t *>(smem + L.exmb); // [W][64] last-stage exit labels << 1 | parity
+    uint32_t *exmb = reinterpret_cast<uint32_t *>(smem + L.exmb); // [W][64] last-stage exit labels << 2 | changed << 1 | parity
     uint32_t *enmb = reinterpret_cast<uint32_t *>(smem + L.enmb); // [W][64] first-stage entry labels << 1 | parity
     int *nf = reinterpret_cast<int *>(smem + L.nf);               // [S][64] node flow
     int *capl = reinterpret_cast<int *>(smem + L.capl);           // [S][64] node capacity
@@ -328,11 +327,7 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
             }
             if (k0 <= klast) {
                 if (k0 >= 1) lds_st(&enmb[w * 64 + lane], uint32_t(din[0]) << 1);
-                if (klast + 1 < S) lds_st(&exmb[w * 64 + lane], uint32_t(kInf) << 1);
-            }
-            if (tid < kRing) {
-                ps.ring[tid] = 0;
-                ps.ring_key[tid] = ~0ull;
+                if (klast + 1 < S) lds_st(&exmb[w * 64 + lane], uint32_t(kInf) << 2);
             }
             if (tid == 0) {
                 ps.stop = 0;
@@ -350,10 +345,10 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
                         if (lane == 0) atomicOr(&ps.fault, 1);
                         break;
                     }
-                    if (__builtin_amdgcn_readfirstlane(lds_ld(&ps.stop)) != 0) break;
                     const uint32_t par = uint32_t(t) & 1u;
                     int why = 0;
                     bool chg = false;
+                    uint32_t upch = 0; // 2 if a stage before this wave's changed in iteration t
                     uint64_t skey = ~0ull;
 #pragma unroll
                     for (int s = 0; s < P; ++s) {
@@ -364,11 +359,17 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
                         const int fl = nf[q], cp = capl[q], nc = ncl[q];
                         // forward input: exit labels of stage k-1, iteration t
                         int X = kInf;
-                        if (k >= 1) X = s == 0 ? mailbox_wait(&exmb[(w - 1) * 64], par, &ps.stop, why) : dout[s - 1];
+                        if (k >= 1 && s == 0) {
+                            const uint32_t word = mailbox_wait(&exmb[(w - 1) * 64], par, &ps.stop, why);
+                            X = int(word >> 2);
+                            upch = __builtin_amdgcn_readfirstlane(word) & 2u;
+                        } else if (k >= 1) {
+                            X = dout[s - 1];
+                        }
                         // backward input: entry labels of stage k+1, iteration t-1
                         int Y = kInf;
                         if (k + 1 < S && !why)
-                            Y = k == klast ? mailbox_wait(&enmb[(w + 1) * 64], par ^ 1u, &ps.stop, why) : din[s + 1];
+                            Y = k == klast ? int(mailbox_wait(&enmb[(w + 1) * 64], par ^ 1u, &ps.stop, why) >> 1) : din[s + 1];
                         if (why) break;
                         ++steps;
                         int di = din[s], dq = dout[s], pi = pred_in(pp[s]), po = pred_out(pp[s]);
@@ -493,7 +494,10 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
                         dout[s] = dq;
                         pp[s] = pred_pack(pi, po);
                         if (s == 0 && k >= 1) lds_st(&enmb[w * 64 + lane], (uint32_t(di) << 1) | par);
-                        if (k == klast && k + 1 < S) lds_st(&exmb[w * 64 + lane], (uint32_t(dq) << 1) | par);
+                        if (k == klast && k + 1 < S) {
+                            const uint32_t ch = (upch | (__any(chg) ? 2u : 0u));
+                            lds_st(&exmb[w * 64 + lane], (uint32_t(dq) << 2) | ch | par);
+                        }
                         if (k == S - 1) {
                             const uint64_t key = (jv && dq < kInf) ? pack_key(dq + snkc, lane) : ~0ull;
                             skey = wave_min_u64(key);
@@ -503,22 +507,14 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
                         if (why == 2 && lane == 0) atomicOr(&ps.fault, 1);
                         break;
                     }
-                    // count this wave into iteration t
-                    const bool anych = __any(chg);
-                    if (lane == 0) {
-                        const int slot = t & (kRing - 1);
-                        if (skey != ~0ull) atomicMin(&ps.ring_key[slot], skey);
-                        const unsigned mine = anych ? 0x101u : 1u;
-                        const unsigned total = atomicAdd(&ps.ring[slot], mine) + mine;
-                        if ((total & 0xffu) == unsigned(nw)) {
-                            if ((total >> 8) == 0) {
-                                ps.final_key = lds_ld(&ps.ring_key[slot]);
-                                lds_st(&ps.stop, t);
-                            } else {
-                                lds_st(&ps.ring[slot], 0u);
-                                lds_st(&ps.ring_key[slot], ~0ull);
-                            }
+                    // the wave of the last stage: no label changed anywhere in
+                    // iteration t ends the search
+                    if (klast == S - 1 && upch == 0 && !__any(chg)) {
+                        if (lane == 0) {
+                            ps.final_key = skey;
+                            lds_st(&ps.stop, t);
                         }
+                        break;
                     }
                 }
             }
