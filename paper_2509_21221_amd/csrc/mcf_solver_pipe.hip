@@ -355,26 +355,11 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
                         const int k = k0 + s;
                         if (k > klast) break;
                         const int q = k * 64 + lane;
-                        // node data for this step, read ahead of the waits
                         const int fl = nf[q], cp = capl[q], nc = ncl[q];
-                        // forward input: exit labels of stage k-1, iteration t
-                        int X = kInf;
-                        if (k >= 1 && s == 0) {
-                            const uint32_t word = mailbox_wait(&exmb[(w - 1) * 64], par, &ps.stop, why);
-                            X = int(word >> 2);
-                            upch = __builtin_amdgcn_readfirstlane(word) & 2u;
-                        } else if (k >= 1) {
-                            X = dout[s - 1];
-                        }
-                        // backward input: entry labels of stage k+1, iteration t-1
-                        int Y = kInf;
-                        if (k + 1 < S && !why)
-                            Y = k == klast ? int(mailbox_wait(&enmb[(w + 1) * 64], par ^ 1u, &ps.stop, why) >> 1) : din[s + 1];
-                        if (why) break;
-                        ++steps;
                         int di = din[s], dq = dout[s], pi = pred_in(pp[s]), po = pred_out(pp[s]);
                         const int di0 = di, dq0 = dq;
-                        if (k >= 1) {
+                        // links from stage k-1's exit labels X
+                        auto relax = [&](const int X) {
                             const bool dr = X < seen[s];
                             seen[s] = dr ? X : seen[s];
                             const uint64_t mask = __ballot(dr);
@@ -450,45 +435,75 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
                                     }
                                 }
                             }
-                        }
-                        if (fl > 0 && dq < kInf && dq - nc < di) {
-                            di = dq - nc;
-                            pi = kPredSplit;
-                        }
-                        if (di < kInf && fl < cp && di + nc < dq) {
-                            dq = di + nc;
-                            po = kPredSplit;
-                        }
+                        };
                         // reverse links, only when some entry label of stage k+1 dropped
                         // since this stage last pulled (lists change only between
                         // searches): four list entries per pass, partner labels from
                         // the partner's lane (the loop runs to the wave's longest
                         // list so every cross-lane read has all lanes active)
-                        const bool ydr = Y < seeny[s];
-                        seeny[s] = ydr ? Y : seeny[s];
-                        if (k + 1 < S && __ballot(ydr) != 0) {
-                            const int lo = lst_lo[s], len = lst_len[s], maxlen = lst_max[s];
-                            for (int e = 0; e < maxlen; e += 4) {
-                                uint32_t ent[4];
+                        auto pull = [&](const int Y) {
+                            const bool ydr = Y < seeny[s];
+                            seeny[s] = ydr ? Y : seeny[s];
+                            if (k + 1 < S && __ballot(ydr) != 0) {
+                                const int lo = lst_lo[s], len = lst_len[s], maxlen = lst_max[s];
+                                for (int e = 0; e < maxlen; e += 4) {
+                                    uint32_t ent[4];
 #pragma unroll
-                                for (int u = 0; u < 4; ++u) ent[u] = lent[lo + e + u];
+                                    for (int u = 0; u < 4; ++u) ent[u] = lent[lo + e + u];
 #pragma unroll
-                                for (int u = 0; u < 4; ++u) {
-                                    const bool here = e + u < len;
-                                    const int j = here ? int(ent[u] & 255u) : 0, c = int(ent[u] >> 8);
-                                    const int dj = __shfl(Y, j);
-                                    if (here && dj < kInf && dj - c < dq) {
-                                        dq = dj - c;
-                                        po = j;
+                                    for (int u = 0; u < 4; ++u) {
+                                        const bool here = e + u < len;
+                                        const int j = here ? int(ent[u] & 255u) : 0, c = int(ent[u] >> 8);
+                                        const int dj = __shfl(Y, j);
+                                        if (here && dj < kInf && dj - c < dq) {
+                                            dq = dj - c;
+                                            po = j;
+                                        }
                                     }
                                 }
+                                pulls += len;
                             }
-                            pulls += len;
+                        };
+                        auto split_rev = [&]() {
+                            if (fl > 0 && dq < kInf && dq - nc < di) {
+                                di = dq - nc;
+                                pi = kPredSplit;
+                            }
+                        };
+                        auto split_fwd = [&]() {
+                            if (di < kInf && fl < cp && di + nc < dq) {
+                                dq = di + nc;
+                                po = kPredSplit;
+                            }
+                        };
+                        // The input held by this wave first (a wave's first stage
+                        // pulls from its second's entry labels of iteration t-1,
+                        // its second relaxes from its first's exit labels of
+                        // iteration t), then the one another wave sends: the work
+                        // between a mailbox read and the next mailbox write is
+                        // what the waves pass to each other.
+                        if (s < P - 1 && k + 1 < S) {
+                            pull(din[s + 1]);
+                            split_rev();
                         }
-                        if (fl > 0 && dq < kInf && dq - nc < di) {
-                            di = dq - nc;
-                            pi = kPredSplit;
+                        if (s > 0) relax(dout[s - 1]);
+                        if (s == 0 && k >= 1) {
+                            // exit labels of stage k-1, iteration t, from the previous wave
+                            const uint32_t word = mailbox_wait(&exmb[(w - 1) * 64], par, &ps.stop, why);
+                            if (why) break;
+                            upch = __builtin_amdgcn_readfirstlane(word) & 2u;
+                            relax(int(word >> 2));
                         }
+                        split_rev();
+                        split_fwd();
+                        if (s == P - 1 && k + 1 < S) {
+                            // entry labels of stage k+1, iteration t-1, from the next wave
+                            const int Y = int(mailbox_wait(&enmb[(w + 1) * 64], par ^ 1u, &ps.stop, why) >> 1);
+                            if (why) break;
+                            pull(Y);
+                            split_rev();
+                        }
+                        ++steps;
                         chg |= (di != di0) | (dq != dq0);
                         din[s] = di;
                         dout[s] = dq;
