@@ -62,21 +62,36 @@ enum : int { kArcSplitFwd = 0, kArcSplitRev = 1, kArcLinkFwd = 2, kArcLinkRev = 
 
 typedef uint32_t u32x32 __attribute__((ext_vector_type(32)));
 
-__device__ __forceinline__ uint64_t pack_key(int label, int idx)
-{
-    return (uint64_t(uint32_t(label + kBias)) << 32) | uint32_t(idx);
-}
 __device__ __forceinline__ int key_label(uint64_t key) { return int(uint32_t(key >> 32)) - kBias; }
 
-__device__ __forceinline__ uint64_t wave_min_u64(uint64_t v)
+// Reduction over the 64 lanes with DPP moves only (no LDS): swaps within
+// quads, rotations within rows of 16, then row broadcasts; lane 63 ends with
+// the result, which every lane reads.
+template <int kCtrl, int kRows> __device__ __forceinline__ uint32_t dpp_mov(uint32_t x)
 {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-        const uint32_t lo = __shfl_xor(uint32_t(v), off), hi = __shfl_xor(uint32_t(v >> 32), off);
-        const uint64_t o = (uint64_t(hi) << 32) | lo;
-        v = o < v ? o : v;
-    }
-    return v;
+    return uint32_t(__builtin_amdgcn_update_dpp(int(x), int(x), kCtrl, kRows, 0xf, false));
+}
+template <bool kMax> __device__ __forceinline__ uint32_t wave_reduce_u32(uint32_t v)
+{
+    auto op = [](uint32_t a, uint32_t b) { return kMax ? max(a, b) : min(a, b); };
+    v = op(v, dpp_mov<0xb1, 0xf>(v));  // quad_perm [1,0,3,2]
+    v = op(v, dpp_mov<0x4e, 0xf>(v));  // quad_perm [2,3,0,1]
+    v = op(v, dpp_mov<0x124, 0xf>(v)); // row_ror:4
+    v = op(v, dpp_mov<0x128, 0xf>(v)); // row_ror:8
+    v = op(v, dpp_mov<0x142, 0xa>(v)); // row_bcast:15 into rows 1 and 3
+    v = op(v, dpp_mov<0x143, 0xc>(v)); // row_bcast:31 into rows 2 and 3
+    return __builtin_amdgcn_readlane(v, 63);
+}
+
+// The sink key of the wave: the smallest label and, among equal labels, the
+// lowest lane; ~0 when no lane has one.
+__device__ __forceinline__ uint64_t wave_min_key(bool has, int label)
+{
+    const uint32_t v = has ? uint32_t(label + kBias) : ~0u;
+    const uint32_t m = wave_reduce_u32<false>(v);
+    if (m == ~0u) return ~0ull;
+    const int first = __builtin_ctzll(__ballot(v == m));
+    return (uint64_t(m) << 32) | uint32_t(first);
 }
 
 // LDS accesses another wave may be racing with.
@@ -311,10 +326,7 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
                 const bool own = k0 + s <= klast && k0 + s + 1 < S;
                 lst_lo[s] = own ? int(loff[q]) : 0;
                 lst_len[s] = own && jv ? int(llen[q]) : 0;
-                int m = lst_len[s];
-#pragma unroll
-                for (int off = 32; off > 0; off >>= 1) m = max(m, __shfl_xor(m, off));
-                lst_max[s] = __builtin_amdgcn_readfirstlane(m);
+                lst_max[s] = int(wave_reduce_u32<true>(uint32_t(lst_len[s])));
             }
 #pragma unroll
             for (int s = 0; s < P; ++s) {
@@ -450,15 +462,17 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
                                     uint32_t ent[4];
 #pragma unroll
                                     for (int u = 0; u < 4; ++u) ent[u] = lent[lo + e + u];
+                                    // the four partner reads first, then the updates as
+                                    // selects, so the reads are in flight together
+                                    int dj[4];
+#pragma unroll
+                                    for (int u = 0; u < 4; ++u) dj[u] = __shfl(Y, e + u < len ? int(ent[u] & 255u) : 0);
 #pragma unroll
                                     for (int u = 0; u < 4; ++u) {
-                                        const bool here = e + u < len;
-                                        const int j = here ? int(ent[u] & 255u) : 0, c = int(ent[u] >> 8);
-                                        const int dj = __shfl(Y, j);
-                                        if (here && dj < kInf && dj - c < dq) {
-                                            dq = dj - c;
-                                            po = j;
-                                        }
+                                        const int cand = dj[u] - int(ent[u] >> 8);
+                                        const bool take = (e + u < len) & (dj[u] < kInf) & (cand < dq);
+                                        dq = take ? cand : dq;
+                                        po = take ? int(ent[u] & 255u) : po;
                                     }
                                 }
                                 pulls += len;
@@ -514,8 +528,7 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
                             lds_st(&exmb[w * 64 + lane], (uint32_t(dq) << 2) | ch | par);
                         }
                         if (k == S - 1) {
-                            const uint64_t key = (jv && dq < kInf) ? pack_key(dq + snkc, lane) : ~0ull;
-                            skey = wave_min_u64(key);
+                            skey = wave_min_key(jv && dq < kInf, dq + snkc);
                         }
                     }
                     if (why) {
