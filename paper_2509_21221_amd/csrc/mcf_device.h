@@ -72,6 +72,25 @@ __device__ __forceinline__ uint64_t lap(uint64_t &tick)
     return d;
 }
 
+// Reduction over the 64 lanes with DPP moves only (no LDS): swaps within
+// quads, rotations within rows of 16, then row broadcasts; lane 63 ends with
+// the result, which every lane reads.
+template <int kCtrl, int kRows> __device__ __forceinline__ uint32_t dpp_mov(uint32_t x)
+{
+    return uint32_t(__builtin_amdgcn_update_dpp(int(x), int(x), kCtrl, kRows, 0xf, false));
+}
+template <bool kMax> __device__ __forceinline__ uint32_t wave_reduce_u32(uint32_t v)
+{
+    auto op = [](uint32_t a, uint32_t b) { return kMax ? max(a, b) : min(a, b); };
+    v = op(v, dpp_mov<0xb1, 0xf>(v));  // quad_perm [1,0,3,2]
+    v = op(v, dpp_mov<0x4e, 0xf>(v));  // quad_perm [2,3,0,1]
+    v = op(v, dpp_mov<0x124, 0xf>(v)); // row_ror:4
+    v = op(v, dpp_mov<0x128, 0xf>(v)); // row_ror:8
+    v = op(v, dpp_mov<0x142, 0xa>(v)); // row_bcast:15 into rows 1 and 3
+    v = op(v, dpp_mov<0x143, 0xc>(v)); // row_bcast:31 into rows 2 and 3
+    return __builtin_amdgcn_readlane(v, 63);
+}
+
 __device__ __forceinline__ void wave_sync()
 {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");

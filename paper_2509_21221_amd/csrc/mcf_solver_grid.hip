@@ -85,15 +85,15 @@ __device__ __forceinline__ uint64_t pack_key(int label, int idx)
 }
 __device__ __forceinline__ int key_label(uint64_t key) { return int(uint32_t(key >> 32)) - kBias; }
 
-__device__ __forceinline__ uint64_t wave_min_u64(uint64_t v)
+// The smallest (label, index) key of the wave, by DPP moves: the smallest
+// label and, among equal labels, the lowest lane, whose index is idx0 + lane
+// (indices increase with the lane); ~0 when no lane has one.
+__device__ __forceinline__ uint64_t wave_min_key(bool has, int label, int idx0)
 {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-        const uint32_t lo = __shfl_xor(uint32_t(v), off), hi = __shfl_xor(uint32_t(v >> 32), off);
-        const uint64_t o = (uint64_t(hi) << 32) | lo;
-        v = o < v ? o : v;
-    }
-    return v;
+    const uint32_t v = has ? uint32_t(label + kBias) : ~0u;
+    const uint32_t m = wave_reduce_u32<false>(v);
+    if (m == ~0u) return ~0ull;
+    return (uint64_t(m) << 32) | uint32_t(idx0 + __builtin_ctzll(__ballot(v == m)));
 }
 
 // Device-coherent accesses for data shared between workgroups.
@@ -443,9 +443,7 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                 }
                 const uint64_t m = __ballot(dropped);
                 const int en_any = __any(en_drop) ? 1 : 0;
-                int wmax = dropped ? dnew : 0;
-#pragma unroll
-                for (int off = 32; off > 0; off >>= 1) wmax = max(wmax, __shfl_xor(wmax, off));
+                const int wmax = int(wave_reduce_u32<true>(dropped ? uint32_t(dnew) : 0u));
                 if (lane == 0) {
                     wcnt[wave] = __popcll(m);
                     wmaxd[wave] = wmax;
@@ -556,6 +554,8 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
 
                 // compute arcs and reverse links of the owned nodes
                 uint64_t skey = ~0ull;
+                bool sink_has = false;
+                int sink_label = 0;
                 if (tid < nown) {
                     const int c = tid, q = k * n + j0 + c;
                     uint64_t kb = red[c];
@@ -602,12 +602,12 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                     st(&ex_out[q], (uint32_t(dq) << 2) | tag_f);
                     st(&en_out[q], (uint32_t(di) << 2) | tag_f);
                     if ((di != di0) | (dq != dq0)) sh_changed = 1;
-                    if (k == S - 1 && dq < kInf) skey = pack_key(dq + snkc[c], j0 + c);
+                    if (k == S - 1) sink_has = dq < kInf, sink_label = dq + snkc[c];
                 }
                 // the sink's best key: per wave first (the owner threads fill
                 // waves 0 and 1), then one LDS atomic per wave
                 if (k == S - 1 && tid < kGridNB) {
-                    skey = wave_min_u64(skey);
+                    skey = wave_min_key(sink_has, sink_label, j0 + wave * 64);
                     if (lane == 0 && skey != ~0ull) atomicMin(&sh_key, (unsigned long long)skey);
                 }
                 __syncthreads();
