@@ -520,6 +520,7 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                         const uint16_t *cc = cost16 + col;
                         if (dense) {
                             int e = lo;
+#pragma unroll 4
                             for (; e + 4 <= hi; e += 4) {
                                 const uint4 kq = *reinterpret_cast<const uint4 *>(&rowkey[e]);
                                 const uint32_t c0 = cc[(e + 0) * kGridNB], c1 = cc[(e + 1) * kGridNB];
@@ -531,6 +532,7 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                         } else {
                             const uint32_t *kl = reinterpret_cast<const uint32_t *>(rowlist);
                             int e = lo;
+#pragma unroll 4
                             for (; e + 4 <= hi; e += 4) {
                                 const uint4 kq = *reinterpret_cast<const uint4 *>(&kl[e]);
                                 const uint32_t c0 = cc[(kq.x & 511u) * kGridNB], c1 = cc[(kq.y & 511u) * kGridNB];
