@@ -580,24 +580,37 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
             };
             if (w != 0) update_potentials();
 
-            // ---- (3) wave 0: lane 0 walks the predecessor chain, then the
+            // ---- (3) wave 0 walks the predecessor chain, then the
             // whole wave takes the bottleneck over the recorded arcs ----
             if (w == 0) {
-                // the whole wave follows the chain (uniform values); lane 0 records
+                // the whole wave follows the chain (uniform values)
                 {
                     int len = 0;
                     bool okw = predt >= 0 && predt < n;
                     uint32_t v = 2 * ((S - 1) * 64 + predt) + 1;
+                    // A node's two vertices are 2q and 2q+1, and a compute arc
+                    // joins them: the partner's word is read with each vertex's
+                    // own, so a compute arc and the arc after it take one round.
+                    // Every lane writes the (uniform) path entries.
+                    static_assert(kChainDone > kChainBad, "one compare finds both markers");
                     while (okw) {
                         const uint32_t word = __builtin_amdgcn_readfirstlane(chain[v]);
-                        const uint32_t nx = word & kChainMask;
-                        if (nx == kChainDone) break;
-                        if (nx == kChainBad || len > 2 * SN + 4) {
-                            okw = false;
+                        const uint32_t part = __builtin_amdgcn_readfirstlane(chain[v ^ 1u]);
+                        uint32_t nx = word & kChainMask;
+                        if (nx >= kChainBad) {
+                            okw = nx == kChainDone;
                             break;
                         }
-                        if (lane == 0) path[len] = int(word >> 13);
-                        ++len;
+                        path[len++] = int(word >> 13);
+                        if (nx == (v ^ 1u)) {
+                            nx = part & kChainMask;
+                            if (nx >= kChainBad) {
+                                okw = nx == kChainDone;
+                                break;
+                            }
+                            path[len++] = int(part >> 13);
+                        }
+                        okw = len <= 2 * SN + 4;
                         v = nx;
                     }
                     if (lane == 0) ps.plen = okw ? len : -1;
@@ -619,8 +632,7 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
                         r = min(r, amt);
                     }
                 }
-#pragma unroll
-                for (int off = 32; off > 0; off >>= 1) r = min(r, __shfl_xor(r, off));
+                r = int(wave_reduce_u32<false>(uint32_t(r)));
                 if (lane == 0) ps.delta = r;
                 update_potentials();
             }
