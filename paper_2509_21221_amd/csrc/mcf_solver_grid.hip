@@ -402,28 +402,41 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                 bool need_ex = has_prev && tid < n, need_en = has_next && tid < n;
                 uint32_t wex = 0, wen = 0;
                 int why = 0; // 1: the search has converged, 2: wait bound exceeded
-                for (int spins = 0;; ++spins) {
-                    const uint32_t a = need_ex ? ld(&ex_f[tid]) : 0u;
-                    const uint32_t c = need_en ? ld(&en_b[tid]) : 0u;
-                    const int stop = (tid == 0 || (spins & 15) == 15) ? ld(&ctrl[kCtlStop]) : 0;
+                // Two rounds of reads in flight: the next round goes out
+                // before this one is looked at, so a word that lands is seen
+                // about half a read latency sooner.  The reads are the same
+                // in every thread (a thread past the stage's nodes reads the
+                // last node's word and ignores it), so none is masked off and
+                // each round waits only for the round before it.  (Once a word
+                // shows its tag it cannot change before this workgroup moves on.)
+                const int wi = min(tid, n - 1);
+                // one round of reads: examine it, or report the stop / a wait
+                // that ran out; true when this thread is done waiting
+                auto take = [&](uint32_t ra, uint32_t rc, int rs, int spins) {
                     if (need_ex) {
-                        wex = a;
-                        need_ex = (a & 3u) != tag_f;
+                        wex = ra;
+                        need_ex = (ra & 3u) != tag_f;
                     }
                     if (need_en) {
-                        wen = c;
-                        need_en = (c & 3u) != tag_b;
+                        wen = rc;
+                        need_en = (rc & 3u) != tag_b;
                     }
-                    if (stop) {
-                        why = 1;
-                        break;
-                    }
-                    if (!(need_ex | need_en)) break;
-                    if (spins > kSpinLimit) {
-                        why = 2;
-                        break;
-                    }
+                    if (rs) why = 1;
+                    else if ((need_ex | need_en) && spins > kSpinLimit) why = 2;
+                    return why != 0 || !(need_ex | need_en);
+                };
+                int s0 = ld(&ctrl[kCtlStop]);
+                uint32_t a0 = ld(&ex_f[wi]), c0 = ld(&en_b[wi]);
+                for (int spins = 0;; spins += 2) {
                     __builtin_amdgcn_s_sleep(1);
+                    const int s1 = ld(&ctrl[kCtlStop]);
+                    const uint32_t a1 = ld(&ex_f[wi]), c1 = ld(&en_b[wi]);
+                    if (take(a0, c0, s0, spins)) break;
+                    __builtin_amdgcn_s_sleep(1);
+                    s0 = ld(&ctrl[kCtlStop]);
+                    a0 = ld(&ex_f[wi]);
+                    c0 = ld(&en_b[wi]);
+                    if (take(a1, c1, s1, spins + 1)) break;
                 }
                 if (why) atomicOr(&sh_why[t & 1], why);
                 int dropped = 0, dnew = 0;
