@@ -116,13 +116,20 @@ struct PipeShared {
 
 // Waits until all 64 words of a mailbox carry parity `par` in bit 0; returns
 // this lane's word.  Sets why to 1 if the search stopped meanwhile, 2 if the
-// wait ran out.
+// wait ran out.  A wave that has its input raises its issue priority: the
+// work between a mailbox read and the next mailbox write is what the other
+// waves wait for, so it goes ahead of the three other waves on its SIMD
+// (which are polling or doing work nobody waits for yet); the wave drops back
+// at the start of its next iteration.
 __device__ __forceinline__ uint32_t mailbox_wait(const uint32_t *mb, uint32_t par, const int *stop, int &why)
 {
     const int lane = threadIdx.x & 63;
     for (int spins = 0;; ++spins) {
         const uint32_t v = lds_ld(&mb[lane]);
-        if (__all((v & 1u) == par)) return v;
+        if (__all((v & 1u) == par)) {
+            __builtin_amdgcn_s_setprio(3);
+            return v;
+        }
         if (lds_ld(stop) != 0) {
             why = 1;
             return ~0u;
@@ -339,6 +346,7 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
                         break;
                     }
                     const uint32_t par = uint32_t(t) & 1u;
+                    __builtin_amdgcn_s_setprio(0);
                     int why = 0;
                     bool chg = false;
                     uint32_t upch = 0; // 2 if a stage before this wave's changed in iteration t
@@ -527,6 +535,7 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
                     }
                 }
             }
+            __builtin_amdgcn_s_setprio(0);
 #pragma unroll
             for (int off = 32; off > 0; off >>= 1) pulls += __shfl_xor(pulls, off);
             if (lane == 0) {
@@ -594,8 +603,11 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
                     // Every lane writes the (uniform) path entries.
                     static_assert(kChainDone > kChainBad, "one compare finds both markers");
                     while (okw) {
-                        const uint32_t word = __builtin_amdgcn_readfirstlane(chain[v]);
-                        const uint32_t part = __builtin_amdgcn_readfirstlane(chain[v ^ 1u]);
+                        // both words of the node in one 8-byte read
+                        const uint64_t both = *reinterpret_cast<const uint64_t *>(&chain[v & ~1u]);
+                        const uint32_t lo = __builtin_amdgcn_readfirstlane(uint32_t(both));
+                        const uint32_t hi = __builtin_amdgcn_readfirstlane(uint32_t(both >> 32));
+                        const uint32_t word = (v & 1u) ? hi : lo, part = (v & 1u) ? lo : hi;
                         uint32_t nx = word & kChainMask;
                         if (nx >= kChainBad) {
                             okw = nx == kChainDone;
