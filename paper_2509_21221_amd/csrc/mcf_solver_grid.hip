@@ -698,48 +698,68 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                 if (wave == 0) {
                     int kk = S - 1, i = predt, len = 0;
                     bool at_exit = true, okw = predt >= 0 && predt < n;
-                    while (okw) {
-                        if (len > 2 * SN + 4) {
-                            okw = false;
-                            break;
-                        }
-                        const int word = __builtin_amdgcn_readfirstlane(all_pred[kk * n + i]);
-                        int code;
-                        if (at_exit) {
-                            const int pr = word >> 16;
-                            if (pr == kPredSplit) {
-                                code = path_code(kArcSplitFwd, kk, i, 0);
-                                at_exit = false;
-                            } else if (pr >= 0 && pr < n && kk + 1 < S) {
-                                code = path_code(kArcLinkRev, kk, i, pr); // entry (kk+1, pr) -> exit (kk, i)
-                                kk = kk + 1;
-                                i = pr;
-                                at_exit = false;
-                            } else {
-                                okw = false;
-                                break;
-                            }
-                        } else {
-                            const int pr = int(int16_t(word & 0xffff));
-                            if (pr == kPredSrc) break;
-                            if (pr == kPredSplit) {
-                                code = path_code(kArcSplitRev, kk, i, 0);
-                                at_exit = true;
-                            } else if (pr >= 0 && pr < n && kk >= 1) {
-                                code = path_code(kArcLinkFwd, kk - 1, pr, i); // exit (kk-1, pr) -> entry (kk, i)
-                                kk = kk - 1;
-                                i = pr;
-                                at_exit = true;
-                            } else {
-                                okw = false;
-                                break;
-                            }
-                        }
+                    auto record = [&](int code) {
                         if (lane == 0) {
                             if (len < kPathLds) lpath[len] = code;
                             else st(&gp.path[len], code);
                         }
                         ++len;
+                    };
+                    // One read per node visited: a compute arc and the link arc
+                    // after it come from the same word (entry predecessor in the
+                    // low half, exit predecessor in the high half).  A compute
+                    // arc followed by the opposite one would be a cycle.
+                    bool done = false;
+                    while (okw && !done) {
+                        if (len > 2 * SN + 4) {
+                            okw = false;
+                            break;
+                        }
+                        const int word = __builtin_amdgcn_readfirstlane(all_pred[kk * n + i]);
+                        const int pex = word >> 16, pen = int(int16_t(word & 0xffff));
+                        const bool ex_link = pex >= 0 && pex < n && kk + 1 < S;
+                        const bool en_link = pen >= 0 && pen < n && kk >= 1;
+                        if (at_exit) {
+                            if (pex == kPredSplit) {
+                                record(path_code(kArcSplitFwd, kk, i, 0));
+                                if (pen == kPredSrc) {
+                                    done = true;
+                                } else if (en_link) {
+                                    record(path_code(kArcLinkFwd, kk - 1, pen, i)); // exit (kk-1, pen) -> entry (kk, i)
+                                    kk = kk - 1;
+                                    i = pen;
+                                } else {
+                                    okw = false;
+                                }
+                            } else if (ex_link) {
+                                record(path_code(kArcLinkRev, kk, i, pex)); // entry (kk+1, pex) -> exit (kk, i)
+                                kk = kk + 1;
+                                i = pex;
+                                at_exit = false;
+                            } else {
+                                okw = false;
+                            }
+                        } else {
+                            if (pen == kPredSrc) {
+                                done = true;
+                            } else if (pen == kPredSplit) {
+                                record(path_code(kArcSplitRev, kk, i, 0));
+                                if (ex_link) {
+                                    record(path_code(kArcLinkRev, kk, i, pex)); // entry (kk+1, pex) -> exit (kk, i)
+                                    kk = kk + 1;
+                                    i = pex;
+                                } else {
+                                    okw = false;
+                                }
+                            } else if (en_link) {
+                                record(path_code(kArcLinkFwd, kk - 1, pen, i)); // exit (kk-1, pen) -> entry (kk, i)
+                                kk = kk - 1;
+                                i = pen;
+                                at_exit = true;
+                            } else {
+                                okw = false;
+                            }
+                        }
                     }
                     if (lane == 0) {
                         sh_len = okw ? len : -1;
