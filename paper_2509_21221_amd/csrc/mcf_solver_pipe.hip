@@ -378,13 +378,20 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
                                     for (int g = 0; g < 8; ++g) {
                                         const uint32_t half = g < 4 ? mlo : mhi;
                                         if (half & (0xffu << (8 * (g & 3)))) {
+                                            // the group's eight keys first, so the reads overlap
+                                            uint32_t xr[8], cand[8];
 #pragma unroll
-                                            for (int r = 8 * g; r < 8 * g + 8; r += 2) {
-                                                const uint32_t wd = lw[s][r >> 1];
-                                                const uint32_t a = __builtin_amdgcn_readlane(xk, r) + (wd & 0xffffu);
-                                                const uint32_t c = __builtin_amdgcn_readlane(xk, r + 1) + (wd >> 16);
-                                                key = min(key, min(a, c));
+                                            for (int u = 0; u < 8; ++u) xr[u] = __builtin_amdgcn_readlane(xk, 8 * g + u);
+#pragma unroll
+                                            for (int u = 0; u < 8; u += 2) {
+                                                const uint32_t wd = lw[s][(8 * g + u) >> 1];
+                                                cand[u] = xr[u] + (wd & 0xffffu);
+                                                cand[u + 1] = xr[u + 1] + (wd >> 16);
                                             }
+                                            const uint32_t m0 = min(min(cand[0], cand[1]), cand[2]);
+                                            const uint32_t m1 = min(min(cand[3], cand[4]), cand[5]);
+                                            const uint32_t m2 = min(min(cand[6], cand[7]), key);
+                                            key = min(min(m0, m1), m2);
                                         }
                                     }
                                 } else {
