@@ -62,7 +62,9 @@ template <int G, int I> __device__ __forceinline__ uint32_t group_bcast(uint32_t
         return uint32_t(__builtin_amdgcn_update_dpp(0, int(x), 0x150 + I, 0xf, 0xf, false));
     } else {
         static_assert(G == 8, "groups of 8 or 16 lanes");
-        const int lo = __builtin_amdgcn_update_dpp(0, int(x), 0x150 + I, 0xf, 0x3, false);
+        // lanes 8-15 of each row are written by the second move, so the
+        // first needs no old value
+        const int lo = __builtin_amdgcn_mov_dpp(int(x), 0x150 + I, 0xf, 0x3, false);
         return uint32_t(__builtin_amdgcn_update_dpp(lo, int(x), 0x158 + I, 0xf, 0xc, false));
     }
 }
