@@ -7,7 +7,7 @@
 
 namespace gwtf {
 
-constexpr int kGridCtrlInts = 32;      // control block: flags, barrier, per-iteration words
+constexpr int kGridCtrlInts = 48;      // control block: flags, barrier, per-iteration words, tied exits
 constexpr int kGridMaxNodes = 512;     // a stage's labels are staged with one thread per node
 constexpr size_t kGridStaticLds = 512; // static LDS of the grid kernel (upper bound)
 struct GridParams {

@@ -76,7 +76,9 @@ enum : int {
     kCtlRelax = 20,    // uint64
     kCtlPulls = 22,    // uint64
     kCtlFinalKey = 24, // uint64: sink label and exit of the converged search
+    kCtlTies = 32,     // [kGridMaxNodes / 32] exits of the last stage that reach the sink at its label
 };
+static_assert(kCtlTies + kGridMaxNodes / 32 <= kGridCtrlInts, "control block too small");
 static_assert(kCtlFinalKey + 2 <= kGridCtrlInts, "control block too small");
 
 __device__ __forceinline__ uint64_t pack_key(int label, int idx)
@@ -164,6 +166,8 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
     __shared__ int sh_ok, sh_flag, sh_bad, sh_maxc, sh_changed, sh_len, sh_delta, sh_fault, sh_why[2];
     __shared__ unsigned long long sh_key;
     __shared__ int wcnt[kGridWaves], wmaxd[kGridWaves], wendrop[kGridWaves];
+    __shared__ uint32_t sh_ties[kGridMaxNodes / 32];
+    __shared__ int sh_from;
 
     // ---- LDS layout (same offsets in every workgroup) ----
     // The leading area holds the link-cost block; workgroup 0 (no incoming
@@ -671,14 +675,32 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                 pin[c] = min(din[c], pin[c] + dred);
                 st(&gp.pred[q], (prin[c] & 0xffff) | (prout[c] << 16));
             }
+            if (k == S - 1 && wave < kGridNB / 64) {
+                // the last stage's exits whose path reaches the sink at its label
+                const bool tie = tid < nown && dout[tid] < kInf && dout[tid] + snkc[tid] == Dt;
+                const uint64_t bm = __ballot(tie);
+                const int w0 = (j0 + wave * 64) >> 5;
+                if (lane == 0) {
+                    if (w0 < kGridMaxNodes / 32) st(&ctrl[kCtlTies + w0], int(uint32_t(bm)));
+                    if (w0 + 1 < kGridMaxNodes / 32) st(&ctrl[kCtlTies + w0 + 1], int(uint32_t(bm >> 32)));
+                }
+            }
             if (!bar.sync(&sh_ok, &sh_flag)) {
                 timed_out = true;
                 break;
             }
 
-            // ---- (3) workgroup 0: walk the path, find the bottleneck ----
+            // ---- (3) workgroup 0: walk the path, find the bottleneck; (4)
+            // the owners apply it.  Then every other exit of the last stage
+            // that reaches the sink at the same label is tried: its tree path
+            // is still a shortest path while none of its arcs is saturated
+            // (an augmentation only removes saturated arcs and adds reverse
+            // arcs, which cannot shorten any distance), so it is augmented
+            // without a new search when its bottleneck is positive. ----
+            bool first = true, quit = false;
+            for (;;) {
             if (g == 0) {
-                {
+                if (first) {
                     // eight loads in flight per thread
                     int q = tid;
                     for (; q + 7 * kGridThreads < SN; q += 8 * kGridThreads) {
@@ -689,15 +711,22 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                         for (int u = 0; u < 8; ++u) all_pred[q + u * kGridThreads] = v[u];
                     }
                     for (; q < SN; q += kGridThreads) all_pred[q] = ld(&gp.pred[q]);
+                    if (tid < kGridMaxNodes / 32) {
+                        uint32_t tw = uint32_t(ld(&ctrl[kCtlTies + tid]));
+                        if (tid == (predt >> 5)) tw &= ~(1u << (predt & 31));
+                        sh_ties[tid] = tw;
+                    }
+                    if (tid == 0) sh_from = predt;
                 }
                 __syncthreads();
+                const int from = sh_from;
                 // Wave 0 follows the predecessors from the sink (uniform values:
                 // every lane walks, lane 0 records); one predecessor word serves
                 // both vertices of a node.  The first kPathLds arcs stay in LDS.
                 int *lpath = reinterpret_cast<int *>(red);
-                if (wave == 0) {
-                    int kk = S - 1, i = predt, len = 0;
-                    bool at_exit = true, okw = predt >= 0 && predt < n;
+                if (wave == 0 && from >= 0) {
+                    int kk = S - 1, i = from, len = 0;
+                    bool at_exit = true, okw = from < n;
                     auto record = [&](int code) {
                         if (lane == 0) {
                             if (len < kPathLds) lpath[len] = code;
@@ -782,21 +811,26 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                 }
                 __syncthreads();
                 if (tid == 0) {
+                    // length -2: no exit left to try
                     st(&ctrl[kCtlDelta], len < 0 ? -1 : sh_delta);
-                    st(&ctrl[kCtlLen], len);
+                    st(&ctrl[kCtlLen], from < 0 ? -2 : len);
                 }
             }
             if (!bar.sync(&sh_ok, &sh_flag)) {
                 timed_out = true;
+                quit = true;
                 break;
             }
 
             // ---- (4) owners apply the augmentation: decrements, then increments ----
             const int delta = ld(&ctrl[kCtlDelta]), len = ld(&ctrl[kCtlLen]);
-            if (delta <= 0 || len < 0 || len > 2 * SN + 5) {
+            if (!first && len == -2) break;
+            if (len < 0 || len > 2 * SN + 5 || (first && delta <= 0)) {
                 if (tid == 0) sh_fault = 1;
+                quit = true;
                 break;
             }
+            if (delta > 0) {
             for (int pass = 0; pass < 2; ++pass) {
                 for (int e = tid; e < len; e += kGridThreads) {
                     const int code = ld(&gp.path[e]), type = code_type(code), ak = code_stage(code), ai = code_node(code);
@@ -858,6 +892,28 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
             F += delta;
             cost += (long long)delta * Dt;
             augs++;
+            }
+            first = false;
+            if (F >= supply) break;
+            // the applied flows are visible to workgroup 0's next bottleneck
+            if (!bar.sync(&sh_ok, &sh_flag)) {
+                timed_out = true;
+                quit = true;
+                break;
+            }
+            if (g == 0 && tid == 0) {
+                int nx = -1;
+                for (int w = 0; w < kGridMaxNodes / 32 && nx < 0; ++w) {
+                    if (sh_ties[w]) {
+                        const int bit = __builtin_ctz(sh_ties[w]);
+                        sh_ties[w] &= sh_ties[w] - 1;
+                        nx = w * 32 + bit;
+                    }
+                }
+                sh_from = nx;
+            }
+            }
+            if (quit) break;
             pit = Dt;
             if (F >= supply) break;
             reset_labels();
