@@ -135,6 +135,21 @@ def test_grid_pass_shapes(S, n, holes, zero):
     assert (g["passes"] == mcf.GWTF_PASS_GRID).all()
 
 
+@pytest.mark.parametrize("S,n,cost_hi", [(3, 200, 0), (6, 130, 1), (12, 300, 2), (4, 512, 3)])
+def test_grid_pass_tied_exits(S, n, cost_hi):
+    """Costs drawn from a handful of values make many exits of the last
+    stage reach the sink at the same label: the grid pass augments them along
+    their tree paths without a new search while their bottleneck is positive,
+    and skips those whose path the previous one saturated."""
+    batch = W.random_small(2, S, n, seed=31, cap_hi=3, cost_hi=cost_hi, supply_hi=80)
+    for a in (batch.node_cost, batch.arc_cost, batch.src_cost, batch.snk_cost):
+        a += 1  # every cost in [1, cost_hi + 1]: no free path, many equal ones
+    say("grid pass ties", S, n, cost_hi)
+    g = gpu_solve(batch, stats=True)
+    compare(batch, g, oracle.solve(batch))
+    assert (g["passes"] == mcf.GWTF_PASS_GRID).all()
+
+
 def test_grid_pass_routing_and_status():
     """At n = 512 a workgroup's LDS holds about 1400 flow-list slots: an
     instance with capacities of 64 reserves 128 * 64 and moves to the global
