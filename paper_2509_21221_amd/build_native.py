@@ -4,7 +4,8 @@
 
 Compiles every .hip source under csrc/ with hipcc into
 paper_2509_21221_amd/libgwtf_mcf.so.  Packed-FP32 instruction selection is
-switched off for all device code.
+switched off for all device code, and the backend schedules for memory
+clauses.
 """
 import glob
 import os
@@ -31,6 +32,9 @@ def build(verbose: bool = False) -> str:
     cmd = [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
            "-Wall", "-Wno-unused-function",
            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+           # the backend's memory-clause scheduling strategy: 2 % faster on the
+           # grid pass (64 x 512 instance), neutral on the other passes
+           "-mllvm", "-amdgpu-sched-strategy=max-memory-clause",
            "-I", os.path.join(ROOT, "include"), "-I", os.path.join(PKG, "csrc"),
            *srcs, "-o", tmp]
     if verbose:
