@@ -70,6 +70,7 @@ enum : int {
     kCtlMaxCost = 1,
     kCtlBarCount = 2, // arrivals in the low 16 bits, raised flags above
     kCtlBarWord = 3,  // epoch << 1 | OR of the last barrier's flags
+    kCtlSinkBest = 4, // uint64: the smallest sink key of the current search so far
     kCtlDelta = 16,
     kCtlLen = 17,
     kCtlStop = 18,     // iteration at which the search converged, 0 while it runs
@@ -215,6 +216,7 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
 
     int *ctrl = gp.ctrl;
     unsigned long long *final_key_w = reinterpret_cast<unsigned long long *>(ctrl + kCtlFinalKey);
+    unsigned long long *sinkbest_w = reinterpret_cast<unsigned long long *>(ctrl + kCtlSinkBest);
     GridBarrier bar{reinterpret_cast<unsigned *>(ctrl + kCtlBarCount), reinterpret_cast<unsigned *>(ctrl + kCtlBarWord),
                     gridDim.x, 0u};
     if (tid == 0) bar.epoch = ld(bar.word) >> 1;
@@ -377,6 +379,7 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
             if (tid == 0) {
                 st(&ctrl[kCtlStop], 0);
                 st(final_key_w, ~0ull);
+                st(sinkbest_w, ~0ull);
             }
         }
         if (tid == 0) sh_why[0] = sh_why[1] = 0;
@@ -397,6 +400,12 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
             uint64_t final_key = ~0ull;
             bool converged = false;
             for (int t = 1; t <= 4 * V + 8; ++t) {
+                // The sink's label so far bounds which changes matter: a vertex
+                // whose reduced label reaches the sink's cannot lie on a
+                // shortest path to it, and its label is only an upper bound,
+                // which the potential update ignores.  The value read is at
+                // least the final one, so the test only counts more changes.
+                const unsigned long long sbest = ld(sinkbest_w);
                 if (located && has_prev && tid < L) mkey[tid] = ~0ull;
                 const uint32_t *ex_f = gp.ex + size_t(t & 1) * SN + size_t(has_prev ? k - 1 : 0) * n;
                 const uint32_t *en_b = gp.en + size_t((t - 1) & 1) * SN + size_t(has_next ? k + 1 : 0) * n;
@@ -620,7 +629,8 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                     prout[c] = po;
                     st(&ex_out[q], (uint32_t(dq) << 2) | tag_f);
                     st(&en_out[q], (uint32_t(di) << 2) | tag_f);
-                    if ((di != di0) | (dq != dq0)) sh_changed = 1;
+                    const int bound = sbest == ~0ull ? kInf : key_label(sbest) - pit;
+                    if (((di != di0) & (di - pin[c] < bound)) | ((dq != dq0) & (dq - pout[c] < bound))) sh_changed = 1;
                     if (k == S - 1) sink_has = dq < kInf, sink_label = dq + snkc[c];
                 }
                 // the sink's best key: per wave first (the owner threads fill
@@ -637,6 +647,7 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                     const int slot = t % gp.ring_slots;
                     if (sh_key != ~0ull) {
                         atomicMin(&gp.ring_key[slot], sh_key);
+                        atomicMin(sinkbest_w, sh_key);
                         drain();
                     }
                     const unsigned mine = sh_changed ? 0x10001u : 1u;
