@@ -74,6 +74,7 @@ enum : int {
     kCtlDelta = 16,
     kCtlLen = 17,
     kCtlStop = 18,     // iteration at which the search converged, 0 while it runs
+    kCtlMore = 19,     // tied exits are left to try after this path
     kCtlRelax = 20,    // uint64
     kCtlPulls = 22,    // uint64
     kCtlFinalKey = 24, // uint64: sink label and exit of the converged search
@@ -168,7 +169,7 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
     __shared__ unsigned long long sh_key;
     __shared__ int wcnt[kGridWaves], wmaxd[kGridWaves], wendrop[kGridWaves];
     __shared__ uint32_t sh_ties[kGridMaxNodes / 32];
-    __shared__ int sh_from;
+    __shared__ int sh_esat;
 
     // ---- LDS layout (same offsets in every workgroup) ----
     // The leading area holds the link-cost block; workgroup 0 (no incoming
@@ -702,16 +703,26 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
             }
 
             // ---- (3) workgroup 0: walk the path, find the bottleneck; (4)
-            // the owners apply it.  Then every other exit of the last stage
-            // that reaches the sink at the same label is tried: its tree path
-            // is still a shortest path while none of its arcs is saturated
-            // (an augmentation only removes saturated arcs and adds reverse
-            // arcs, which cannot shorten any distance), so it is augmented
-            // without a new search when its bottleneck is positive. ----
+            // the owners apply it.  Then the other exits of the last stage
+            // that reach the sink at the same label are tried: an exit's tree
+            // path is still a shortest path unless an earlier path of this
+            // search saturated one of its arcs (an augmentation only removes
+            // saturated arcs and adds reverse arcs, which cannot shorten any
+            // distance), so it is augmented without a new search.  Workgroup
+            // 0 marks, after each path, the path's vertices from the sink back
+            // to the head of its first saturated arc (counted from the data
+            // node): a tree path that meets a marked vertex continues through
+            // that arc, so the walk drops the exit there and takes the next. ----
             bool first = true, quit = false;
             for (;;) {
             if (g == 0) {
                 if (first) {
+                    // predecessors biased by 3 into 15-bit fields, the
+                    // marks in bits 15 (entry) and 31 (exit)
+                    auto bias = [](int w) {
+                        const int pen = int(int16_t(w & 0xffff)), pex = w >> 16;
+                        return int(uint32_t(pen + 3) | (uint32_t(pex + 3) << 16));
+                    };
                     // eight loads in flight per thread
                     int q = tid;
                     for (; q + 7 * kGridThreads < SN; q += 8 * kGridThreads) {
@@ -719,112 +730,157 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
 #pragma unroll
                         for (int u = 0; u < 8; ++u) v[u] = ld(&gp.pred[q + u * kGridThreads]);
 #pragma unroll
-                        for (int u = 0; u < 8; ++u) all_pred[q + u * kGridThreads] = v[u];
+                        for (int u = 0; u < 8; ++u) all_pred[q + u * kGridThreads] = bias(v[u]);
                     }
-                    for (; q < SN; q += kGridThreads) all_pred[q] = ld(&gp.pred[q]);
+                    for (; q < SN; q += kGridThreads) all_pred[q] = bias(ld(&gp.pred[q]));
                     if (tid < kGridMaxNodes / 32) {
                         uint32_t tw = uint32_t(ld(&ctrl[kCtlTies + tid]));
                         if (tid == (predt >> 5)) tw &= ~(1u << (predt & 31));
                         sh_ties[tid] = tw;
                     }
-                    if (tid == 0) sh_from = predt;
                 }
                 __syncthreads();
-                const int from = sh_from;
                 // Wave 0 follows the predecessors from the sink (uniform values:
                 // every lane walks, lane 0 records); one predecessor word serves
                 // both vertices of a node.  The first kPathLds arcs stay in LDS.
                 int *lpath = reinterpret_cast<int *>(red);
-                if (wave == 0 && from >= 0) {
-                    int kk = S - 1, i = from, len = 0;
-                    bool at_exit = true, okw = from < n;
-                    auto record = [&](int code) {
-                        if (lane == 0) {
-                            if (len < kPathLds) lpath[len] = code;
-                            else st(&gp.path[len], code);
+                if (wave == 0) {
+                    // the next tied exit not tried yet (uniform), -1 if none
+                    auto next_tie = [&]() {
+                        for (int w = 0; w < kGridMaxNodes / 32; ++w) {
+                            const uint32_t tw = __builtin_amdgcn_readfirstlane(sh_ties[w]);
+                            if (tw) {
+                                if (lane == 0) sh_ties[w] = tw & (tw - 1);
+                                return w * 32 + __builtin_ctz(tw);
+                            }
                         }
-                        ++len;
+                        return -1;
                     };
-                    // One read per node visited: a compute arc and the link arc
-                    // after it come from the same word (entry predecessor in the
-                    // low half, exit predecessor in the high half).  A compute
-                    // arc followed by the opposite one would be a cycle.
-                    bool done = false;
-                    while (okw && !done) {
-                        if (len > 2 * SN + 4) {
-                            okw = false;
-                            break;
-                        }
-                        const int word = __builtin_amdgcn_readfirstlane(all_pred[kk * n + i]);
-                        const int pex = word >> 16, pen = int(int16_t(word & 0xffff));
-                        const bool ex_link = pex >= 0 && pex < n && kk + 1 < S;
-                        const bool en_link = pen >= 0 && pen < n && kk >= 1;
-                        if (at_exit) {
-                            if (pex == kPredSplit) {
-                                record(path_code(kArcSplitFwd, kk, i, 0));
+                    int from = first ? predt : next_tie();
+                    int len = 0;
+                    bool okw = false;
+                    while (from >= 0) {
+                        int kk = S - 1, i = from;
+                        bool at_exit = true, blocked = false, done = false;
+                        okw = from < n;
+                        len = 0;
+                        auto record = [&](int code) {
+                            if (lane == 0) {
+                                if (len < kPathLds) lpath[len] = code;
+                                else st(&gp.path[len], code);
+                            }
+                            ++len;
+                        };
+                        // One read per node visited: a compute arc and the link arc
+                        // after it come from the same word (entry predecessor in the
+                        // low half, exit predecessor in the high half).  A compute
+                        // arc followed by the opposite one would be a cycle.
+                        while (okw && !done) {
+                            if (len > 2 * SN + 4) {
+                                okw = false;
+                                break;
+                            }
+                            const uint32_t word = __builtin_amdgcn_readfirstlane(uint32_t(all_pred[kk * n + i]));
+                            const int pen = int(word & 0x7fffu) - 3, pex = int((word >> 16) & 0x7fffu) - 3;
+                            const bool men = (word & 0x8000u) != 0, mex = (word >> 31) != 0;
+                            const bool ex_link = pex >= 0 && pex < n && kk + 1 < S;
+                            const bool en_link = pen >= 0 && pen < n && kk >= 1;
+                            if (at_exit) {
+                                if (mex) {
+                                    blocked = true;
+                                    break;
+                                }
+                                if (pex == kPredSplit) {
+                                    record(path_code(kArcSplitFwd, kk, i, 0));
+                                    if (men) {
+                                        blocked = true;
+                                        break;
+                                    }
+                                    if (pen == kPredSrc) {
+                                        done = true;
+                                    } else if (en_link) {
+                                        record(path_code(kArcLinkFwd, kk - 1, pen, i)); // exit (kk-1, pen) -> entry (kk, i)
+                                        kk = kk - 1;
+                                        i = pen;
+                                    } else {
+                                        okw = false;
+                                    }
+                                } else if (ex_link) {
+                                    record(path_code(kArcLinkRev, kk, i, pex)); // entry (kk+1, pex) -> exit (kk, i)
+                                    kk = kk + 1;
+                                    i = pex;
+                                    at_exit = false;
+                                } else {
+                                    okw = false;
+                                }
+                            } else {
+                                if (men) {
+                                    blocked = true;
+                                    break;
+                                }
                                 if (pen == kPredSrc) {
                                     done = true;
+                                } else if (pen == kPredSplit) {
+                                    record(path_code(kArcSplitRev, kk, i, 0));
+                                    if (mex) {
+                                        blocked = true;
+                                        break;
+                                    }
+                                    if (ex_link) {
+                                        record(path_code(kArcLinkRev, kk, i, pex)); // entry (kk+1, pex) -> exit (kk, i)
+                                        kk = kk + 1;
+                                        i = pex;
+                                    } else {
+                                        okw = false;
+                                    }
                                 } else if (en_link) {
                                     record(path_code(kArcLinkFwd, kk - 1, pen, i)); // exit (kk-1, pen) -> entry (kk, i)
                                     kk = kk - 1;
                                     i = pen;
+                                    at_exit = true;
                                 } else {
                                     okw = false;
                                 }
-                            } else if (ex_link) {
-                                record(path_code(kArcLinkRev, kk, i, pex)); // entry (kk+1, pex) -> exit (kk, i)
-                                kk = kk + 1;
-                                i = pex;
-                                at_exit = false;
-                            } else {
-                                okw = false;
-                            }
-                        } else {
-                            if (pen == kPredSrc) {
-                                done = true;
-                            } else if (pen == kPredSplit) {
-                                record(path_code(kArcSplitRev, kk, i, 0));
-                                if (ex_link) {
-                                    record(path_code(kArcLinkRev, kk, i, pex)); // entry (kk+1, pex) -> exit (kk, i)
-                                    kk = kk + 1;
-                                    i = pex;
-                                } else {
-                                    okw = false;
-                                }
-                            } else if (en_link) {
-                                record(path_code(kArcLinkFwd, kk - 1, pen, i)); // exit (kk-1, pen) -> entry (kk, i)
-                                kk = kk - 1;
-                                i = pen;
-                                at_exit = true;
-                            } else {
-                                okw = false;
                             }
                         }
+                        if (!blocked) break;
+                        from = next_tie();
                     }
                     if (lane == 0) {
-                        sh_len = okw ? len : -1;
+                        // length -2: no exit left to try
+                        sh_len = from < 0 ? -2 : (okw ? len : -1);
                         sh_delta = supply - int(F);
+                        sh_esat = -1;
                     }
                 }
                 __syncthreads();
                 const int len = sh_len;
+                // the bottleneck, and the path's saturated arc nearest the
+                // data node (path entries run from the sink back)
+                int rl = 0x7fffffff, el = -1;
                 if (len >= 0) {
-                    int r = 0x7fffffff;
                     for (int e = tid; e < len; e += kGridThreads) {
                         const int code = e < kPathLds ? lpath[e] : ld(&gp.path[e]);
                         if (e < kPathLds) st(&gp.path[e], code);
                         const int type = code_type(code), q = code_stage(code) * n + code_node(code);
-                        if (type == kArcSplitFwd) r = min(r, gcap[q] - ld(&gnf[q]));
-                        else if (type == kArcSplitRev) r = min(r, ld(&gnf[q]));
-                        else if (type == kArcLinkRev) r = min(r, ld(&gaf[size_t(q) * n + code_head(code)]));
+                        int res = 0x7fffffff;
+                        if (type == kArcSplitFwd) res = gcap[q] - ld(&gnf[q]);
+                        else if (type == kArcSplitRev) res = ld(&gnf[q]);
+                        else if (type == kArcLinkRev) res = ld(&gaf[size_t(q) * n + code_head(code)]);
+                        el = res <= rl ? e : el;
+                        rl = min(rl, res);
                     }
-                    atomicMin(&sh_delta, r);
+                    atomicMin(&sh_delta, rl);
                 }
                 __syncthreads();
+                if (len >= 0 && el >= 0 && rl == sh_delta) atomicMax(&sh_esat, el);
+                __syncthreads();
                 if (tid == 0) {
-                    // length -2: no exit left to try
+                    int more = 0;
+                    for (int w = 0; w < kGridMaxNodes / 32; ++w) more |= sh_ties[w] != 0;
                     st(&ctrl[kCtlDelta], len < 0 ? -1 : sh_delta);
-                    st(&ctrl[kCtlLen], from < 0 ? -2 : len);
+                    st(&ctrl[kCtlLen], len);
+                    st(&ctrl[kCtlMore], more);
                 }
             }
             if (!bar.sync(&sh_ok, &sh_flag)) {
@@ -834,7 +890,7 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
             }
 
             // ---- (4) owners apply the augmentation: decrements, then increments ----
-            const int delta = ld(&ctrl[kCtlDelta]), len = ld(&ctrl[kCtlLen]);
+            const int delta = ld(&ctrl[kCtlDelta]), len = ld(&ctrl[kCtlLen]), more = ld(&ctrl[kCtlMore]);
             if (!first && len == -2) break;
             if (len < 0 || len > 2 * SN + 5 || (first && delta <= 0)) {
                 if (tid == 0) sh_fault = 1;
@@ -904,24 +960,26 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
             cost += (long long)delta * Dt;
             augs++;
             }
+            if (g == 0 && delta > 0) {
+                // mark the path's vertices from the sink back to the head of
+                // its saturated arc nearest the data node
+                const int esat = sh_esat;
+                for (int e = tid; e <= esat; e += kGridThreads) {
+                    const int code = e < kPathLds ? reinterpret_cast<int *>(red)[e] : ld(&gp.path[e]);
+                    const int type = code_type(code), kk = code_stage(code), i = code_node(code), j = code_head(code);
+                    if (type == kArcSplitFwd) atomicOr(reinterpret_cast<unsigned *>(&all_pred[kk * n + i]), 0x80000000u);
+                    else if (type == kArcSplitRev) atomicOr(reinterpret_cast<unsigned *>(&all_pred[kk * n + i]), 0x8000u);
+                    else if (type == kArcLinkFwd) atomicOr(reinterpret_cast<unsigned *>(&all_pred[(kk + 1) * n + j]), 0x8000u);
+                    else atomicOr(reinterpret_cast<unsigned *>(&all_pred[kk * n + i]), 0x80000000u);
+                }
+            }
             first = false;
-            if (F >= supply) break;
+            if (F >= supply || !more) break;
             // the applied flows are visible to workgroup 0's next bottleneck
             if (!bar.sync(&sh_ok, &sh_flag)) {
                 timed_out = true;
                 quit = true;
                 break;
-            }
-            if (g == 0 && tid == 0) {
-                int nx = -1;
-                for (int w = 0; w < kGridMaxNodes / 32 && nx < 0; ++w) {
-                    if (sh_ties[w]) {
-                        const int bit = __builtin_ctz(sh_ties[w]);
-                        sh_ties[w] &= sh_ties[w] - 1;
-                        nx = w * 32 + bit;
-                    }
-                }
-                sh_from = nx;
             }
             }
             if (quit) break;
