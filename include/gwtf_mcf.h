@@ -47,7 +47,9 @@ typedef enum {
 enum {
     GWTF_INST_OK = 0,
     GWTF_INST_BAD_INPUT = 1, /* a capacity, cost or supply < 0, or an arc cost < -1 */
-    GWTF_INST_OVERFLOW = 2   /* (2*S*n + 3) * max cost >= 2^29: labels could leave int32 */
+    GWTF_INST_OVERFLOW = 2,  /* (2*S*n + 3) * max cost >= 2^29: labels could leave int32 */
+    GWTF_INST_NOT_CONVERGED = 3 /* churn re-solve only: stopped at its safety limit of 2^20
+                                   label-correcting rounds (not expected on valid input) */
 };
 
 /* Solver pass that produced an instance's result (gwtf_mcf_get_passes). */
@@ -237,6 +239,49 @@ gwtf_status_t gwtf_mcf_whatif_expand(gwtf_mcf_t *h, const gwtf_mcf_batch_t *base
 gwtf_status_t gwtf_mcf_whatif_best(gwtf_mcf_t *h, int32_t count, const int64_t *flow_value,
                                    const int64_t *total_cost, const int32_t *status, int64_t first,
                                    int32_t merge, int64_t *best);
+
+/* ---- Warm-started re-solve after churn (paper Sec. VI: nodes leave and
+ * link delays change between iterations, and the flow problem is solved
+ * again on the changed instance) ----
+ *
+ * Solves every instance of `b` (same layout, checks and per-instance status
+ * as gwtf_mcf_solve_batch; b->batch <= max_batch) starting from a feasible
+ * flow of the same shape instead of from zero, typically the optimum of the
+ * instance before the churn as returned by gwtf_mcf_get_flows.  The result
+ * (F, cost) equals a cold solve's: the start flow loses whole source-to-sink
+ * paths until it respects the new capacities, the missing links and the
+ * supply; negative residual cycles are cancelled (the flow is then of least
+ * cost for its value); shortest augmenting paths finish the solve.
+ *
+ * The start flow is in the layout of gwtf_mcf_get_flows: node_flow
+ * [.][S][n], arc_flow [.][S-1][n][n] (NULL iff S == 1), src_flow and
+ * snk_flow [.][n], with one entry for the whole batch when per_instance == 0
+ * and one per instance otherwise.  It must be conserved (a node's flow equals
+ * its inflow and its outflow; stage 0 is fed by src_flow, stage S-1 drains
+ * into snk_flow) with every value in [0, 2^29); otherwise the instance gets
+ * GWTF_INST_BAD_INPUT.  Its capacities and links need not match the new
+ * instance. */
+typedef struct {
+    const int32_t *node_flow, *arc_flow, *src_flow, *snk_flow;
+    int32_t per_instance;
+} gwtf_mcf_flow_in_t;
+
+/* Caller device buffers for result flows of `batch` instances, in the same
+ * layout (arc_flow NULL iff S == 1). */
+typedef struct {
+    int32_t *node_flow, *arc_flow, *src_flow, *snk_flow;
+} gwtf_mcf_flow_out_t;
+
+/* One workgroup per instance holds the instance in LDS: requires S*n <= 512
+ * and (S-1)*n*n <= 4096 (GWTF_ERR_INVALID_ARG otherwise, nothing enqueued).
+ * `out` may be NULL (no flows written; an instance that is not OK gets zero
+ * flows).  `work` (device int64 [batch][4], or NULL) receives per instance
+ * the paths removed, cycles cancelled, augmentations and label-correcting
+ * rounds.  Uses no handle workspace: gwtf_mcf_get_flows keeps referring to
+ * the last gwtf_mcf_solve_batch.  Enqueued on the handle's stream. */
+gwtf_status_t gwtf_mcf_resolve_churn(gwtf_mcf_t *h, const gwtf_mcf_batch_t *b,
+                                     const gwtf_mcf_flow_in_t *start,
+                                     const gwtf_mcf_flow_out_t *out, int64_t *work);
 
 /* Frees the handle and its workspace after draining its stream; NULL-safe. */
 void gwtf_mcf_destroy(gwtf_mcf_t *h);

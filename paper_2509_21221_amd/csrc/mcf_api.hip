@@ -531,3 +531,55 @@ extern "C" gwtf_status_t gwtf_mcf_whatif_best(gwtf_mcf_t *h, int32_t count, cons
         return hip_fail(h, e, "what-if best launch");
     return GWTF_OK;
 }
+
+extern "C" gwtf_status_t gwtf_mcf_resolve_churn(gwtf_mcf_t *h, const gwtf_mcf_batch_t *b,
+                                                const gwtf_mcf_flow_in_t *start,
+                                                const gwtf_mcf_flow_out_t *out, int64_t *work)
+{
+    if (!h) return fail(nullptr, GWTF_ERR_INVALID_ARG, "handle is NULL");
+    if (!b || !start) return fail(h, GWTF_ERR_INVALID_ARG, "batch or start flow is NULL");
+    const int S = h->shape.num_stages, n = h->shape.nodes_per_stage;
+    if (int64_t(S) * n > kChurnMaxNodes || int64_t(S - 1) * n * n > kChurnMaxLinks)
+        return fail(h, GWTF_ERR_INVALID_ARG, "churn re-solve needs S*n <= 512 and (S-1)*n*n <= 4096");
+    if (b->batch < 1 || b->batch > h->shape.max_batch)
+        return fail(h, GWTF_ERR_INVALID_ARG, "batch outside [1, max_batch]");
+    if (!b->node_cap || !b->node_cost || !b->supply || !b->flow_value || !b->total_cost || !b->status)
+        return fail(h, GWTF_ERR_INVALID_ARG, "required pointer is NULL");
+    if ((S > 1) != (b->arc_cost != nullptr))
+        return fail(h, GWTF_ERR_INVALID_ARG, "arc_cost must be non-NULL exactly when S > 1");
+    if (!start->node_flow || !start->src_flow || !start->snk_flow || (S > 1) != (start->arc_flow != nullptr))
+        return fail(h, GWTF_ERR_INVALID_ARG,
+                    "start flow needs node_flow, src_flow, snk_flow, and arc_flow exactly when S > 1");
+    if (out && (!out->node_flow || !out->src_flow || !out->snk_flow || (S > 1) != (out->arc_flow != nullptr)))
+        return fail(h, GWTF_ERR_INVALID_ARG,
+                    "result flows need node_flow, src_flow, snk_flow, and arc_flow exactly when S > 1");
+    hipError_t e = hipSetDevice(h->shape.device);
+    if (e != hipSuccess) return hip_fail(h, e, "hipSetDevice");
+    ChurnParams p{};
+    p.B = b->batch;
+    p.S = S;
+    p.n = n;
+    p.start_per_instance = start->per_instance != 0;
+    p.cap = b->node_cap;
+    p.ncost = b->node_cost;
+    p.acost = b->arc_cost;
+    p.src = b->src_cost;
+    p.snk = b->snk_cost;
+    p.supply = b->supply;
+    p.nf0 = start->node_flow;
+    p.af0 = start->arc_flow;
+    p.sf0 = start->src_flow;
+    p.tf0 = start->snk_flow;
+    p.F_out = b->flow_value;
+    p.cost_out = b->total_cost;
+    p.status_out = b->status;
+    if (out) {
+        p.nf_out = out->node_flow;
+        p.af_out = out->arc_flow;
+        p.sf_out = out->src_flow;
+        p.tf_out = out->snk_flow;
+    }
+    p.work = work;
+    if ((e = launch_churn_resolve(p, h->stream)) != hipSuccess) return hip_fail(h, e, "churn re-solve launch");
+    return GWTF_OK;
+}

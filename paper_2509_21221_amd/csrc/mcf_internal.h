@@ -116,4 +116,21 @@ hipError_t launch_located_expand(int32_t B, int32_t S, int32_t n, int32_t L, con
 int fallback_waves();
 hipError_t set_lds_limits(size_t max_bytes);
 
+// Warm-started re-solve of churn variants (mcf_churn.hip): one workgroup per
+// instance with the instance in LDS, so S*n <= kChurnMaxNodes and
+// (S-1)*n*n <= kChurnMaxLinks.
+constexpr int kChurnMaxNodes = 512;
+constexpr int kChurnMaxLinks = 4096;
+struct ChurnParams {
+    int32_t B, S, n, start_per_instance;
+    const int32_t *cap, *ncost, *acost, *src, *snk, *supply; // caller inputs
+    const int32_t *nf0, *af0, *sf0, *tf0;                    // start flow ([B] or [1])
+    int64_t *F_out, *cost_out;                               // [B]
+    int32_t *status_out;                                     // [B]
+    int32_t *nf_out, *af_out, *sf_out, *tf_out;              // result flows, or all NULL
+    int64_t *work;                                           // [B][4] or NULL
+};
+size_t churn_lds_bytes(int S, int n);
+hipError_t launch_churn_resolve(const ChurnParams &p, hipStream_t stream);
+
 } // namespace gwtf

@@ -4,6 +4,7 @@ marshalling only -- every step of the solve runs in the HIP library).
 The functions carry the C names (``gwtf_mcf_create``, ``gwtf_mcf_solve_batch``,
 ``gwtf_mcf_get_flows``, ``gwtf_mcf_get_stats``, ``gwtf_mcf_get_passes``,
 ``gwtf_mcf_solve_located``, ``gwtf_whatif_count``, ``gwtf_mcf_whatif_expand``, ``gwtf_mcf_whatif_best``,
+``gwtf_mcf_resolve_churn``,
 ``gwtf_mcf_destroy``, ``gwtf_mcf_last_error``); ``Solver`` wraps them for
 torch device tensors.
 PyTorch only provides device memory and the HIP stream.
@@ -29,6 +30,8 @@ GWTF_ERR_RANGE = 5
 GWTF_INST_OK = 0
 GWTF_INST_BAD_INPUT = 1
 GWTF_INST_OVERFLOW = 2
+GWTF_INST_NOT_CONVERGED = 3
+CHURN_WORK_PER_INSTANCE = 4
 GWTF_NO_ARC = -1
 STATS_PER_INSTANCE = 10
 GWTF_PASS_REGISTER = 1
@@ -77,6 +80,17 @@ class gwtf_mcf_instances_t(ctypes.Structure):
                 ("snk_cost", ctypes.c_void_p), ("supply", ctypes.c_void_p)]
 
 
+class gwtf_mcf_flow_in_t(ctypes.Structure):
+    _fields_ = [("node_flow", ctypes.c_void_p), ("arc_flow", ctypes.c_void_p),
+                ("src_flow", ctypes.c_void_p), ("snk_flow", ctypes.c_void_p),
+                ("per_instance", ctypes.c_int32)]
+
+
+class gwtf_mcf_flow_out_t(ctypes.Structure):
+    _fields_ = [("node_flow", ctypes.c_void_p), ("arc_flow", ctypes.c_void_p),
+                ("src_flow", ctypes.c_void_p), ("snk_flow", ctypes.c_void_p)]
+
+
 class GwtfError(RuntimeError):
     def __init__(self, code, msg):
         super().__init__(f"{STATUS_NAMES.get(code, code)}: {msg}")
@@ -119,6 +133,10 @@ def load_library(path: str = LIB_PATH):
         lib.gwtf_mcf_whatif_expand.restype = ctypes.c_int
         lib.gwtf_mcf_whatif_best.argtypes = [vp, i32, vp, vp, vp, ctypes.c_int64, i32, vp]
         lib.gwtf_mcf_whatif_best.restype = ctypes.c_int
+        lib.gwtf_mcf_resolve_churn.argtypes = [vp, ctypes.POINTER(gwtf_mcf_batch_t),
+                                               ctypes.POINTER(gwtf_mcf_flow_in_t),
+                                               ctypes.POINTER(gwtf_mcf_flow_out_t), vp]
+        lib.gwtf_mcf_resolve_churn.restype = ctypes.c_int
         lib.gwtf_mcf_destroy.argtypes = [vp]
         lib.gwtf_mcf_destroy.restype = None
         lib.gwtf_mcf_last_error.argtypes = [vp]
@@ -213,6 +231,24 @@ def gwtf_mcf_whatif_best(handle, count: int, flow_value: int, total_cost: int, s
                                                best or None), handle)
 
 
+def gwtf_mcf_resolve_churn(handle, batch: int, node_cap: int, node_cost: int, arc_cost: int,
+                           src_cost: int, snk_cost: int, supply: int, flow_value: int,
+                           total_cost: int, status: int, start: dict, per_instance: bool,
+                           out: dict | None = None, work: int = 0) -> None:
+    """Device addresses as for ``gwtf_mcf_solve_batch``; ``start`` (and
+    ``out``, if given) map node_flow, arc_flow, src_flow, snk_flow to device
+    addresses (0 = NULL)."""
+    b = gwtf_mcf_batch_t(batch, node_cap or None, node_cost or None, arc_cost or None,
+                         src_cost or None, snk_cost or None, supply or None, flow_value or None,
+                         total_cost or None, status or None)
+    keys = ("node_flow", "arc_flow", "src_flow", "snk_flow")
+    st = gwtf_mcf_flow_in_t(*[start.get(k) or None for k in keys], int(bool(per_instance)))
+    o = gwtf_mcf_flow_out_t(*[out.get(k) or None for k in keys]) if out is not None else None
+    _check(load_library().gwtf_mcf_resolve_churn(ctypes.c_void_p(handle), ctypes.byref(b), ctypes.byref(st),
+                                                 ctypes.byref(o) if o is not None else None,
+                                                 ctypes.c_void_p(work or None)), handle)
+
+
 def gwtf_mcf_destroy(handle) -> None:
     load_library().gwtf_mcf_destroy(ctypes.c_void_p(handle))
 
@@ -292,6 +328,51 @@ class Solver:
         gwtf_mcf_solve_located(self.handle, B, L, *args, F.data_ptr(), cost.data_ptr(), status.data_ptr())
         self.last_batch = B
         return F, cost, status
+
+    def resolve_churn(self, node_cap, node_cost, arc_cost, supply, start, src_cost=None, snk_cost=None,
+                      flows=False, work=False):
+        """Warm-started solve of a batch from ``start`` (a dict of int32 device
+        tensors node_flow, arc_flow, src_flow, snk_flow with a leading
+        dimension of 1 for one flow shared by the batch, or B).  Returns
+        (F, cost, status) and, when asked, a dict of result flows and the
+        [B][4] work counters."""
+        torch = self.torch
+        S, n = self.S, self.n
+        B = int(supply.shape[0])
+        args = [self._arg(node_cap, (B, S, n), "node_cap"), self._arg(node_cost, (B, S, n), "node_cost"),
+                self._arg(arc_cost, (B, S - 1, n, n), "arc_cost") if S > 1 else 0,
+                self._arg(src_cost, (B, n), "src_cost"), self._arg(snk_cost, (B, n), "snk_cost"),
+                self._arg(supply, (B,), "supply")]
+        if S > 1 and arc_cost is None:
+            raise ValueError("arc_cost is required when S > 1")
+        m = int(start["node_flow"].shape[0])
+        if m not in (1, B):
+            raise ValueError("start flow: leading dimension must be 1 or the batch size")
+        shapes = {"node_flow": (m, S, n), "arc_flow": (m, S - 1, n, n), "src_flow": (m, n), "snk_flow": (m, n)}
+        st = {k: (self._arg(start[k], shp, "start " + k) if (k != "arc_flow" or S > 1) else 0)
+              for k, shp in shapes.items()}
+        dev = torch.device("cuda", self.device)
+        F = torch.empty(B, dtype=torch.int64, device=dev)
+        cost = torch.empty(B, dtype=torch.int64, device=dev)
+        status = torch.empty(B, dtype=torch.int32, device=dev)
+        out = None
+        if flows:
+            out = {"node_flow": torch.empty((B, S, n), dtype=torch.int32, device=dev),
+                   "arc_flow": torch.empty((B, max(S - 1, 0), n, n), dtype=torch.int32, device=dev),
+                   "src_flow": torch.empty((B, n), dtype=torch.int32, device=dev),
+                   "snk_flow": torch.empty((B, n), dtype=torch.int32, device=dev)}
+        wk = torch.empty((B, CHURN_WORK_PER_INSTANCE), dtype=torch.int64, device=dev) if work else None
+        gwtf_mcf_resolve_churn(self.handle, B, *args, F.data_ptr(), cost.data_ptr(), status.data_ptr(), st,
+                               m == B and B > 1,
+                               {k: (v.data_ptr() if (k != "arc_flow" or S > 1) else 0) for k, v in out.items()}
+                               if out is not None else None,
+                               wk.data_ptr() if wk is not None else 0)
+        res = (F, cost, status)
+        if flows:
+            res = res + (out,)
+        if work:
+            res = res + (wk,)
+        return res
 
     def flows(self, first: int = 0, count: int | None = None):
         torch = self.torch

@@ -1,0 +1,183 @@
+"""GPU parity of the warm-started churn re-solve (paper Sec. VI: the flow
+problem is solved again after nodes leave and link delays change) through
+the C ABI, against the oracle's cold solve of the changed instances.
+
+(F, cost, status) must match the oracle exactly.  The returned flows must
+pass the optimality certificate under the oracle's potentials: any optimal
+dual is complementary to every optimal flow of the same value, so a
+different but equally optimal flow passes too.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2509_21221_amd import mcf
+from paper_2509_21221_amd import workloads as W
+from mcf_checks import certify
+
+pytestmark = pytest.mark.gpu
+FLOW_KEYS = ("node_flow", "arc_flow", "src_flow", "snk_flow")
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def _t(a):
+    import torch
+
+    return torch.from_numpy(np.ascontiguousarray(a)).to(torch.device("cuda", 0))
+
+
+def churn(batch, start, flows=True):
+    """Run the warm-started re-solve of ``batch`` from ``start`` (numpy
+    arrays with a leading dimension of 1, shared, or B) on cuda:0."""
+    import torch
+
+    with mcf.Solver(batch.S, batch.n, batch.B) as s:
+        st = {k: _t(start[k]) for k in FLOW_KEYS}
+        res = s.resolve_churn(_t(batch.node_cap), _t(batch.node_cost),
+                              _t(batch.arc_cost) if batch.S > 1 else None, _t(batch.supply), st,
+                              _t(batch.src_cost), _t(batch.snk_cost), flows=flows, work=True)
+        torch.cuda.synchronize()
+    F, cost, status = (x.cpu().numpy() for x in res[:3])
+    out = {k: v.cpu().numpy() for k, v in res[3].items()} if flows else None
+    return F, cost, status, out, res[-1].cpu().numpy()
+
+
+def check(batch, F, cost, status, out, ref, certify_first=8):
+    np.testing.assert_array_equal(status, ref["status"])
+    np.testing.assert_array_equal(F, ref["F"])
+    np.testing.assert_array_equal(cost, ref["cost"])
+    if out is None:
+        return
+    for b in range(min(certify_first, batch.B)):
+        if status[b] != 0:
+            continue
+        certify(batch, b, int(F[b]), int(cost[b]), out["node_flow"][b], out["arc_flow"][b],
+                out["src_flow"][b], out["snk_flow"][b], ref["potential"][b])
+
+
+def test_churn_variants_from_base_optimum():
+    """Churn variants of a base instance (8 x 8, 10-30 % of nodes deleted,
+    delays jittered), each re-solved from the base's optimal flow."""
+    base = W.config2(1, 0)
+    var = W.config3(512, 0)
+    say("churn: 512 variants of the 8x8 base, start = oracle optimum of the base")
+    b0 = oracle.solve(base)
+    start = {k: b0[k][:1] for k in FLOW_KEYS}
+    F, cost, status, out, work = churn(var, start)
+    check(var, F, cost, status, out, oracle.solve(var), certify_first=32)
+    assert (work[:, 0] > 0).any()          # deleted nodes carried flow
+    assert (work[:, 1] >= 0).all() and (work[:, 3] > 0).all()
+
+
+def test_churn_from_gpu_base_flows():
+    """The start flow comes from the GPU's own cold solve of the base."""
+    import torch
+
+    base = W.config2(1, 0)
+    var = W.config3(2048, 512)
+    say("churn: 2048 variants, start = GPU cold solve of the base")
+    with mcf.Solver(base.S, base.n, 1) as s:
+        s.solve(_t(base.node_cap), _t(base.node_cost), _t(base.arc_cost), _t(base.supply),
+                _t(base.src_cost), _t(base.snk_cost))
+        fl = {k: v.cpu().numpy()[:1] for k, v in s.flows().items() if k in FLOW_KEYS}
+        torch.cuda.synchronize()
+    F, cost, status, out, _ = churn(var, fl)
+    check(var, F, cost, status, out, oracle.solve(var))
+
+
+SHAPES = [(1, 5), (2, 3), (3, 4), (5, 8), (8, 8), (4, 16), (2, 64), (16, 5), (64, 2), (8, 24)]
+
+
+@pytest.mark.parametrize("S,n", SHAPES)
+def test_churn_from_unrelated_optimum(S, n):
+    """Start from the optimum of an unrelated instance of the same shape (new
+    capacities, costs, holes, deleted nodes and supply)."""
+    B = 160
+    prev = W.random_small(B, S, n, seed=71, cap_hi=4, cost_hi=25, supply_hi=12)
+    var = W.random_small(B, S, n, seed=72, cap_hi=4, cost_hi=25, supply_hi=12, holes=0.2, zero_cap=0.2)
+    say(f"churn: S={S} n={n} B={B} from unrelated optima")
+    p = oracle.solve(prev)
+    F, cost, status, out, _ = churn(var, {k: p[k] for k in FLOW_KEYS})
+    check(var, F, cost, status, out, oracle.solve(var))
+
+
+@pytest.mark.parametrize("S,n", [(3, 4), (8, 8), (2, 64)])
+def test_churn_from_zero_flow(S, n):
+    """A zero start flow makes the re-solve a cold solve."""
+    B = 128
+    var = W.random_small(B, S, n, seed=73, cap_hi=3, cost_hi=40, supply_hi=10, holes=0.1)
+    say(f"churn: S={S} n={n} from zero flow")
+    z = {"node_flow": np.zeros((1, S, n), np.int32), "arc_flow": np.zeros((1, max(S - 1, 0), n, n), np.int32),
+         "src_flow": np.zeros((1, n), np.int32), "snk_flow": np.zeros((1, n), np.int32)}
+    F, cost, status, out, work = churn(var, z)
+    check(var, F, cost, status, out, oracle.solve(var))
+    assert (work[:, 0] == 0).all() and (work[:, 1] == 0).all()
+
+
+def test_churn_bad_start_and_bad_values():
+    """A start flow that is not conserved, a negative start value and a
+    negative capacity give GWTF_INST_BAD_INPUT with F = cost = 0 and zero
+    flows; the other instances are unaffected; a cost that lets labels leave
+    int32 gives GWTF_INST_OVERFLOW, as in the cold solve (the int64 oracle
+    has no such limit)."""
+    S, n, B = 4, 6, 8
+    prev = W.random_small(B, S, n, seed=74, cap_hi=4, supply_hi=12)
+    var = W.random_small(B, S, n, seed=75, cap_hi=4, supply_hi=12)
+    p = oracle.solve(prev)
+    start = {k: p[k].copy() for k in FLOW_KEYS}
+    nz = np.argwhere(start["arc_flow"][1] > 0)
+    assert len(nz), "instance 1 of the start batch carries no flow"
+    k, i, j = nz[0]
+    start["arc_flow"][1, k, i, j] -= 1                 # breaks conservation
+    start["src_flow"][2, 0] = -1                       # negative value
+    var.node_cap[3, 1, 2] = -1                         # negative capacity
+    var.node_cost[4, 0, 0] = 1 << 26                   # (2Sn+3) * max cost >= 2^29
+    say("churn: bad start flows and bad values")
+    F, cost, status, out, _ = churn(var, start)
+    ref = oracle.solve(var)
+    assert list(status[1:5]) == [mcf.GWTF_INST_BAD_INPUT] * 3 + [mcf.GWTF_INST_OVERFLOW]
+    assert ref["status"][3] == mcf.GWTF_INST_BAD_INPUT
+    for b in (1, 2, 3, 4):
+        assert F[b] == 0 and cost[b] == 0
+        assert all(not out[k][b].any() for k in FLOW_KEYS)
+    keep = [0, 5, 6, 7]
+    np.testing.assert_array_equal(status[keep], ref["status"][keep])
+    np.testing.assert_array_equal(F[keep], ref["F"][keep])
+    np.testing.assert_array_equal(cost[keep], ref["cost"][keep])
+
+
+def test_churn_supply_drop_and_missing_links():
+    """The new supply is below the start value and links that carried flow
+    are gone (GWTF_NO_ARC)."""
+    S, n, B = 6, 8, 128
+    prev = W.random_small(B, S, n, seed=76, cap_hi=5, cost_hi=30, supply_hi=30)
+    p = oracle.solve(prev)
+    var = W.random_small(B, S, n, seed=76, cap_hi=5, cost_hi=30, supply_hi=30)
+    rng = np.random.default_rng(77)
+    var.supply[:] = (p["F"] * rng.uniform(0.0, 1.0, B)).astype(np.int32)
+    used = p["arc_flow"] > 0
+    var.arc_cost[used & (rng.random(used.shape) < 0.5)] = W.NO_ARC
+    say("churn: supply drop and missing links")
+    F, cost, status, out, work = churn(var, {k: p[k] for k in FLOW_KEYS})
+    check(var, F, cost, status, out, oracle.solve(var))
+    assert (work[:, 0] > 0).any()
+
+
+def test_churn_argument_errors():
+    import torch
+
+    with mcf.Solver(2, 65, 4) as s:                    # (S-1) n^2 > 4096
+        z = {k: _t(np.zeros(shp, np.int32)) for k, shp in
+             {"node_flow": (1, 2, 65), "arc_flow": (1, 1, 65, 65), "src_flow": (1, 65),
+              "snk_flow": (1, 65)}.items()}
+        with pytest.raises(mcf.GwtfError) as e:
+            s.resolve_churn(_t(np.ones((4, 2, 65), np.int32)), _t(np.ones((4, 2, 65), np.int32)),
+                            _t(np.ones((4, 1, 65, 65), np.int32)), _t(np.ones(4, np.int32)), z)
+        assert e.value.code == mcf.GWTF_ERR_INVALID_ARG
+    torch.cuda.synchronize()
