@@ -460,7 +460,11 @@ size_t churn_lds_bytes(int S, int n)
 
 hipError_t launch_churn_resolve(const ChurnParams &p, hipStream_t stream)
 {
-    hipLaunchKernelGGL(churn_kernel, dim3(p.B), dim3(kChurnThreads), churn_lds_bytes(p.S, p.n), stream, p);
+    // A single wave for small instances: its barriers cost next to nothing
+    // and more instances share a CU.
+    const int V = 2 * p.S * p.n + 2;
+    const int threads = V <= 192 ? 64 : kChurnThreads;
+    hipLaunchKernelGGL(churn_kernel, dim3(p.B), dim3(threads), churn_lds_bytes(p.S, p.n), stream, p);
     return hipGetLastError();
 }
 
