@@ -60,6 +60,8 @@ def test_null_handle_calls_fail_cleanly():
     assert lib.gwtf_mcf_get_passes(None, 0, 1, None) == mcf.GWTF_ERR_INVALID_ARG
     assert lib.gwtf_mcf_whatif_expand(None, None, None, 0, 1, None) == mcf.GWTF_ERR_INVALID_ARG
     assert lib.gwtf_mcf_whatif_best(None, 1, None, None, None, 0, 0, None) == mcf.GWTF_ERR_INVALID_ARG
+    assert lib.gwtf_mcf_resolve_churn(None, None, None, None, None) == mcf.GWTF_ERR_INVALID_ARG
+    assert "handle" in mcf.gwtf_mcf_last_error(None)
     lib.gwtf_mcf_destroy(None)
     out = ctypes.c_void_p(1)
     assert lib.gwtf_mcf_create(None, None, ctypes.byref(out)) == mcf.GWTF_ERR_INVALID_ARG
