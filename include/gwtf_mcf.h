@@ -130,6 +130,31 @@ gwtf_status_t gwtf_mcf_get_stats(gwtf_mcf_t *h, int32_t first, int32_t count, in
  * handle's stream; errors as for gwtf_mcf_get_stats. */
 gwtf_status_t gwtf_mcf_get_passes(gwtf_mcf_t *h, int32_t first, int32_t count, int32_t *pass);
 
+/* ---- Solve without allocation ----
+ *
+ * For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  The same
+ * solve as gwtf_mcf_solve_batch (same passes, checks, per-instance status and
+ * outputs), with no handle: every workspace buffer lives in one fixed array
+ * of 64 MiB per device, declared in the library, that each device holds from
+ * the first call on it until the process ends.  The call allocates nothing
+ * (no hipMalloc, hipFree or other allocating routine).
+ *
+ * `shape` gives S, n and the device (max_batch bounds b->batch as for a
+ * handle); the batch and its outputs are as for gwtf_mcf_solve_batch, on the
+ * HIP stream `hip_stream` (NULL = the device's null stream).  A batch whose
+ * workspace does not fit in the array gives GWTF_ERR_INVALID_ARG with nothing
+ * enqueued, and gwtf_mcf_last_error(NULL) names the bytes it needs: about
+ * 6,600 instances of 8 x 8 or 34 of 32 x 64 fit (larger batches are solved
+ * in slices), and one 64 x 512 instance (about 223 MiB) does not.  Every call on a device shares that device's array and
+ * leaves its contents behind: calls that overlap in time on one device (two
+ * streams, or two host threads) race and give wrong results, so they must be
+ * serialised by the caller.  Flows, stats and passes of these solves are
+ * not kept (gwtf_mcf_get_flows needs a handle).  Errors are reported through
+ * gwtf_mcf_last_error(NULL) of the calling thread. */
+gwtf_status_t gwtf_mcf_solve_batch_noalloc(const gwtf_mcf_shape_t *shape, void *hip_stream,
+                                           const gwtf_mcf_batch_t *b);
+
 /* ---- Location-factored instances (paper Sec. VI testbed: every node sits at
  * one of a few geographic locations, and Eq. 1's link term is the latency
  * between the two nodes' locations) ----
@@ -287,7 +312,9 @@ gwtf_status_t gwtf_mcf_resolve_churn(gwtf_mcf_t *h, const gwtf_mcf_batch_t *b,
 void gwtf_mcf_destroy(gwtf_mcf_t *h);
 
 /* Text of the last error on this handle ("" if none); NULL handle gives the
- * last create error of the calling thread. */
+ * last error of a call made without a handle (gwtf_mcf_create,
+ * gwtf_mcf_solve_batch_noalloc, or one given a NULL handle) on the calling
+ * thread. */
 const char *gwtf_mcf_last_error(const gwtf_mcf_t *h);
 
 #ifdef __cplusplus

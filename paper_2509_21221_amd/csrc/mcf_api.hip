@@ -13,18 +13,19 @@
 #include <algorithm>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 
 using namespace gwtf;
 
-struct gwtf_mcf {
-    gwtf_mcf_shape_t shape;
-    hipStream_t stream;
-    std::string err;
-    size_t lds_max;
-    int clock_khz = 0;
-    // workspace
+namespace {
+
+// Device buffers the passes write besides the caller's outputs: routes,
+// flows, potentials and counters of every instance, the fallback pass's
+// per-instance state, and the grid pass's label words, predecessors, path
+// and control block.
+struct Workspace {
     int32_t *route = nullptr, *node_flow = nullptr, *arc_flow = nullptr, *pot = nullptr;
     int64_t *stats = nullptr;
     unsigned char *state = nullptr;
@@ -37,18 +38,110 @@ struct gwtf_mcf {
     uint32_t *g_ex = nullptr, *g_en = nullptr, *g_ring = nullptr;
     unsigned long long *g_ring_key = nullptr;
     int32_t *g_pred = nullptr, *g_path = nullptr, *g_ctrl = nullptr;
+};
+
+// Device properties the pass choice depends on.
+struct DeviceInfo {
+    size_t lds_max = 0;
+    int clock_khz = 0;
+    int coop = 0;
+    int cus = 0;
+};
+
+// Queries `device` (which must be current) and raises the kernels' dynamic
+// LDS ceilings.  No allocation.
+hipError_t query_device(int device, DeviceInfo &d)
+{
+    int lds = 0;
+    hipError_t e = hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerBlock, device);
+    if (e != hipSuccess) return e;
+    d.lds_max = size_t(lds);
+    if (hipDeviceGetAttribute(&d.clock_khz, hipDeviceAttributeWallClockRate, device) != hipSuccess) d.clock_khz = 0;
+    if (hipDeviceGetAttribute(&d.coop, hipDeviceAttributeCooperativeLaunch, device) != hipSuccess) d.coop = 0;
+    if (hipDeviceGetAttribute(&d.cus, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess) d.cus = 0;
+    (void)hipGetLastError();
+    // Raising the per-kernel dynamic-LDS ceiling is not needed on every
+    // runtime (some reject the attribute); failure is harmless, but its error
+    // must not linger where a later launch check would read it.
+    if (set_lds_limits(d.lds_max) != hipSuccess) (void)hipGetLastError();
+    return hipSuccess;
+}
+
+// Sizes the workspace of up to B instances of S x n (pointers stay NULL):
+// fallback state for the worst case (every exit vertex may need
+// min(cap, n, supply) <= n flow-list entries), and the grid pass when its
+// S * ceil(n / 128) workgroups can all be resident at once (cooperative
+// launch, one per CU given their LDS).
+void plan_workspace(Workspace &w, int S, int n, const DeviceInfo &d)
+{
+    w.fallback_slots = int64_t(std::max(S - 1, 0)) * n * n;
+    w.state_stride = align16(make_layout(S, n, w.fallback_slots, false).total);
+    w.grid = false;
+    if (n > 64 && n <= kGridMaxNodes && S <= 1024 && d.coop && d.cus > 0) {
+        const int64_t slots = grid_pass_list_slots(S, n, d.lds_max);
+        if (slots >= 64) {
+            const size_t lds = grid_pass_lds_bytes(S, n, slots);
+            const int per_cu = grid_pass_blocks_per_cu(lds);
+            if (per_cu >= 1 && int64_t(S) * grid_pass_slices(n) <= int64_t(per_cu) * d.cus) {
+                w.grid = true;
+                w.grid_slots = slots;
+                w.grid_lds = lds;
+            }
+        }
+    }
+}
+
+// Calls f(&buffer_pointer, bytes) for every workspace buffer of B instances
+// (bytes may be 0: the buffer is not used).
+template <class Fn>
+void for_each_buffer(Workspace &w, int S, int n, int B, Fn f)
+{
+    const size_t SN = size_t(S) * n, V = 2 * SN + 3, na = size_t(std::max(S - 1, 0)) * n * n;
+    const size_t gsn = w.grid ? SN : 0;
+    f((void **)&w.route, sizeof(int32_t) * B);
+    f((void **)&w.node_flow, sizeof(int32_t) * SN * B);
+    f((void **)&w.arc_flow, sizeof(int32_t) * std::max<size_t>(na, 1) * B);
+    f((void **)&w.pot, sizeof(int32_t) * V * B);
+    f((void **)&w.stats, sizeof(int64_t) * kStatsPerInstance * B);
+    f((void **)&w.state, w.state_stride * B);
+    f((void **)&w.g_ex, sizeof(uint32_t) * 2 * gsn);
+    f((void **)&w.g_en, sizeof(uint32_t) * 2 * gsn);
+    f((void **)&w.g_pred, sizeof(int32_t) * gsn);
+    f((void **)&w.g_path, w.grid ? sizeof(int32_t) * (2 * gsn + 8) : 0);
+    f((void **)&w.g_ctrl, w.grid ? sizeof(int32_t) * kGridCtrlInts : 0);
+    f((void **)&w.g_ring, w.grid ? sizeof(uint32_t) * grid_ring_slots(S) : 0);
+    f((void **)&w.g_ring_key, w.grid ? sizeof(unsigned long long) * grid_ring_slots(S) : 0);
+}
+
+} // namespace
+
+struct gwtf_mcf {
+    gwtf_mcf_shape_t shape;
+    hipStream_t stream;
+    std::string err;
+    DeviceInfo dev;
+    Workspace ws;
     int32_t *dense_arc = nullptr; // located batches: implied link delays, allocated on first use
     int32_t solved = 0; // batch size of the last successful solve (0 = none)
 };
 
 namespace {
 
-thread_local std::string g_create_err;
+// Last error of a call made without a handle (create, the no-allocation
+// solve), per thread; a fixed buffer, so reporting allocates nothing.
+thread_local char g_thread_err[256];
+
+gwtf_status_t fail_thread(gwtf_status_t code, const char *what, hipError_t e = hipSuccess)
+{
+    if (e != hipSuccess) snprintf(g_thread_err, sizeof g_thread_err, "%s: %s", what, hipGetErrorString(e));
+    else snprintf(g_thread_err, sizeof g_thread_err, "%s", what);
+    return code;
+}
 
 gwtf_status_t fail(gwtf_mcf_t *h, gwtf_status_t code, const std::string &msg)
 {
     if (h) h->err = msg;
-    else g_create_err = msg;
+    else fail_thread(code, msg.c_str());
     return code;
 }
 
@@ -74,117 +167,61 @@ int lds_waves(int n) { return n <= 16 ? 1 : 4; }
 
 void free_ws(gwtf_mcf_t *h)
 {
-    (void)hipFree(h->route);
-    (void)hipFree(h->node_flow);
-    (void)hipFree(h->arc_flow);
-    (void)hipFree(h->pot);
-    (void)hipFree(h->stats);
-    (void)hipFree(h->state);
-    (void)hipFree(h->g_ex);
-    (void)hipFree(h->g_en);
-    (void)hipFree(h->g_pred);
-    (void)hipFree(h->g_path);
-    (void)hipFree(h->g_ctrl);
-    (void)hipFree(h->g_ring);
-    (void)hipFree(h->g_ring_key);
+    for_each_buffer(h->ws, h->shape.num_stages, h->shape.nodes_per_stage, h->shape.max_batch,
+                    [](void **p, size_t) {
+                        (void)hipFree(*p);
+                        *p = nullptr;
+                    });
     (void)hipFree(h->dense_arc);
     h->dense_arc = nullptr;
-    h->route = h->node_flow = h->arc_flow = h->pot = nullptr;
-    h->stats = nullptr;
-    h->state = nullptr;
-    h->g_ex = h->g_en = h->g_ring = nullptr;
-    h->g_ring_key = nullptr;
-    h->g_pred = h->g_path = h->g_ctrl = nullptr;
+}
+
+// Shape checks shared by gwtf_mcf_create and the no-allocation solve.
+const char *check_shape(int S, int n, int B)
+{
+    if (S < 1 || n < 1 || B < 1) return "shape values must be >= 1";
+    if (n > 32767) return "nodes_per_stage must be <= 32767";
+    const int64_t V = 2 * int64_t(S) * n + 3;
+    if (V > (int64_t(1) << 30) / 4) return "shape too large";
+    return nullptr;
 }
 
 } // namespace
 
 extern "C" gwtf_status_t gwtf_mcf_create(const gwtf_mcf_shape_t *shape, void *hip_stream, gwtf_mcf_t **out)
 {
-    if (!out) return fail(nullptr, GWTF_ERR_INVALID_ARG, "out is NULL");
+    if (!out) return fail_thread(GWTF_ERR_INVALID_ARG, "out is NULL");
     *out = nullptr;
-    if (!shape) return fail(nullptr, GWTF_ERR_INVALID_ARG, "shape is NULL");
+    if (!shape) return fail_thread(GWTF_ERR_INVALID_ARG, "shape is NULL");
     const int S = shape->num_stages, n = shape->nodes_per_stage, B = shape->max_batch;
-    if (S < 1 || n < 1 || B < 1) return fail(nullptr, GWTF_ERR_INVALID_ARG, "shape values must be >= 1");
-    if (n > 32767) return fail(nullptr, GWTF_ERR_INVALID_ARG, "nodes_per_stage must be <= 32767");
-    const int64_t SN = int64_t(S) * n, V = 2 * SN + 3;
-    if (V > (int64_t(1) << 30) / 4) return fail(nullptr, GWTF_ERR_INVALID_ARG, "shape too large");
+    if (const char *bad = check_shape(S, n, B)) return fail_thread(GWTF_ERR_INVALID_ARG, bad);
     int ndev = 0;
     hipError_t e = hipGetDeviceCount(&ndev);
-    if (e != hipSuccess) return fail(nullptr, GWTF_ERR_DEVICE, std::string("hipGetDeviceCount: ") + hipGetErrorString(e));
-    if (shape->device < 0 || shape->device >= ndev) return fail(nullptr, GWTF_ERR_INVALID_ARG, "bad device ordinal");
-    if ((e = hipSetDevice(shape->device)) != hipSuccess)
-        return fail(nullptr, GWTF_ERR_DEVICE, std::string("hipSetDevice: ") + hipGetErrorString(e));
+    if (e != hipSuccess) return fail_thread(GWTF_ERR_DEVICE, "hipGetDeviceCount", e);
+    if (shape->device < 0 || shape->device >= ndev) return fail_thread(GWTF_ERR_INVALID_ARG, "bad device ordinal");
+    if ((e = hipSetDevice(shape->device)) != hipSuccess) return fail_thread(GWTF_ERR_DEVICE, "hipSetDevice", e);
 
     gwtf_mcf_t *h = new (std::nothrow) gwtf_mcf_t();
-    if (!h) return fail(nullptr, GWTF_ERR_OUT_OF_MEMORY, "host allocation failed");
+    if (!h) return fail_thread(GWTF_ERR_OUT_OF_MEMORY, "host allocation failed");
     h->shape = *shape;
     h->stream = static_cast<hipStream_t>(hip_stream);
-    int lds = 0;
-    if ((e = hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerBlock, shape->device)) != hipSuccess) {
-        g_create_err = std::string("hipDeviceGetAttribute: ") + hipGetErrorString(e);
+    if ((e = query_device(shape->device, h->dev)) != hipSuccess) {
         delete h;
-        return GWTF_ERR_DEVICE;
+        return fail_thread(GWTF_ERR_DEVICE, "hipDeviceGetAttribute", e);
     }
-    h->lds_max = size_t(lds);
-    if (hipDeviceGetAttribute(&h->clock_khz, hipDeviceAttributeWallClockRate, shape->device) != hipSuccess)
-        h->clock_khz = 0;
-    // Raising the per-kernel dynamic-LDS ceiling is not needed on every
-    // runtime (some reject the attribute); failure is harmless, but its error
-    // must not linger where a later launch check would read it.
-    if (set_lds_limits(h->lds_max) != hipSuccess) (void)hipGetLastError();
-
-    // Fallback state sized for the worst case: every exit vertex may need
-    // min(cap, n, supply) <= n flow-list entries.
-    h->fallback_slots = int64_t(std::max(S - 1, 0)) * n * n;
-    h->state_stride = align16(make_layout(S, n, h->fallback_slots, false).total);
-    const size_t na = size_t(std::max(S - 1, 0)) * n * n;
-
-    // Grid-cooperative pass: S * ceil(n / 128) workgroups must all be
-    // resident at once (cooperative launch), one per CU given their LDS.
-    if (n > 64 && n <= kGridMaxNodes && S <= 1024) {
-        int coop = 0, cus = 0;
-        if (hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, shape->device) != hipSuccess) coop = 0;
-        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, shape->device) != hipSuccess) cus = 0;
-        (void)hipGetLastError();
-        const int64_t slots = grid_pass_list_slots(S, n, h->lds_max);
-        if (coop && cus > 0 && slots >= 64) {
-            const size_t lds = grid_pass_lds_bytes(S, n, slots);
-            const int per_cu = grid_pass_blocks_per_cu(lds);
-            if (per_cu >= 1 && int64_t(S) * grid_pass_slices(n) <= int64_t(per_cu) * cus) {
-                h->grid = true;
-                h->grid_slots = slots;
-                h->grid_lds = lds;
-            }
+    plan_workspace(h->ws, S, n, h->dev);
+    hipError_t first = hipSuccess;
+    for_each_buffer(h->ws, S, n, B, [&](void **p, size_t bytes) {
+        if (bytes == 0 || first != hipSuccess) return;
+        if ((e = hipMalloc(p, bytes)) != hipSuccess) {
+            *p = nullptr;
+            first = e;
         }
-    }
-    const size_t gsn = h->grid ? size_t(SN) : 0;
-    struct {
-        void **p;
-        size_t bytes;
-    } allocs[] = {
-        {(void **)&h->route, sizeof(int32_t) * B},
-        {(void **)&h->node_flow, sizeof(int32_t) * SN * B},
-        {(void **)&h->arc_flow, sizeof(int32_t) * std::max<size_t>(na, 1) * B},
-        {(void **)&h->pot, sizeof(int32_t) * V * B},
-        {(void **)&h->stats, sizeof(int64_t) * kStatsPerInstance * B},
-        {(void **)&h->state, h->state_stride * B},
-        {(void **)&h->g_ex, sizeof(uint32_t) * 2 * gsn},
-        {(void **)&h->g_en, sizeof(uint32_t) * 2 * gsn},
-        {(void **)&h->g_pred, sizeof(int32_t) * gsn},
-        {(void **)&h->g_path, sizeof(int32_t) * (2 * gsn + 8)},
-        {(void **)&h->g_ctrl, sizeof(int32_t) * kGridCtrlInts},
-        {(void **)&h->g_ring, h->grid ? sizeof(uint32_t) * grid_ring_slots(S) : 0},
-        {(void **)&h->g_ring_key, h->grid ? sizeof(unsigned long long) * grid_ring_slots(S) : 0},
-    };
-    for (auto &a : allocs) {
-        if (a.bytes == 0) continue;
-        if ((e = hipMalloc(a.p, a.bytes)) != hipSuccess) {
-            g_create_err = std::string("hipMalloc workspace: ") + hipGetErrorString(e);
-            free_ws(h);
-            delete h;
-            return GWTF_ERR_OUT_OF_MEMORY;
-        }
+    });
+    if (first != hipSuccess) {
+        free_ws(h);
+        delete h;
+        return fail_thread(GWTF_ERR_OUT_OF_MEMORY, "hipMalloc workspace", first);
     }
     *out = h;
     return GWTF_OK;
@@ -192,60 +229,66 @@ extern "C" gwtf_status_t gwtf_mcf_create(const gwtf_mcf_shape_t *shape, void *hi
 
 namespace {
 
-// Runs the solver passes for one batch (p describes it; loc/lat non-NULL
-// selects the location-factored grid pass for shapes that use the grid).
-gwtf_status_t run_passes(gwtf_mcf_t *h, SolveParams &p, const int32_t *loc, const int32_t *lat, int32_t L)
-{
-    const int S = h->shape.num_stages, n = h->shape.nodes_per_stage;
-    hipError_t e;
-    p.route = h->route;
-    p.node_flow = h->node_flow;
-    p.arc_flow = h->arc_flow;
-    p.pot = h->pot;
-    p.stats = h->stats;
-    p.state = h->state;
-    p.state_stride = h->state_stride;
-    p.clock_khz = h->clock_khz;
+struct PassResult {
+    gwtf_status_t code;
+    const char *what; // failing step (code != GWTF_OK)
+    hipError_t e;     // its HIP error (GWTF_ERR_DEVICE)
+};
 
-    h->solved = 0;
+// Enqueues the solver passes for one batch (p describes it; loc/lat non-NULL
+// selects the location-factored grid pass for shapes that use the grid),
+// with workspace `w` and the properties `d` of the current device.
+PassResult run_passes(const Workspace &w, const DeviceInfo &d, int S, int n, hipStream_t stream, SolveParams &p,
+                      const int32_t *loc, const int32_t *lat, int32_t L)
+{
+    hipError_t e;
+    p.route = w.route;
+    p.node_flow = w.node_flow;
+    p.arc_flow = w.arc_flow;
+    p.pot = w.pot;
+    p.stats = w.stats;
+    p.state = w.state;
+    p.state_stride = w.state_stride;
+    p.clock_khz = d.clock_khz;
+
     const int64_t worst = int64_t(std::max(S - 1, 0)) * n * n;
     bool need_fallback = true;
-    const int64_t pipe_slots = (n > 16 && pipe_pass_fits(S, n)) ? pipe_pass_slots(S, h->lds_max) : 0;
+    const int64_t pipe_slots = (n > 16 && pipe_pass_fits(S, n)) ? pipe_pass_slots(S, d.lds_max) : 0;
     const int waves = lds_waves(n);
-    const int64_t slots = pipe_slots > 0 ? 0 : lds_slots(S, n, waves, h->lds_max);
+    const int64_t slots = pipe_slots > 0 ? 0 : lds_slots(S, n, waves, d.lds_max);
     if (small_pass_fits(S, n)) {
         // Four instances per wave; instances outside the packed bounds go to
         // the fallback pass.
         p.list_slots = 0;
         p.route_all = 0;
-        if ((e = launch_small_pass(p, h->stream)) != hipSuccess) return hip_fail(h, e, "packed solver launch");
+        if ((e = launch_small_pass(p, stream)) != hipSuccess) return {GWTF_ERR_DEVICE, "packed solver launch", e};
         need_fallback = true;
-    } else if (h->grid) {
+    } else if (w.grid) {
         // One cooperative launch per instance; instances whose link costs
         // need more than 16 bits or whose flow lists outgrow LDS go to the
         // fallback pass.
         GridParams gp{};
         gp.base = p;
-        gp.base.list_slots = h->grid_slots;
+        gp.base.list_slots = w.grid_slots;
         gp.base.route_all = 0;
         gp.slices = grid_pass_slices(n);
-        gp.list_slots = h->grid_slots;
+        gp.list_slots = w.grid_slots;
         gp.big_bytes = grid_pass_big_bytes(S, n);
-        gp.ex = h->g_ex;
-        gp.en = h->g_en;
-        gp.pred = h->g_pred;
-        gp.path = h->g_path;
-        gp.ctrl = h->g_ctrl;
-        gp.ring = h->g_ring;
-        gp.ring_key = h->g_ring_key;
+        gp.ex = w.g_ex;
+        gp.en = w.g_en;
+        gp.pred = w.g_pred;
+        gp.path = w.g_path;
+        gp.ctrl = w.g_ctrl;
+        gp.ring = w.g_ring;
+        gp.ring_key = w.g_ring_key;
         gp.ring_slots = grid_ring_slots(S);
         gp.loc = loc;
         gp.lat = lat;
         gp.L = L;
         for (int i = 0; i < p.B; ++i) {
             gp.instance = i;
-            if ((e = launch_grid_pass(gp, h->grid_lds, h->stream)) != hipSuccess)
-                return hip_fail(h, e, "grid solver launch");
+            if ((e = launch_grid_pass(gp, w.grid_lds, stream)) != hipSuccess)
+                return {GWTF_ERR_DEVICE, "grid solver launch", e};
         }
         need_fallback = true;
     } else if (pipe_slots > 0) {
@@ -253,25 +296,36 @@ gwtf_status_t run_passes(gwtf_mcf_t *h, SolveParams &p, const int32_t *loc, cons
         // or more flow-list slots go to the fallback pass.
         p.list_slots = pipe_slots;
         p.route_all = 0;
-        if ((e = launch_pipe_pass(p, h->stream)) != hipSuccess) return hip_fail(h, e, "pipelined solver launch");
+        if ((e = launch_pipe_pass(p, stream)) != hipSuccess) return {GWTF_ERR_DEVICE, "pipelined solver launch", e};
         need_fallback = true;
     } else if (slots > 0) {
         p.list_slots = slots;
         p.route_all = 0;
         size_t lds = make_layout(S, n, slots, true).total + scratch_bytes(waves, n);
-        if ((e = launch_lds_pass(p, waves, lds, h->stream)) != hipSuccess) return hip_fail(h, e, "LDS solver launch");
+        if ((e = launch_lds_pass(p, waves, lds, stream)) != hipSuccess) return {GWTF_ERR_DEVICE, "LDS solver launch", e};
         // Worst-case list demand of an instance: (S-1) * n * min(n, cap, supply).
         need_fallback = slots < worst;
     } else {
         p.route_all = 1;
     }
     if (need_fallback) {
-        p.list_slots = h->fallback_slots;
+        p.list_slots = w.fallback_slots;
         size_t lds = scratch_bytes(fallback_waves(), n);
-        if (lds > h->lds_max) return fail(h, GWTF_ERR_INVALID_ARG, "nodes_per_stage too large for LDS scratch");
-        if ((e = launch_fallback_pass(p, lds, h->stream)) != hipSuccess)
-            return hip_fail(h, e, "fallback solver launch");
+        if (lds > d.lds_max) return {GWTF_ERR_INVALID_ARG, "nodes_per_stage too large for LDS scratch", hipSuccess};
+        if ((e = launch_fallback_pass(p, lds, stream)) != hipSuccess)
+            return {GWTF_ERR_DEVICE, "fallback solver launch", e};
     }
+    return {GWTF_OK, nullptr, hipSuccess};
+}
+
+// run_passes on a handle's workspace, with the outcome in the handle.
+gwtf_status_t run_handle_passes(gwtf_mcf_t *h, SolveParams &p, const int32_t *loc, const int32_t *lat, int32_t L)
+{
+    h->solved = 0;
+    const PassResult r = run_passes(h->ws, h->dev, h->shape.num_stages, h->shape.nodes_per_stage, h->stream, p,
+                                    loc, lat, L);
+    if (r.code == GWTF_ERR_DEVICE) return hip_fail(h, r.e, r.what);
+    if (r.code != GWTF_OK) return fail(h, r.code, r.what);
     h->solved = p.B;
     h->err.clear();
     return GWTF_OK;
@@ -306,7 +360,108 @@ extern "C" gwtf_status_t gwtf_mcf_solve_batch(gwtf_mcf_t *h, const gwtf_mcf_batc
     p.F_out = b->flow_value;
     p.cost_out = b->total_cost;
     p.status_out = b->status;
-    return run_passes(h, p, nullptr, nullptr, 0);
+    return run_handle_passes(h, p, nullptr, nullptr, 0);
+}
+
+// ---- Solve without allocation ----
+//
+// Workspace of gwtf_mcf_solve_batch_noalloc: one array per device, held
+// until the process ends.  In host code this name is only a host-side
+// stand-in; the device address comes from hipGetSymbolAddress, once per
+// device, and only that address is handed to kernels.
+constexpr size_t kScratchBytes = size_t(64) << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+
+constexpr int kScratchMaxDevices = 64;
+struct ScratchDevice {
+    bool ready = false;
+    unsigned char *ptr = nullptr; // device address of `scratch` on this device
+    DeviceInfo dev;
+};
+ScratchDevice g_scratch[kScratchMaxDevices];
+std::mutex g_scratch_lock;
+
+} // namespace
+
+extern "C" gwtf_status_t gwtf_mcf_solve_batch_noalloc(const gwtf_mcf_shape_t *shape, void *hip_stream,
+                                                      const gwtf_mcf_batch_t *b)
+{
+    if (!shape) return fail_thread(GWTF_ERR_INVALID_ARG, "shape is NULL");
+    if (!b) return fail_thread(GWTF_ERR_INVALID_ARG, "batch is NULL");
+    const int S = shape->num_stages, n = shape->nodes_per_stage;
+    if (const char *bad = check_shape(S, n, shape->max_batch)) return fail_thread(GWTF_ERR_INVALID_ARG, bad);
+    if (b->batch < 1 || b->batch > shape->max_batch)
+        return fail_thread(GWTF_ERR_INVALID_ARG, "batch outside [1, max_batch]");
+    if (!b->node_cap || !b->node_cost || !b->supply || !b->flow_value || !b->total_cost || !b->status)
+        return fail_thread(GWTF_ERR_INVALID_ARG, "required pointer is NULL");
+    if ((S > 1) != (b->arc_cost != nullptr))
+        return fail_thread(GWTF_ERR_INVALID_ARG, "arc_cost must be non-NULL exactly when S > 1");
+    int ndev = 0;
+    hipError_t e = hipGetDeviceCount(&ndev);
+    if (e != hipSuccess) return fail_thread(GWTF_ERR_DEVICE, "hipGetDeviceCount", e);
+    const int device = shape->device;
+    if (device < 0 || device >= ndev || device >= kScratchMaxDevices)
+        return fail_thread(GWTF_ERR_INVALID_ARG, "bad device ordinal");
+    if ((e = hipSetDevice(device)) != hipSuccess) return fail_thread(GWTF_ERR_DEVICE, "hipSetDevice", e);
+
+    DeviceInfo dev;
+    unsigned char *base = nullptr;
+    {
+        std::lock_guard<std::mutex> lock(g_scratch_lock);
+        ScratchDevice &sd = g_scratch[device];
+        if (!sd.ready) {
+            void *ptr = nullptr;
+            if ((e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch))) != hipSuccess)
+                return fail_thread(GWTF_ERR_DEVICE, "hipGetSymbolAddress(scratch)", e);
+            if ((e = query_device(device, sd.dev)) != hipSuccess)
+                return fail_thread(GWTF_ERR_DEVICE, "hipDeviceGetAttribute", e);
+            sd.ptr = static_cast<unsigned char *>(ptr);
+            sd.ready = true;
+        }
+        dev = sd.dev;
+        base = sd.ptr;
+    }
+
+    // Lay the workspace of this batch out in the array (256-byte aligned
+    // buffers), or refuse the batch if it does not fit.
+    Workspace w;
+    plan_workspace(w, S, n, dev);
+    size_t need = 0;
+    for_each_buffer(w, S, n, b->batch, [&](void **, size_t bytes) {
+        if (bytes) need = ((need + 255) & ~size_t(255)) + bytes;
+    });
+    if (need > kScratchBytes) {
+        snprintf(g_thread_err, sizeof g_thread_err,
+                 "batch needs %zu bytes of workspace, more than the %zu-byte scratch array; split it", need,
+                 kScratchBytes);
+        return GWTF_ERR_INVALID_ARG;
+    }
+    size_t off = 0;
+    for_each_buffer(w, S, n, b->batch, [&](void **p, size_t bytes) {
+        if (!bytes) return;
+        off = (off + 255) & ~size_t(255);
+        *p = base + off;
+        off += bytes;
+    });
+
+    SolveParams p{};
+    p.B = b->batch;
+    p.S = S;
+    p.n = n;
+    p.cap = b->node_cap;
+    p.ncost = b->node_cost;
+    p.acost = b->arc_cost;
+    p.src = b->src_cost;
+    p.snk = b->snk_cost;
+    p.supply = b->supply;
+    p.F_out = b->flow_value;
+    p.cost_out = b->total_cost;
+    p.status_out = b->status;
+    const PassResult r = run_passes(w, dev, S, n, static_cast<hipStream_t>(hip_stream), p, nullptr, nullptr, 0);
+    if (r.code != GWTF_OK) return fail_thread(r.code, r.what, r.e);
+    return GWTF_OK;
 }
 
 extern "C" gwtf_status_t gwtf_mcf_solve_located(gwtf_mcf_t *h, const gwtf_mcf_located_batch_t *b)
@@ -347,7 +502,7 @@ extern "C" gwtf_status_t gwtf_mcf_solve_located(gwtf_mcf_t *h, const gwtf_mcf_lo
     p.F_out = b->flow_value;
     p.cost_out = b->total_cost;
     p.status_out = b->status;
-    return run_passes(h, p, b->location, b->latency, L);
+    return run_handle_passes(h, p, b->location, b->latency, L);
 }
 
 extern "C" gwtf_status_t gwtf_mcf_get_flows(gwtf_mcf_t *h, int32_t first, int32_t count, int32_t *node_flow,
@@ -367,14 +522,14 @@ extern "C" gwtf_status_t gwtf_mcf_get_flows(gwtf_mcf_t *h, int32_t first, int32_
         if (!dst || bytes == 0) return hipSuccess;
         return hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, h->stream);
     };
-    if ((e = copy(node_flow, h->node_flow + size_t(first) * SN, sizeof(int32_t) * SN * count)) != hipSuccess)
+    if ((e = copy(node_flow, h->ws.node_flow + size_t(first) * SN, sizeof(int32_t) * SN * count)) != hipSuccess)
         return hip_fail(h, e, "copy node_flow");
-    if ((e = copy(arc_flow, h->arc_flow + size_t(first) * na, sizeof(int32_t) * na * count)) != hipSuccess)
+    if ((e = copy(arc_flow, h->ws.arc_flow + size_t(first) * na, sizeof(int32_t) * na * count)) != hipSuccess)
         return hip_fail(h, e, "copy arc_flow");
-    if ((e = copy(potential, h->pot + size_t(first) * V, sizeof(int32_t) * V * count)) != hipSuccess)
+    if ((e = copy(potential, h->ws.pot + size_t(first) * V, sizeof(int32_t) * V * count)) != hipSuccess)
         return hip_fail(h, e, "copy potential");
     if (src_flow || snk_flow) {
-        if ((e = launch_export(h->node_flow, S, n, first, count, src_flow, snk_flow, h->stream)) != hipSuccess)
+        if ((e = launch_export(h->ws.node_flow, S, n, first, count, src_flow, snk_flow, h->stream)) != hipSuccess)
             return hip_fail(h, e, "export launch");
     }
     return GWTF_OK;
@@ -390,7 +545,7 @@ extern "C" gwtf_status_t gwtf_mcf_get_stats(gwtf_mcf_t *h, int32_t first, int32_
     if (count == 0) return GWTF_OK;
     hipError_t e = hipSetDevice(h->shape.device);
     if (e != hipSuccess) return hip_fail(h, e, "hipSetDevice");
-    e = hipMemcpyAsync(stats, h->stats + size_t(first) * kStatsPerInstance,
+    e = hipMemcpyAsync(stats, h->ws.stats + size_t(first) * kStatsPerInstance,
                        sizeof(int64_t) * kStatsPerInstance * count, hipMemcpyDeviceToDevice, h->stream);
     if (e != hipSuccess) return hip_fail(h, e, "copy stats");
     return GWTF_OK;
@@ -406,7 +561,7 @@ extern "C" gwtf_status_t gwtf_mcf_get_passes(gwtf_mcf_t *h, int32_t first, int32
     if (count == 0) return GWTF_OK;
     hipError_t e = hipSetDevice(h->shape.device);
     if (e != hipSuccess) return hip_fail(h, e, "hipSetDevice");
-    e = hipMemcpyAsync(pass, h->route + first, sizeof(int32_t) * count, hipMemcpyDeviceToDevice, h->stream);
+    e = hipMemcpyAsync(pass, h->ws.route + first, sizeof(int32_t) * count, hipMemcpyDeviceToDevice, h->stream);
     if (e != hipSuccess) return hip_fail(h, e, "copy pass");
     return GWTF_OK;
 }
@@ -421,7 +576,7 @@ extern "C" void gwtf_mcf_destroy(gwtf_mcf_t *h)
 
 extern "C" const char *gwtf_mcf_last_error(const gwtf_mcf_t *h)
 {
-    return h ? h->err.c_str() : g_create_err.c_str();
+    return h ? h->err.c_str() : g_thread_err;
 }
 
 namespace {

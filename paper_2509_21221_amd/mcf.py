@@ -3,6 +3,7 @@ marshalling only -- every step of the solve runs in the HIP library).
 
 The functions carry the C names (``gwtf_mcf_create``, ``gwtf_mcf_solve_batch``,
 ``gwtf_mcf_get_flows``, ``gwtf_mcf_get_stats``, ``gwtf_mcf_get_passes``,
+``gwtf_mcf_solve_batch_noalloc``,
 ``gwtf_mcf_solve_located``, ``gwtf_whatif_count``, ``gwtf_mcf_whatif_expand``, ``gwtf_mcf_whatif_best``,
 ``gwtf_mcf_resolve_churn``,
 ``gwtf_mcf_destroy``, ``gwtf_mcf_last_error``); ``Solver`` wraps them for
@@ -123,6 +124,9 @@ def load_library(path: str = LIB_PATH):
         lib.gwtf_mcf_get_stats.restype = ctypes.c_int
         lib.gwtf_mcf_get_passes.argtypes = [vp, i32, i32, vp]
         lib.gwtf_mcf_get_passes.restype = ctypes.c_int
+        lib.gwtf_mcf_solve_batch_noalloc.argtypes = [ctypes.POINTER(gwtf_mcf_shape_t), vp,
+                                                     ctypes.POINTER(gwtf_mcf_batch_t)]
+        lib.gwtf_mcf_solve_batch_noalloc.restype = ctypes.c_int
         lib.gwtf_mcf_solve_located.argtypes = [vp, ctypes.POINTER(gwtf_mcf_located_batch_t)]
         lib.gwtf_mcf_solve_located.restype = ctypes.c_int
         lib.gwtf_whatif_count.argtypes = [i32, i32, ctypes.POINTER(ctypes.c_int64)]
@@ -173,6 +177,21 @@ def gwtf_mcf_solve_batch(handle, batch: int, node_cap: int, node_cost: int, arc_
                          src_cost or None, snk_cost or None, supply or None, flow_value or None,
                          total_cost or None, status or None)
     _check(load_library().gwtf_mcf_solve_batch(ctypes.c_void_p(handle), ctypes.byref(b)), handle)
+
+
+def gwtf_mcf_solve_batch_noalloc(num_stages: int, nodes_per_stage: int, max_batch: int, device: int,
+                                 hip_stream: int, batch: int, node_cap: int, node_cost: int, arc_cost: int,
+                                 src_cost: int, snk_cost: int, supply: int, flow_value: int,
+                                 total_cost: int, status: int) -> None:
+    """The solve of ``gwtf_mcf_solve_batch`` without a handle, its workspace
+    in the library's fixed per-device array (no allocation).  Arguments
+    after ``batch`` are device addresses (0 = NULL)."""
+    shape = gwtf_mcf_shape_t(num_stages, nodes_per_stage, max_batch, device)
+    b = gwtf_mcf_batch_t(batch, node_cap or None, node_cost or None, arc_cost or None,
+                         src_cost or None, snk_cost or None, supply or None, flow_value or None,
+                         total_cost or None, status or None)
+    _check(load_library().gwtf_mcf_solve_batch_noalloc(ctypes.byref(shape), ctypes.c_void_p(hip_stream or None),
+                                                        ctypes.byref(b)))
 
 
 def gwtf_mcf_solve_located(handle, batch: int, num_locations: int, node_cap: int, node_cost: int,

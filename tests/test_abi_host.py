@@ -71,6 +71,21 @@ def test_null_handle_calls_fail_cleanly():
     assert lib.gwtf_mcf_create(ctypes.byref(bad), None, ctypes.byref(out)) == mcf.GWTF_ERR_INVALID_ARG
 
 
+def test_noalloc_solve_rejects_arguments_before_touching_a_device():
+    lib = mcf.load_library()
+    assert lib.gwtf_mcf_solve_batch_noalloc(None, None, None) == mcf.GWTF_ERR_INVALID_ARG
+    assert "shape" in mcf.gwtf_mcf_last_error(None)
+    shape = mcf.gwtf_mcf_shape_t(8, 8, 4, 0)
+    assert lib.gwtf_mcf_solve_batch_noalloc(ctypes.byref(shape), None, None) == mcf.GWTF_ERR_INVALID_ARG
+    assert "batch" in mcf.gwtf_mcf_last_error(None)
+    b = mcf.gwtf_mcf_batch_t(5, 1, 1, 1, None, None, 1, 1, 1, 1)
+    assert lib.gwtf_mcf_solve_batch_noalloc(ctypes.byref(shape), None, ctypes.byref(b)) == mcf.GWTF_ERR_INVALID_ARG
+    assert "max_batch" in mcf.gwtf_mcf_last_error(None)
+    b = mcf.gwtf_mcf_batch_t(2, 1, 1, None, None, None, 1, 1, 1, 1)
+    assert lib.gwtf_mcf_solve_batch_noalloc(ctypes.byref(shape), None, ctypes.byref(b)) == mcf.GWTF_ERR_INVALID_ARG
+    assert "arc_cost" in mcf.gwtf_mcf_last_error(None)
+
+
 def test_product_path_fails_loudly_without_library(tmp_path):
     saved = mcf._lib
     mcf._lib = None
