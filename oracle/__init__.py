@@ -35,11 +35,15 @@ STATUS_SELFCHECK = 99
 
 
 def build() -> str:
-    """Compile the oracle with gcc into oracle/liboracle.so."""
+    """Compile the oracle with gcc into oracle/liboracle.so, and the
+    decentralized-heuristic simulator (oracle/heuristic.py) beside it."""
     tmp = _LIB_PATH + f".tmp{os.getpid()}"
     subprocess.check_call(["gcc", "-O2", "-std=c11", "-Wall", "-Wextra", "-shared", "-fPIC",
                            "-pthread", _SRC, "-o", tmp])
     os.replace(tmp, _LIB_PATH)
+    from . import heuristic
+
+    heuristic.build()
     return _LIB_PATH
 
 
