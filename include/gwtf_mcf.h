@@ -308,6 +308,76 @@ gwtf_status_t gwtf_mcf_resolve_churn(gwtf_mcf_t *h, const gwtf_mcf_batch_t *b,
                                      const gwtf_mcf_flow_in_t *start,
                                      const gwtf_mcf_flow_out_t *out, int64_t *work);
 
+/* ---- Simulation of the decentralized flow heuristic (paper Sec. V-C:
+ * Request Flow, Request Change and Request Redirect with simulated
+ * annealing; Sec. VI setup: T0 = 1.7, alpha = 0.95) ----
+ *
+ * Runs the paper's decentralized routing heuristic on every instance of a
+ * batch for a number of synchronous rounds, so that its result can be scored
+ * against the exact optimum of gwtf_mcf_solve_batch on the same instances
+ * (the flow ablation of Sec. VI).  Relay (k, i) holds cap[k][i] slots, one
+ * per microbatch; each round:
+ *   1. every relay computes, from the last stage to the first, the cost to
+ *      the sink of each of its outflows (compute cost + link + the next
+ *      hop's cost to the sink);
+ *   2. Request Flow: a relay with no unpaired outflow and a free slot asks
+ *      the next-stage relay whose unpaired outflow minimises (its cost to
+ *      the sink + the link cost), lowest index on ties; a relay asked by
+ *      several approves the lowest-index one, the data node as sink approves
+ *      last-stage requesters in index order while it has flow left (it
+ *      starts with `supply`), and the data node as source pairs first-stage
+ *      unpaired outflows, cheapest first, while it has flow left;
+ *   3. improvement: stages of even index, then odd ones, are shuffled and
+ *      split into pairs; a proposer that made no request this round draws a
+ *      Request Redirect (carrying one of its partner's paired flows itself,
+ *      if it has a free slot) or a Request Change (swapping the next hops of
+ *      one flow each) and takes it when exp((cost_cur - cost_new) / T) >
+ *      U(0, 1); costs are the Eq. 1 costs of the changed links, summed
+ *      (GWTF_HEUR_SUM, Eq. 2) or maximised (GWTF_HEUR_MAX, the local max
+ *      objective of Sec. V-A); each accepted move multiplies the proposer's
+ *      temperature by alpha.
+ * Random numbers are Philox4x64-10 with key (seed, instance index) and
+ * counter (round, stage, 0, block) for a stage's shuffle and (round, stage,
+ * 1, pair) for a pair's four draws: the same inputs and seed give the same
+ * result.
+ *
+ * Result: the complete paths (data node -> one relay per stage -> data node)
+ * present after the last round.  b->flow_value receives their number,
+ * b->total_cost their summed cost (Eq. 2, the exact solver's objective) and
+ * b->status the instance status (GWTF_INST_BAD_INPUT as for the solver, or a
+ * total capacity above max_slots, or an invalid initial path;
+ * GWTF_INST_OVERFLOW when (2S + 2) * the largest cost >= 2^30).  Requires
+ * S * n <= 64 (one lane per relay, one wave per instance); every input array
+ * is a device pointer in the layout of gwtf_mcf_solve_batch.  Uses no handle
+ * workspace; enqueued on the handle's stream. */
+enum { GWTF_HEUR_SUM = 0, GWTF_HEUR_MAX = 1 };
+
+typedef struct {
+    int32_t rounds;        /* synchronous rounds, >= 0 (the paper runs at most 120) */
+    int32_t objective;     /* GWTF_HEUR_SUM or GWTF_HEUR_MAX */
+    double t0, alpha;      /* initial temperature and cooling factor, > 0 */
+    uint64_t seed;         /* Philox key word 0 */
+    int32_t max_slots;     /* bound on an instance's total capacity, 1..4096 (sizes LDS) */
+    int32_t num_paths;     /* P >= 0: initial complete paths per instance */
+    const int32_t *paths;  /* [B][P][S] device, node index per stage (rows starting
+                              with -1 unused), NULL iff P == 0: the flow starts with
+                              these paths, each node taking its lowest free slot */
+} gwtf_heur_config_t;
+
+/* Optional per-instance outputs (device pointers, any may be NULL). */
+typedef struct {
+    int32_t *node_flow;    /* [B][S][n] complete paths through each relay */
+    int32_t *arc_flow;     /* [B][S-1][n][n] complete paths on each link (NULL iff S == 1) */
+    int32_t *used;         /* [B][S][n] slots in use, incomplete chains included */
+    int32_t *accepted;     /* [B][S][n] moves each relay proposed and had accepted */
+    double *temperature;   /* [B][S][n] final temperature of each relay */
+    int64_t *counters;     /* [B][4]: paths the data node paired, Request Flow approvals,
+                              accepted moves, slots in incomplete chains */
+} gwtf_heur_out_t;
+
+gwtf_status_t gwtf_mcf_simulate_heuristic(gwtf_mcf_t *h, const gwtf_mcf_batch_t *b,
+                                          const gwtf_heur_config_t *cfg, const gwtf_heur_out_t *out);
+
 /* Frees the handle and its workspace after draining its stream; NULL-safe. */
 void gwtf_mcf_destroy(gwtf_mcf_t *h);
 

@@ -738,3 +738,65 @@ extern "C" gwtf_status_t gwtf_mcf_resolve_churn(gwtf_mcf_t *h, const gwtf_mcf_ba
     if ((e = launch_churn_resolve(p, h->stream)) != hipSuccess) return hip_fail(h, e, "churn re-solve launch");
     return GWTF_OK;
 }
+
+extern "C" gwtf_status_t gwtf_mcf_simulate_heuristic(gwtf_mcf_t *h, const gwtf_mcf_batch_t *b,
+                                                     const gwtf_heur_config_t *cfg, const gwtf_heur_out_t *out)
+{
+    if (!h) return fail(nullptr, GWTF_ERR_INVALID_ARG, "handle is NULL");
+    if (!b || !cfg) return fail(h, GWTF_ERR_INVALID_ARG, "batch or config is NULL");
+    const int S = h->shape.num_stages, n = h->shape.nodes_per_stage;
+    if (int64_t(S) * n > kHeurMaxNodes)
+        return fail(h, GWTF_ERR_INVALID_ARG, "heuristic simulation needs S*n <= 64 (one lane per relay)");
+    if (b->batch < 1 || b->batch > h->shape.max_batch)
+        return fail(h, GWTF_ERR_INVALID_ARG, "batch outside [1, max_batch]");
+    if (!b->node_cap || !b->node_cost || !b->supply || !b->flow_value || !b->total_cost || !b->status)
+        return fail(h, GWTF_ERR_INVALID_ARG, "required pointer is NULL");
+    if ((S > 1) != (b->arc_cost != nullptr))
+        return fail(h, GWTF_ERR_INVALID_ARG, "arc_cost must be non-NULL exactly when S > 1");
+    if (cfg->rounds < 0) return fail(h, GWTF_ERR_INVALID_ARG, "rounds must be >= 0");
+    if (cfg->objective != GWTF_HEUR_SUM && cfg->objective != GWTF_HEUR_MAX)
+        return fail(h, GWTF_ERR_INVALID_ARG, "objective must be GWTF_HEUR_SUM or GWTF_HEUR_MAX");
+    if (!(cfg->t0 > 0.0) || !(cfg->t0 < 1e300) || !(cfg->alpha > 0.0) || !(cfg->alpha < 1e300))
+        return fail(h, GWTF_ERR_INVALID_ARG, "t0 and alpha must be positive and finite");
+    if (cfg->max_slots < 1 || cfg->max_slots > kHeurMaxSlots)
+        return fail(h, GWTF_ERR_INVALID_ARG, "max_slots outside [1, 4096]");
+    if (cfg->num_paths < 0 || (cfg->num_paths > 0) != (cfg->paths != nullptr))
+        return fail(h, GWTF_ERR_INVALID_ARG, "paths must be non-NULL exactly when num_paths > 0");
+    if (S == 1 && out && out->arc_flow)
+        return fail(h, GWTF_ERR_INVALID_ARG, "arc_flow must be NULL when S == 1");
+    hipError_t e = hipSetDevice(h->shape.device);
+    if (e != hipSuccess) return hip_fail(h, e, "hipSetDevice");
+    if (heuristic_lds_bytes(S, n, cfg->max_slots) > h->dev.lds_max)
+        return fail(h, GWTF_ERR_INVALID_ARG, "max_slots too large for LDS");
+    HeurParams p{};
+    p.B = b->batch;
+    p.S = S;
+    p.n = n;
+    p.rounds = cfg->rounds;
+    p.objective = cfg->objective;
+    p.max_slots = cfg->max_slots;
+    p.num_paths = cfg->num_paths;
+    p.t0 = cfg->t0;
+    p.alpha = cfg->alpha;
+    p.seed = cfg->seed;
+    p.cap = b->node_cap;
+    p.cost = b->node_cost;
+    p.arc = b->arc_cost;
+    p.src = b->src_cost;
+    p.snk = b->snk_cost;
+    p.supply = b->supply;
+    p.paths = cfg->paths;
+    p.F_out = b->flow_value;
+    p.cost_out = b->total_cost;
+    p.status_out = b->status;
+    if (out) {
+        p.node_flow = out->node_flow;
+        p.arc_flow = out->arc_flow;
+        p.used = out->used;
+        p.accepted = out->accepted;
+        p.temperature = out->temperature;
+        p.counters = out->counters;
+    }
+    if ((e = launch_heuristic(p, h->stream)) != hipSuccess) return hip_fail(h, e, "heuristic simulation launch");
+    return GWTF_OK;
+}

@@ -133,4 +133,24 @@ struct ChurnParams {
 size_t churn_lds_bytes(int S, int n);
 hipError_t launch_churn_resolve(const ChurnParams &p, hipStream_t stream);
 
+// Simulation of the decentralized flow heuristic (mcf_heuristic.hip): one
+// wave per instance, one lane per relay, so S*n <= kHeurMaxNodes; at most
+// kHeurMaxSlots slots (units of capacity) per instance.
+constexpr int kHeurMaxNodes = 64;
+constexpr int kHeurMaxSlots = 4096;
+struct HeurParams {
+    int32_t B, S, n, rounds, objective, max_slots, num_paths;
+    double t0, alpha;
+    uint64_t seed;
+    const int32_t *cap, *cost, *arc, *src, *snk, *supply; // caller inputs
+    const int32_t *paths;                                 // [B][num_paths][S] or NULL
+    int64_t *F_out, *cost_out;                            // [B]
+    int32_t *status_out;                                  // [B]
+    int32_t *node_flow, *arc_flow, *used, *accepted;      // optional outputs
+    double *temperature;                                  // optional [B][S][n]
+    int64_t *counters;                                    // optional [B][4]
+};
+size_t heuristic_lds_bytes(int S, int n, int max_slots);
+hipError_t launch_heuristic(const HeurParams &p, hipStream_t stream);
+
 } // namespace gwtf

@@ -5,7 +5,7 @@ The functions carry the C names (``gwtf_mcf_create``, ``gwtf_mcf_solve_batch``,
 ``gwtf_mcf_get_flows``, ``gwtf_mcf_get_stats``, ``gwtf_mcf_get_passes``,
 ``gwtf_mcf_solve_batch_noalloc``,
 ``gwtf_mcf_solve_located``, ``gwtf_whatif_count``, ``gwtf_mcf_whatif_expand``, ``gwtf_mcf_whatif_best``,
-``gwtf_mcf_resolve_churn``,
+``gwtf_mcf_resolve_churn``, ``gwtf_mcf_simulate_heuristic``,
 ``gwtf_mcf_destroy``, ``gwtf_mcf_last_error``); ``Solver`` wraps them for
 torch device tensors.
 PyTorch only provides device memory and the HIP stream.
@@ -92,6 +92,22 @@ class gwtf_mcf_flow_out_t(ctypes.Structure):
                 ("src_flow", ctypes.c_void_p), ("snk_flow", ctypes.c_void_p)]
 
 
+class gwtf_heur_config_t(ctypes.Structure):
+    _fields_ = [("rounds", ctypes.c_int32), ("objective", ctypes.c_int32), ("t0", ctypes.c_double),
+                ("alpha", ctypes.c_double), ("seed", ctypes.c_uint64), ("max_slots", ctypes.c_int32),
+                ("num_paths", ctypes.c_int32), ("paths", ctypes.c_void_p)]
+
+
+class gwtf_heur_out_t(ctypes.Structure):
+    _fields_ = [("node_flow", ctypes.c_void_p), ("arc_flow", ctypes.c_void_p), ("used", ctypes.c_void_p),
+                ("accepted", ctypes.c_void_p), ("temperature", ctypes.c_void_p), ("counters", ctypes.c_void_p)]
+
+
+GWTF_HEUR_SUM = 0
+GWTF_HEUR_MAX = 1
+HEUR_COUNTERS_PER_INSTANCE = 4
+
+
 class GwtfError(RuntimeError):
     def __init__(self, code, msg):
         super().__init__(f"{STATUS_NAMES.get(code, code)}: {msg}")
@@ -141,6 +157,10 @@ def load_library(path: str = LIB_PATH):
                                                ctypes.POINTER(gwtf_mcf_flow_in_t),
                                                ctypes.POINTER(gwtf_mcf_flow_out_t), vp]
         lib.gwtf_mcf_resolve_churn.restype = ctypes.c_int
+        lib.gwtf_mcf_simulate_heuristic.argtypes = [vp, ctypes.POINTER(gwtf_mcf_batch_t),
+                                                    ctypes.POINTER(gwtf_heur_config_t),
+                                                    ctypes.POINTER(gwtf_heur_out_t)]
+        lib.gwtf_mcf_simulate_heuristic.restype = ctypes.c_int
         lib.gwtf_mcf_destroy.argtypes = [vp]
         lib.gwtf_mcf_destroy.restype = None
         lib.gwtf_mcf_last_error.argtypes = [vp]
@@ -268,6 +288,24 @@ def gwtf_mcf_resolve_churn(handle, batch: int, node_cap: int, node_cost: int, ar
                                                  ctypes.c_void_p(work or None)), handle)
 
 
+def gwtf_mcf_simulate_heuristic(handle, batch: int, node_cap: int, node_cost: int, arc_cost: int,
+                                src_cost: int, snk_cost: int, supply: int, flow_value: int, total_cost: int,
+                                status: int, rounds: int, objective: int, t0: float, alpha: float, seed: int,
+                                max_slots: int, num_paths: int = 0, paths: int = 0, out: dict | None = None) -> None:
+    """Device addresses as for ``gwtf_mcf_solve_batch``; ``out`` maps the
+    gwtf_heur_out_t field names to device addresses (0 = NULL)."""
+    b = gwtf_mcf_batch_t(batch, node_cap or None, node_cost or None, arc_cost or None,
+                         src_cost or None, snk_cost or None, supply or None, flow_value or None,
+                         total_cost or None, status or None)
+    c = gwtf_heur_config_t(rounds, objective, t0, alpha, seed & (2**64 - 1), max_slots, num_paths, paths or None)
+    o = None
+    if out is not None:
+        o = gwtf_heur_out_t(*(out.get(k) or None for k in ("node_flow", "arc_flow", "used", "accepted",
+                                                             "temperature", "counters")))
+    _check(load_library().gwtf_mcf_simulate_heuristic(ctypes.c_void_p(handle), ctypes.byref(b), ctypes.byref(c),
+                                                      ctypes.byref(o) if o is not None else None), handle)
+
+
 def gwtf_mcf_destroy(handle) -> None:
     load_library().gwtf_mcf_destroy(ctypes.c_void_p(handle))
 
@@ -392,6 +430,47 @@ class Solver:
         if work:
             res = res + (wk,)
         return res
+
+    def simulate_heuristic(self, node_cap, node_cost, arc_cost, supply, src_cost=None, snk_cost=None,
+                           rounds: int = 120, objective: str = "sum", t0: float = 1.7, alpha: float = 0.95,
+                           seed: int = 0, max_slots: int = 1024, paths=None, details: bool = False):
+        """Decentralized-heuristic simulation of a batch (one wave per
+        instance).  Returns (F, cost, status) device tensors and, with
+        ``details``, a dict of node_flow, arc_flow, used, accepted,
+        temperature and counters tensors.  ``paths``: optional int32 device
+        tensor [B][P][S] of initial complete paths."""
+        torch = self.torch
+        S, n = self.S, self.n
+        B = int(supply.shape[0])
+        args = [self._arg(node_cap, (B, S, n), "node_cap"), self._arg(node_cost, (B, S, n), "node_cost"),
+                self._arg(arc_cost, (B, S - 1, n, n), "arc_cost") if S > 1 else 0,
+                self._arg(src_cost, (B, n), "src_cost"), self._arg(snk_cost, (B, n), "snk_cost"),
+                self._arg(supply, (B,), "supply")]
+        if S > 1 and arc_cost is None:
+            raise ValueError("arc_cost is required when S > 1")
+        P = 0
+        pp = 0
+        if paths is not None:
+            P = int(paths.shape[1])
+            pp = self._arg(paths, (B, P, S), "paths")
+        dev = torch.device("cuda", self.device)
+        F = torch.empty(B, dtype=torch.int64, device=dev)
+        cost = torch.empty(B, dtype=torch.int64, device=dev)
+        status = torch.empty(B, dtype=torch.int32, device=dev)
+        det = None
+        if details:
+            det = {"node_flow": torch.empty((B, S, n), dtype=torch.int32, device=dev),
+                   "arc_flow": torch.empty((B, max(S - 1, 0), n, n), dtype=torch.int32, device=dev),
+                   "used": torch.empty((B, S, n), dtype=torch.int32, device=dev),
+                   "accepted": torch.empty((B, S, n), dtype=torch.int32, device=dev),
+                   "temperature": torch.empty((B, S, n), dtype=torch.float64, device=dev),
+                   "counters": torch.empty((B, HEUR_COUNTERS_PER_INSTANCE), dtype=torch.int64, device=dev)}
+        obj = {"sum": GWTF_HEUR_SUM, "max": GWTF_HEUR_MAX}[objective]
+        gwtf_mcf_simulate_heuristic(
+            self.handle, B, *args, F.data_ptr(), cost.data_ptr(), status.data_ptr(), rounds, obj, t0, alpha,
+            seed, max_slots, P, pp,
+            {k: (v.data_ptr() if (k != "arc_flow" or S > 1) else 0) for k, v in det.items()} if det else None)
+        return (F, cost, status, det) if details else (F, cost, status)
 
     def flows(self, first: int = 0, count: int | None = None):
         torch = self.torch
