@@ -3,6 +3,7 @@
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 4]
     python bench.py --whatif 1        # what-if node addition, paper setting 1
     python bench.py --config 5 --located   # link delays as location latencies
+    python bench.py --heuristic        # decentralized heuristic vs the exact optimum
 
 A step solves one whole batch of the workload (every instance to optimality)
 with inputs already resident in HBM.  The default workload is the 7B-scale
@@ -17,6 +18,11 @@ paper's node-addition test (Sec. VI, handling joining nodes; settings 1-3:
 8 stages of 12 relays plus one joining position, 8 candidates, 8! = 40320
 placements): expand all placements on the device, solve them, reduce to the
 best placement.  The value is placements evaluated per second.
+
+With --heuristic a step simulates the paper's decentralized routing
+heuristic (Sec. V-C, 120 rounds) on flow-test settings 1-4, 16384 instances
+each, and the line scores its cost against the exact optimum of the same
+instances (solved on the GPU).  The value is simulated instances per second.
 
 With --located the same preset (2, 4 or 5) is passed in located form (each
 node's location and the latency matrix instead of the n x n delays) to
@@ -149,6 +155,52 @@ def roofline_for(main_pass, relax, kernel_s, traffic, kernel, floor_bytes=None):
                                  "basis": "12 B per relaxation performed; link costs stay on chip"}}
     return {"bound": "hbm", "achieved": counted, "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": counted / HBM_PEAK_GBS, "traffic": traffic, "kernel": kernel, "kernel_ms": kernel_s * 1e3}
+
+
+# VALU issue peak: each CU issues at most one wave64 vector instruction per
+# cycle (four SIMDs of 16 lanes, four cycles per wave64 instruction).
+VALU_ISSUE_PEAK = 256 * 2.4e9
+
+
+def heuristic_counters():
+    """Per-setting counters of the heuristic kernel from the committed
+    rocprofv3 record, or None when the kernel's sources changed since."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", "heuristic_kernel_flowtests_counters.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    h = hashlib.sha256()
+    for f in rec["sources"]:
+        full = os.path.join(ROOT, f)
+        if not os.path.exists(full):
+            return None
+        h.update(open(full, "rb").read())
+    return rec if h.hexdigest() == rec["kernel_sources_sha256"] else None
+
+
+def heuristic_roofline(instance_rounds, kernel_ms, batch):
+    """The heuristic simulation keeps each instance in LDS and issues vector
+    instructions back to back: rocprofv3 counts about 91 % of the VALU issue
+    peak on settings 1, 2 and 4.  Its roofline is that issue rate: VALU
+    wave-instructions per launch (the committed counter record, which holds
+    for the same sources, batch and seed) over the measured kernel time."""
+    rec = heuristic_counters()
+    total_s = sum(kernel_ms.values()) / 1e3
+    line = {"bound": "alu", "unit": "VALU wave-instructions/s", "peak": VALU_ISSUE_PEAK,
+            "achieved": None, "frac": None, "traffic": None,
+            "kernel": "heuristic_kernel (one launch per setting)", "kernel_ms": total_s * 1e3,
+            "instance_rounds_per_s": instance_rounds / total_s}
+    if rec is not None and batch == 16384:
+        per = rec["per_setting"]
+        valu = sum(per[f"setting {s}"]["SQ_INSTS_VALU"] for s in kernel_ms)
+        traffic = sum(per[f"setting {s}"]["traffic_bytes"] for s in kernel_ms)
+        line.update(achieved=valu / total_s, frac=valu / total_s / VALU_ISSUE_PEAK,
+                    traffic=traffic / total_s / 1e9, traffic_unit="GB/s",
+                    valu_per_instance_round=valu / instance_rounds,
+                    counters="profiles/heuristic_kernel_flowtests_counters.json")
+    return line
 
 
 def whatif_cpu_baseline(base, slot, cands, total: int, budget_s: float, threads: int):
@@ -345,6 +397,103 @@ def run_churn(args):
     print(json.dumps(line), flush=True)
 
 
+def run_heuristic(args):
+    """Time the decentralized-heuristic simulation on flow-test settings 1-4
+    and score it against the exact optimum of the same instances."""
+    import numpy as np
+    import torch
+
+    from paper_2509_21221_amd import workloads as W
+    from paper_2509_21221_amd.mcf import Solver
+
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    t = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    stream = torch.cuda.current_stream(dev)
+    B, rounds, settings = args.heuristic_batch, args.rounds, (1, 2, 3, 4)
+    jobs = []
+    for s in settings:
+        batch = W.paper_flow_test(s, B)
+        solver = Solver(batch.S, batch.n, B, device=0, stream=stream)
+        inputs = (t(batch.node_cap), t(batch.node_cost), t(batch.arc_cost), t(batch.supply),
+                  t(batch.src_cost), t(batch.snk_cost))
+        # slots (LDS) sized to the batch's largest total capacity
+        slots = int(-(-int(batch.node_cap.sum(axis=(1, 2)).max()) // 32) * 32)
+        jobs.append((s, batch, solver, inputs, slots))
+
+    def step():
+        return [solver.simulate_heuristic(*inp, rounds=rounds, objective=args.objective, seed=0,
+                                          max_slots=slots) for _, _, solver, inp, slots in jobs]
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in jobs]
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        for (s, batch, solver, inp, slots), (e0, e1) in zip(jobs, ev):
+            if k == args.steps - 1:
+                e0.record(stream)
+            solver.simulate_heuristic(*inp, rounds=rounds, objective=args.objective, seed=0, max_slots=slots)
+            if k == args.steps - 1:
+                e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kernel_ms = {s: e0.elapsed_time(e1) for (s, *_), (e0, e1) in zip(jobs, ev)}
+    per_setting = {}
+    for s, batch, solver, inp, slots in jobs:
+        F, cost, status = (x.cpu().numpy() for x in solver.simulate_heuristic(
+            *inp, rounds=rounds, objective=args.objective, seed=0, max_slots=slots))
+        eF, ecost, estatus = (x.cpu().numpy() for x in solver.solve(*inp[:4], src_cost=inp[4], snk_cost=inp[5]))
+        if (status != 0).any() or (estatus != 0).any():
+            raise SystemExit(f"setting {s}: non-ok status")
+        same = F == eF
+        per_setting[f"setting {s}"] = {
+            "stages": batch.S, "relays_per_stage": batch.n,
+            "heuristic_over_optimum": float(cost[same].sum() / ecost[same].sum()),
+            "mean_instance_ratio": float(np.mean(cost[same] / ecost[same])),
+            "reached_optimal_flow": float(same.mean()),
+            "max_slots": slots, "kernel_ms": kernel_ms[s]}
+    total_ms = sum(kernel_ms.values())
+    line = {
+        "metric": "decentralized-heuristic instances simulated/sec (120 rounds) and cost / exact optimum",
+        "value": len(jobs) * B * args.steps / wall,
+        "unit": "instances/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": wall / args.steps * 1e3,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "int32+f64", "data": "synthetic (seeded generator, paper-shaped)",
+        "config": {"workload": f"flow-test settings 1-4 (40 relays over 8 or 10 stages, one data node), {B} "
+                               f"instances each, {rounds} rounds, {args.objective} objective, T0 1.7, alpha 0.95",
+                   "instances": len(jobs) * B, "rounds": rounds, "seed": 0},
+        "instance_rounds_per_s": len(jobs) * B * rounds / (total_ms / 1e3),
+        "per_setting": per_setting,
+        # the committed counters hold for the default workload only
+        "roofline": heuristic_roofline(len(jobs) * B * rounds, kernel_ms,
+                                       B if (args.objective, rounds) == ("sum", 120) else 0),
+    }
+    if args.cpu_budget > 0:
+        from oracle import heuristic as H
+
+        threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+        threads = max(1, min(threads, os.cpu_count() or 1))
+        done, used_s = 0, 0.0
+        while used_s < args.cpu_budget and done < B:
+            for s, batch, *_ in jobs:
+                sub = batch.subset(range(done, min(B, done + 256)))
+                t1 = time.perf_counter()
+                r = H.simulate(sub, rounds=rounds, objective=args.objective, seed=0, nthreads=threads)
+                used_s += time.perf_counter() - t1
+            done = min(B, done + 256)
+        line["cpu_baseline"] = {"value": len(jobs) * done / used_s, "unit": "instances/s", "cores": r["threads"],
+                                "kind": "oracle",
+                                "sample": f"first {done} instances of each of the 4 settings, {used_s:.1f} s wall "
+                                          f"on {r['threads']} threads"}
+    for _, _, solver, _, _ in jobs:
+        solver.close()
+    print(json.dumps(line), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -355,6 +504,11 @@ def main():
                     help="time what-if node addition for this paper setting instead (0 = off)")
     ap.add_argument("--churn", action="store_true",
                     help="warm-started re-solve of the 8x8 churn variants beside cold solves")
+    ap.add_argument("--heuristic", action="store_true",
+                    help="simulate the decentralized heuristic on flow-test settings 1-4 and score it")
+    ap.add_argument("--heuristic-batch", type=int, default=16384, help="instances per setting (--heuristic)")
+    ap.add_argument("--rounds", type=int, default=120, help="heuristic rounds (--heuristic)")
+    ap.add_argument("--objective", choices=["sum", "max"], default="sum", help="heuristic objective")
     ap.add_argument("--located", action="store_true",
                     help="pass the preset (2, 4 or 5) in located form to gwtf_mcf_solve_located")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
@@ -382,6 +536,8 @@ def main():
         return run_whatif(args)
     if args.churn:
         return run_churn(args)
+    if args.heuristic:
+        return run_heuristic(args)
 
     import numpy as np
     import torch

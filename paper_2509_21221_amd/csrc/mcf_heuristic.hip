@@ -77,7 +77,7 @@ __device__ inline void philox(uint64_t c0, uint64_t c1, uint64_t c2, uint64_t c3
 {
     const uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
     const uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
-#pragma unroll
+#pragma unroll 1 // rolled: the unrolled rounds cost a wave per SIMD in registers
     for (int r = 0; r < 10; ++r) {
         if (r > 0) {
             k0 += W0;
