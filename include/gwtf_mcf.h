@@ -8,7 +8,7 @@
  * microbatches at a time (its memory, Sec. III) and costs c_i to run one;
  * sending from node i of stage k to node j of stage k+1 costs the delay
  * d(i, j).  One microbatch is one unit of flow (Sec. V-A).  The solver finds,
- * per instance, the largest number of microbatches F the stages can carry
+ * per instance, the most microbatches F the stages can carry
  * (capped by the data node's supply) and, among flows of that value, one of
  * minimum total cost sum f(i, j) * d(i, j) (Eq. 2).  Eq. 1's compute halves
  * summed along a microbatch's closed route equal the sum of the compute costs
@@ -48,8 +48,9 @@ enum {
     GWTF_INST_OK = 0,
     GWTF_INST_BAD_INPUT = 1, /* a capacity, cost or supply < 0, or an arc cost < -1 */
     GWTF_INST_OVERFLOW = 2,  /* (2*S*n + 3) * max cost >= 2^29: labels could leave int32 */
-    GWTF_INST_NOT_CONVERGED = 3 /* churn re-solve only: stopped at its safety limit of 2^20
-                                   label-correcting rounds (not expected on valid input) */
+    GWTF_INST_NOT_CONVERGED = 3 /* churn re-solve only: its final augmenting phase stopped at
+                                   the safety limit of 2^20 label-correcting rounds (not
+                                   expected on valid input) */
 };
 
 /* Solver pass that produced an instance's result (gwtf_mcf_get_passes). */
@@ -265,9 +266,9 @@ gwtf_status_t gwtf_mcf_whatif_best(gwtf_mcf_t *h, int32_t count, const int64_t *
                                    const int64_t *total_cost, const int32_t *status, int64_t first,
                                    int32_t merge, int64_t *best);
 
-/* ---- Warm-started re-solve after churn (paper Sec. VI: nodes leave and
- * link delays change between iterations, and the flow problem is solved
- * again on the changed instance) ----
+/* ---- Warm-started re-solve after churn (paper Sec. VI: nodes join and
+ * leave between iterations; re-solving from the previous optimum instead of
+ * from zero is this library's extension, the paper does not describe it) ----
  *
  * Solves every instance of `b` (same layout, checks and per-instance status
  * as gwtf_mcf_solve_batch; b->batch <= max_batch) starting from a feasible
@@ -276,15 +277,17 @@ gwtf_status_t gwtf_mcf_whatif_best(gwtf_mcf_t *h, int32_t count, const int64_t *
  * (F, cost) equals a cold solve's: the start flow loses whole source-to-sink
  * paths until it respects the new capacities, the missing links and the
  * supply; negative residual cycles are cancelled (the flow is then of least
- * cost for its value); shortest augmenting paths finish the solve.
+ * cost for its value); shortest augmenting paths finish the solve.  Should
+ * the cancelling stop at its safety limit of 2^20 label-correcting rounds,
+ * the instance restarts from the zero flow, which is the cold solve.
  *
  * The start flow is in the layout of gwtf_mcf_get_flows: node_flow
  * [.][S][n], arc_flow [.][S-1][n][n] (NULL iff S == 1), src_flow and
  * snk_flow [.][n], with one entry for the whole batch when per_instance == 0
  * and one per instance otherwise.  It must be conserved (a node's flow equals
  * its inflow and its outflow; stage 0 is fed by src_flow, stage S-1 drains
- * into snk_flow) with every value in [0, 2^29); otherwise the instance gets
- * GWTF_INST_BAD_INPUT.  Its capacities and links need not match the new
+ * into snk_flow) with every value in [0, 2^29) and a value (sum of src_flow)
+ * below 2^29; otherwise the instance gets GWTF_INST_BAD_INPUT.  Its capacities and links need not match the new
  * instance. */
 typedef struct {
     const int32_t *node_flow, *arc_flow, *src_flow, *snk_flow;

@@ -9,8 +9,8 @@
  * library (it does not include the library's header), and it computes
  * everything in 64-bit integers.
  *
- * What it computes (paper Sec. V-A, Eq. 2, and Sec. IV "largest number of
- * microbatches at the lowest global cost"): on the flow network
+ * What it computes (paper Sec. V-A, Eq. 2, and Sec. IV: route as many
+ * microbatches as possible, then at the least total delay): on the flow network
  *
  *     s0 -> s                     capacity supply,   cost 0
  *     s  -> in(0,i)               capacity infinite, cost src_cost[i]

@@ -1,6 +1,7 @@
-// Warm-started re-solve of churn variants (paper Sec. VI: nodes leave and
-// link delays change between iterations; the solver is re-run on the changed
-// instance).  Each instance starts from a feasible flow of the same shape,
+// Warm-started re-solve of churn variants.  The churn is the paper's (Sec.
+// VI: nodes join and leave between iterations); re-solving the exact optimum
+// from the previous one is this library's extension, not a method of the
+// paper.  Each instance starts from a feasible flow of the same shape,
 // typically the optimum of the instance before the churn, and reaches the
 // same (F, cost) as a cold solve:
 //
@@ -161,7 +162,7 @@ __device__ int32_t strip_path(Inst &I, int k0, int i0, int k1, int i1, int32_t w
 
 struct Shared {
     int32_t flag[3];
-    int32_t found, bad, err, mx;
+    int32_t found, bad, strip_bad, err, mx;
     int32_t F;
     unsigned long long cost;
 };
@@ -193,8 +194,10 @@ __device__ bool find_cycle(Inst &I, Shared &sh, int L)
 // Label correction to a fixed point.  from_source: shortest distances from
 // s (no negative cycle may exist); otherwise every label starts at 0 (a
 // virtual root joined to all vertices) and the pass stops at the first
-// predecessor cycle.  Returns 0 converged, 1 cycle found, 2 round cap hit.
-__device__ int correct_labels(Inst &I, Shared &sh, bool from_source, int32_t bound, int L, int64_t &rounds)
+// predecessor cycle.  Returns 0 converged, 1 cycle found, 2 once `rounds`
+// has grown by the round cap since `phase_start`.
+__device__ int correct_labels(Inst &I, Shared &sh, bool from_source, int32_t bound, int L, int64_t &rounds,
+                              int64_t phase_start)
 {
     const int tid = threadIdx.x, nt = blockDim.x, V = I.V;
     for (int v = tid; v < V; v += nt) {
@@ -221,7 +224,7 @@ __device__ int correct_labels(Inst &I, Shared &sh, bool from_source, int32_t bou
         const int fl = sh.flag[it % 3];
         ++rounds;
         if (!(fl & 1)) return 0;
-        if (rounds >= kChurnRoundCap) return 2;
+        if (rounds - phase_start >= kChurnRoundCap) return 2;
         if (!from_source && ((fl & 2) || (it & 3) == 3) && find_cycle(I, sh, L)) return 1;
     }
 }
@@ -255,6 +258,7 @@ __global__ void __launch_bounds__(kChurnThreads) churn_kernel(ChurnParams p)
 
     if (tid == 0) {
         sh.bad = 0;
+        sh.strip_bad = 0;
         sh.err = 0;
         sh.mx = 0;
         sh.cost = 0;
@@ -346,20 +350,23 @@ __global__ void __launch_bounds__(kChurnThreads) churn_kernel(ChurnParams p)
                 ++removed;
             }
             sh.F = int32_t(F);
-            sh.bad = ok ? 0 : 1;
+            sh.strip_bad = ok ? 0 : 1;
         }
         __syncthreads();
-        if (sh.bad) status = GWTF_INST_BAD_INPUT;
+        if (sh.strip_bad) status = GWTF_INST_BAD_INPUT;
     }
 
     const int32_t bound = int32_t((V - 1) * int64_t(sh.mx));
     const int L = 32 - __clz(V);
-    // 2. cancel
+    // 2. cancel.  Should it stop at its round cap or meet a cycle it cannot
+    // push (neither happens on valid input), the instance restarts from the
+    // zero flow: step 3 alone is then the cold solve and reaches its result.
+    bool restart = false;
     while (status == GWTF_INST_OK) {
-        const int r = correct_labels(I, sh, false, bound, L, rounds);
+        const int r = correct_labels(I, sh, false, bound, L, rounds, 0);
         if (r == 0) break;
         if (r == 2) {
-            status = GWTF_INST_NOT_CONVERGED;
+            restart = true;
             break;
         }
         if (tid == 0) {
@@ -384,11 +391,26 @@ __global__ void __launch_bounds__(kChurnThreads) churn_kernel(ChurnParams p)
         }
         __syncthreads();
         ++cycles;
-        if (sh.err) status = GWTF_INST_NOT_CONVERGED;
+        if (sh.err) {
+            restart = true;
+            break;
+        }
     }
+    if (restart) {
+        for (int e = tid; e < links; e += nt) I.af[e] = 0;
+        for (int e = tid; e < Sn; e += nt) I.nf[e] = 0;
+        for (int i = tid; i < n; i += nt) I.sf[i] = I.tf[i] = 0;
+        __syncthreads();
+        if (tid == 0) {
+            sh.F = 0;
+            sh.err = 0;
+        }
+        __syncthreads();
+    }
+    const int64_t augment_start = rounds;
     // 3. augment
     while (status == GWTF_INST_OK && sh.F < supply) {
-        if (correct_labels(I, sh, true, bound, L, rounds) == 2) {
+        if (correct_labels(I, sh, true, bound, L, rounds, augment_start) == 2) {
             status = GWTF_INST_NOT_CONVERGED;
             break;
         }

@@ -1,6 +1,7 @@
-"""GPU parity of the warm-started churn re-solve (paper Sec. VI: the flow
-problem is solved again after nodes leave and link delays change) through
-the C ABI, against the oracle's cold solve of the changed instances.
+"""GPU parity of the warm-started churn re-solve (the churn of paper Sec. VI:
+nodes leave and link delays change; re-solving from the previous optimum is
+the library's extension) through the C ABI, against the oracle's cold solve
+of the changed instances.
 
 (F, cost, status) must match the oracle exactly.  The returned flows must
 pass the optimality certificate under the oracle's potentials: any optimal
@@ -147,6 +148,36 @@ def test_churn_bad_start_and_bad_values():
         assert F[b] == 0 and cost[b] == 0
         assert all(not out[k][b].any() for k in FLOW_KEYS)
     keep = [0, 5, 6, 7]
+    np.testing.assert_array_equal(status[keep], ref["status"][keep])
+    np.testing.assert_array_equal(F[keep], ref["F"][keep])
+    np.testing.assert_array_equal(cost[keep], ref["cost"][keep])
+
+
+def test_churn_start_value_sum_limit_multiwave():
+    """Shape 8 x 24 (386 vertices: 256-thread workgroups of four waves).
+    Instance 2 starts from a conserved flow whose values are each below
+    2^29 but whose source flows sum to 2^29 + 2: the strip step refuses it
+    (GWTF_INST_BAD_INPUT) while the other waves of the workgroup still read
+    the input checks' flag.  Instance 4 starts from a sum of 2^29 - 2, which
+    is accepted and stripped down to the new capacities."""
+    S, n, B = 8, 24, 6
+    prev = W.random_small(B, S, n, seed=78, cap_hi=4, cost_hi=30, supply_hi=40)
+    var = W.random_small(B, S, n, seed=79, cap_hi=4, cost_hi=30, supply_hi=40)
+    p = oracle.solve(prev)
+    start = {k: p[k].copy() for k in FLOW_KEYS}
+    for b, unit in ((2, (1 << 28) + 1), (4, (1 << 28) - 1)):
+        for k in FLOW_KEYS:
+            start[k][b] = 0
+        for i in (0, 1):
+            start["node_flow"][b, :, i] = unit
+            start["arc_flow"][b, :, i, i] = unit
+            start["src_flow"][b, i] = unit
+            start["snk_flow"][b, i] = unit
+    say("churn: start-flow value sum at the 2^29 limit, 8 x 24")
+    F, cost, status, out, _ = churn(var, start)
+    ref = oracle.solve(var)
+    assert status[2] == mcf.GWTF_INST_BAD_INPUT and F[2] == 0 and cost[2] == 0
+    keep = [0, 1, 3, 4, 5]
     np.testing.assert_array_equal(status[keep], ref["status"][keep])
     np.testing.assert_array_equal(F[keep], ref["F"][keep])
     np.testing.assert_array_equal(cost[keep], ref["cost"][keep])
