@@ -93,28 +93,33 @@ KERNEL_SYMBOLS = {1: "solve_pipe_kernel", 2: "solve_kernel_lds", 3: "solve_grid_
                   5: "solve_small_kernel"}
 
 
-def stored_oracle_baseline(config: int):
-    """The oracle's time on a workload too long to re-run inside a bench
-    (one instance of c5 takes about 16 minutes on one core), as recorded when
-    its stored optimum was produced."""
-    path = os.path.join(ROOT, "tests", "golden", f"c{config}_oracle.json")
-    rec = json.load(open(path))
-    return {"value": rec["B"] / rec["oracle_seconds"], "unit": "instances/s",
-            "cores": rec["oracle_threads"], "kind": "oracle",
-            "sample": f"all {rec['B']} instance(s), {rec['oracle_seconds']:.0f} s on "
-                      f"{rec['oracle_threads']} thread(s), timed when tests/golden/c{config}_oracle.json "
-                      f"was written (not re-run by this bench)"}
+def cpu_model() -> str:
+    """The host CPU's model name from /proc/cpuinfo."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
-def cpu_baseline(batch, budget_s: float, threads: int):
-    """The oracle on the host cores, on a bounded prefix of the workload."""
+def host_threads() -> int:
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return max(1, min(threads, os.cpu_count() or 1))
+
+
+def oracle_rate(batch, budget_s: float, threads: int):
+    """The oracle on `threads` host threads over a growing prefix of the
+    batch until `budget_s` is spent: (instances done, seconds, arc scans,
+    threads used)."""
     import numpy as np
 
     import oracle
     import oracle.located
 
     solve = oracle.located.solve if hasattr(batch, "location") else oracle.solve
-    done, t_used, scans = 0, 0.0, 0
+    done, t_used, scans, used = 0, 0.0, 0, threads
     chunk = max(1, threads)
     while done < batch.B and t_used < budget_s:
         idx = list(range(done, min(batch.B, done + chunk)))
@@ -125,36 +130,111 @@ def cpu_baseline(batch, budget_s: float, threads: int):
         scans += int(np.sum(r["arc_scans"]))
         done += len(idx)
         used = r["threads"]
+    return done, t_used, scans, used
+
+
+def cpu_baseline(batch, budget_s: float, threads: int):
+    """The oracle on the host cores, on a bounded prefix of the workload:
+    all threads for two thirds of the budget, one thread for the rest."""
+    done, t_used, scans, used = oracle_rate(batch, budget_s * 2 / 3, threads)
+    d1, t1, s1, _ = oracle_rate(batch, budget_s / 3, 1)
     return {"value": done / t_used, "unit": "instances/s", "cores": used, "kind": "oracle",
             "sample": f"first {done} of {batch.B} instances of the same workload, "
                       f"{t_used:.1f} s wall on {used} threads (one instance per thread)",
-            "arc_scans_per_s": scans / t_used}
+            "arc_scans_per_s": scans / t_used,
+            "one_core": {"value": d1 / t1, "unit": "instances/s", "arc_scans_per_s": s1 / t1,
+                         "sample": f"first {d1} instances, {t1:.1f} s on 1 thread"},
+            "cpu_model": cpu_model(), "os_cpu_count": os.cpu_count()}
 
 
-def roofline_for(main_pass, relax, kernel_s, traffic, kernel, floor_bytes=None):
-    """Integer-ALU roofline for the packed pass (costs in registers).  For
-    the pipelined and grid passes, the HBM roofline of the algorithmic floor
-    of a sweep-based method: 12 B per residual arc, one sweep of every
-    residual arc per augmenting path.  Those passes hold their link costs on
-    chip, so 12 B per relaxation they actually perform is reported beside it
-    as counted work (it can exceed the HBM peak: those bytes never leave the
-    chip).  The other passes stream their arcs: 12 B per counted relaxation."""
+def cpu_baseline_single(batch, budget_s: float):
+    """One huge instance: the oracle solves it on one thread only (its
+    shortest-path searches are sequential), so the bounded sample is the same
+    instance with the data node's supply capped at A units, i.e. its first A
+    augmenting paths; the rate is scaled to the whole instance by its
+    augmenting paths (one unit each here: the capped solve finds the same
+    first paths).  The time of a complete solve of this instance, stored when
+    its optimum was written, is reported beside it."""
+    import numpy as np
+
+    import oracle
+
+    full = json.load(open(os.path.join(ROOT, "tests", "golden", "c5_oracle.json")))
+    paths = int(full["augmentations"][0])
+    # about 0.25-0.35 s per augmenting path on one core of the test hosts
+    units = int(max(8, min(256, budget_s / 0.3)))
+    sub = batch.subset([0])
+    sub.supply = np.full_like(sub.supply, units)
+    t0 = time.perf_counter()
+    r = oracle.solve(sub, nthreads=1, flows=False, potentials=False)
+    t_used = time.perf_counter() - t0
+    got = int(r["F"][0])
+    est_s = t_used / max(1, got) * paths
+    return {"value": 1.0 / est_s, "unit": "instances/s", "cores": 1, "kind": "oracle",
+            "sample": f"the same instance with its supply capped at {units} units: {got} augmenting paths "
+                      f"in {t_used:.1f} s on 1 thread (graph build included), scaled to the instance's "
+                      f"{paths} paths = {est_s:.0f} s per solve",
+            "stored_full_solve_s": full["oracle_seconds"], "stored_full_solve_threads": full["oracle_threads"],
+            "cpu_model": cpu_model(), "os_cpu_count": os.cpu_count()}
+
+
+def roofline_for(main_pass, relax, kernel_s, traffic, kernel):
+    """Integer-ALU roofline for the packed pass (costs in registers); HBM
+    roofline, 12 B per counted relaxation, for the passes that stream their
+    arcs.  The stage-pipelined passes use latency_roofline instead."""
     if main_pass == 5:
         achieved = OPS_PER_RELAX * relax / kernel_s / 1e12
         return {"bound": "alu", "achieved": achieved, "peak": ALU_PEAK_TOPS, "unit": "Tops/s",
                 "frac": achieved / ALU_PEAK_TOPS, "traffic": traffic, "traffic_unit": "GB/s",
                 "kernel": kernel, "kernel_ms": kernel_s * 1e3}
     counted = BYTES_PER_RELAX * relax / kernel_s / 1e9
-    if main_pass in (1, 3) and floor_bytes is not None:
-        achieved = floor_bytes / kernel_s / 1e9
-        return {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": achieved / HBM_PEAK_GBS, "traffic": traffic, "kernel": kernel,
-                "kernel_ms": kernel_s * 1e3,
-                "algorithmic_bytes": "12 B x residual arcs x augmenting paths (one sweep per path)",
-                "counted_work": {"achieved": counted, "frac": counted / HBM_PEAK_GBS, "unit": "GB/s",
-                                 "basis": "12 B per relaxation performed; link costs stay on chip"}}
     return {"bound": "hbm", "achieved": counted, "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": counted / HBM_PEAK_GBS, "traffic": traffic, "kernel": kernel, "kernel_ms": kernel_s * 1e3}
+
+
+def pipeline_depth(main_pass, S):
+    """Owners a label passes through in the first iteration of a search:
+    the register pass gives each wave two stages above 16 stages (one
+    below), the grid pass one stage per group of workgroups."""
+    if main_pass == 1:
+        return -(-S // (2 if S > 16 else 1))
+    return S
+
+
+def latency_roofline(main_pass, stats, S, kernel_s, handoff, traffic, kernel):
+    """Critical-path model of the stage-pipelined passes.  Iteration t of a
+    search at pipeline position k waits for position k-1 at iteration t and
+    position k+1 at iteration t-1, so a search that converges at iteration
+    T_s costs (H - 1) + 2 (T_s - 1) sequential hand-offs, H the pipeline
+    depth.  The unit is such a hop; the floor of one hop is the bare hand-off
+    latency measured on this device in the same run (LDS between two waves
+    for the register pass, device-scope between neighbouring stages'
+    workgroups for the grid pass).  achieved = hops on the launch's critical
+    path / kernel time (the batch's slowest instance for the register pass,
+    which solves one instance per workgroup); frac = that time floor / the
+    measured time."""
+    import numpy as np
+
+    H = pipeline_depth(main_pass, S)
+    rounds = stats[:, 1].astype(np.float64)
+    searches = (stats[:, 8] if main_pass == 3 else stats[:, 0]).astype(np.float64)
+    hops = searches * (H - 1) + 2.0 * (rounds - searches)
+    crit = float(hops.max())
+    floor_ns = handoff["lds_wave_ns"] if main_pass == 1 else handoff["device_neighbour_ns"]
+    if floor_ns <= 0:
+        return {"bound": "latency", "achieved": None, "peak": None, "frac": None, "traffic": traffic,
+                "kernel": kernel, "kernel_ms": kernel_s * 1e3, "note": "hand-off calibration failed"}
+    achieved = crit / kernel_s
+    peak = 1e9 / floor_ns
+    return {"bound": "latency", "achieved": achieved, "peak": peak, "unit": "pipeline hops/s",
+            "frac": achieved / peak, "traffic": traffic, "traffic_unit": "GB/s", "kernel": kernel,
+            "kernel_ms": kernel_s * 1e3,
+            "model": {"pipeline_depth": H, "searches": float(searches[int(hops.argmax())]),
+                      "iterations": float(rounds[int(hops.argmax())]), "critical_hops": crit,
+                      "hop_floor_ns": floor_ns,
+                      "hop_floor": "LDS wave-to-wave hand-off" if main_pass == 1
+                      else "device-scope hand-off between neighbouring stages' workgroups",
+                      "ns_per_hop": kernel_s * 1e9 / crit, "handoff_calibration_ns": handoff}}
 
 
 # VALU issue peak: each CU issues at most one wave64 vector instruction per
@@ -390,9 +470,7 @@ def run_churn(args):
                      "kernel": "churn_kernel (one launch per step)"},
     }
     if args.cpu_budget > 0:
-        threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-        threads = max(1, min(threads, os.cpu_count() or 1))
-        line["cpu_baseline"] = cpu_baseline(var, args.cpu_budget, threads)
+        line["cpu_baseline"] = cpu_baseline(var, args.cpu_budget, host_threads())
     solver.close()
     print(json.dumps(line), flush=True)
 
@@ -597,6 +675,35 @@ def main():
     res_arcs = 2 * (1 + 2 * n_ + S_ * n_ + (S_ - 1) * n_ * n_)  # residual arcs, every link present
     floor_bytes = BYTES_PER_RELAX * res_arcs * float(stats[:, 0].sum())
     floor_gbs = floor_bytes / kernel_s / 1e9
+    kernel = KERNELS.get(main_pass, "?") + PASS_LAUNCHES.get(main_pass, " (one launch per step)")
+    traffic = measured_traffic(KERNEL_SYMBOLS.get(main_pass, "?"),
+                               f"c{args.config}_located" if args.located else args.config, kernel_s)
+    if main_pass in (1, 3):
+        # stage-pipelined passes: link costs stay on chip, the hand-offs
+        # between stages bound them
+        from paper_2509_21221_amd.mcf import gwtf_mcf_calibrate_handoff
+
+        handoff = gwtf_mcf_calibrate_handoff(0, stream.cuda_stream, max(1, -(-batch.n // 128)) if main_pass == 3
+                                             else 4)
+        roof = latency_roofline(main_pass, stats, batch.S, kernel_s, handoff, traffic, kernel)
+        if not args.located:
+            # The 12 B per residual arc of a sweep-based method, one sweep per
+            # augmenting path, over the same time: what a CSR-streaming
+            # solver would need from HBM to match this speed.
+            counted = BYTES_PER_RELAX * relax / kernel_s / 1e9
+            roof["hbm_floor_equivalent"] = {
+                "achieved": floor_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": floor_gbs / HBM_PEAK_GBS,
+                "bytes_per_launch": floor_bytes,
+                "basis": "12 B x residual arcs x augmenting paths (one sweep per path)",
+                "counted_work": {"achieved": counted, "frac": counted / HBM_PEAK_GBS, "unit": "GB/s",
+                                 "basis": "12 B per relaxation performed; link costs stay on chip"}}
+    else:
+        roof = roofline_for(main_pass, relax, kernel_s, traffic, kernel)
+        # The same 12 B per residual arc at the floor of a sweep-based
+        # method: one pass over every residual arc per augmenting path.
+        roof["sweep_floor"] = {"achieved": floor_gbs, "frac": floor_gbs / HBM_PEAK_GBS,
+                               "unit": "GB/s", "bytes": floor_bytes}
+    roof["instances_per_pass"] = {KERNELS[p]: int((passes == p).sum()) for p in np.unique(passes)}
 
     line = {
         "metric": "MCMF instances solved/sec (+ arc relaxations/sec, % of HBM roofline)",
@@ -615,33 +722,26 @@ def main():
         "rounds_per_augmentation": float(stats[:, 1].sum() / max(1, stats[:, 0].sum())),
         "phase_ms_per_instance": {name: float(stats[:, col].mean()) / 1e6 for name, col in
                                   (("forward", 4), ("backward", 5), ("augment", 6), ("other", 7))},
-        "layer_steps_per_augmentation": {
-            "forward": float(stats[:, 8].sum() / max(1, stats[:, 0].sum())),
-            "backward": float(stats[:, 9].sum() / max(1, stats[:, 0].sum()))},
-        "roofline": {**roofline_for(main_pass, relax, kernel_s,
-                                    measured_traffic(KERNEL_SYMBOLS.get(main_pass, "?"), args.config, kernel_s),
-                                    KERNELS.get(main_pass, "?") + PASS_LAUNCHES.get(main_pass, " (one launch per step)"),
-                                    floor_bytes),
-                     "instances_per_pass": {KERNELS[p]: int((passes == p).sum()) for p in np.unique(passes)}},
+        "roofline": roof,
     }
-    if main_pass in (1, 3):
-        line["roofline"]["bytes_per_launch"] = floor_bytes
+    if main_pass == 3:
+        line["searches_per_instance"] = float(stats[:, 8].mean())
+        line["phase_ms_per_instance"] = {name: float(stats[:, col].mean()) / 1e6 for name, col in
+                                         (("label_iterations", 4), ("potentials_walks_augment", 6),
+                                          ("resets_barriers", 7))}
     else:
-        # The same 12 B per residual arc at the floor of a sweep-based
-        # method: one pass over every residual arc per augmenting path.
-        line["roofline"]["sweep_floor"] = {"achieved": floor_gbs, "frac": floor_gbs / HBM_PEAK_GBS,
-                                           "unit": "GB/s", "bytes": floor_bytes}
+        line["layer_steps_per_augmentation"] = {
+            "forward": float(stats[:, 8].sum() / max(1, stats[:, 0].sum())),
+            "backward": float(stats[:, 9].sum() / max(1, stats[:, 0].sum()))}
     if args.located:
         line["metric"] = "MCMF instances solved/sec, located form (+ relaxation operations/sec)"
+        line["factored_relaxation_ops_per_s"] = relax / kernel_s if main_pass == 3 else None
+        line["arc_relaxations_per_s"] = None if main_pass == 3 else line["arc_relaxations_per_s"]
         line["dense_link_relaxations_per_s"] = None
-        line["roofline"]["traffic"] = measured_traffic(KERNEL_SYMBOLS.get(main_pass, "?"),
-                                                       f"c{args.config}_located", kernel_s)
-    if args.cpu_budget > 0 and args.config == 5:
-        line["cpu_baseline"] = stored_oracle_baseline(args.config)
+    if args.cpu_budget > 0 and batch.B == 1:
+        line["cpu_baseline"] = cpu_baseline_single(batch, args.cpu_budget)
     elif args.cpu_budget > 0:
-        threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-        threads = max(1, min(threads, os.cpu_count() or 1))
-        line["cpu_baseline"] = cpu_baseline(batch, args.cpu_budget, threads)
+        line["cpu_baseline"] = cpu_baseline(batch, args.cpu_budget, host_threads())
     solver.close()
     print(json.dumps(line), flush=True)
 

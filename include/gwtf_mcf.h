@@ -120,7 +120,11 @@ gwtf_status_t gwtf_mcf_get_flows(gwtf_mcf_t *h, int32_t first, int32_t count,
  * flow-list (reverse-arc) relaxations, the nanoseconds the instance's
  * workgroup spent in forward sweeps, backward sweeps, augmentation with the
  * potential update, and the rest (label reset, sink update), then the
- * executed forward and backward layer steps (0 where not tracked). */
+ * executed forward and backward layer steps (0 where not tracked).  For
+ * instances of the grid pass (GWTF_PASS_GRID) the clocks are workgroup 0's:
+ * label iterations, then 0, then the potential update with the path walks
+ * and augmentations of a search (tied exits included), then the rest (label
+ * resets, barriers); column 8 counts the shortest-path searches. */
 gwtf_status_t gwtf_mcf_get_stats(gwtf_mcf_t *h, int32_t first, int32_t count, int64_t *stats);
 
 /* Which solver pass produced each instance of the last solve, into a caller
@@ -382,6 +386,31 @@ gwtf_status_t gwtf_mcf_simulate_heuristic(gwtf_mcf_t *h, const gwtf_mcf_batch_t 
                                           const gwtf_heur_config_t *cfg, const gwtf_heur_out_t *out);
 
 /* Frees the handle and its workspace after draining its stream; NULL-safe. */
+/* ---- Hand-off latency calibration ----
+ *
+ * Measures on `device` the least time one hop of the stage pipelines can
+ * take: the shortest paths of Sec. V-A are computed by passing labels from
+ * each stage's owner to the next stage's owner, and the register and grid
+ * passes each wait for such a hand-off per pipeline hop.  Runs three
+ * ping-pongs of 2000 round trips each, with nothing else around them, and
+ * writes the one-way latency in nanoseconds (half a round trip) to the HOST
+ * array latency_ns[3]:
+ *   [0] one wave to another of the same workgroup through LDS (the register
+ *       pass's mailboxes);
+ *   [1] workgroup 0 to workgroup `block_distance` of one cooperative launch
+ *       through device-scope atomic loads and stores (the grid pass's label
+ *       words; its neighbouring stages are `ceil(n/128)` workgroups apart);
+ *   [2] workgroup 0 to workgroup 8 (on the same XCD when workgroups are
+ *       dealt round robin over 8 XCDs).
+ * An entry is -1 if its bounded wait ran out.  Enqueued on hip_stream (NULL
+ * = the null stream), which it synchronises before returning; it allocates
+ * and frees 1 KB of device memory.  Errors: GWTF_ERR_INVALID_ARG for a NULL
+ * array, a bad device ordinal or block_distance outside [1, 15] or equal to
+ * 8; GWTF_ERR_DEVICE if the device has no cooperative launch or a HIP call
+ * fails (text in gwtf_mcf_last_error(NULL) of the calling thread). */
+gwtf_status_t gwtf_mcf_calibrate_handoff(int32_t device, void *hip_stream, int32_t block_distance,
+                                         double *latency_ns);
+
 void gwtf_mcf_destroy(gwtf_mcf_t *h);
 
 /* Text of the last error on this handle ("" if none); NULL handle gives the

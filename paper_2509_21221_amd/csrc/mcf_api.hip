@@ -365,6 +365,31 @@ extern "C" gwtf_status_t gwtf_mcf_solve_batch(gwtf_mcf_t *h, const gwtf_mcf_batc
 
 // ---- Solve without allocation ----
 //
+extern "C" gwtf_status_t gwtf_mcf_calibrate_handoff(int32_t device, void *hip_stream, int32_t block_distance,
+                                                    double *latency_ns)
+{
+    if (!latency_ns) return fail_thread(GWTF_ERR_INVALID_ARG, "latency_ns is NULL");
+    if (block_distance < 1 || block_distance > 15 || block_distance == 8)
+        return fail_thread(GWTF_ERR_INVALID_ARG, "block_distance outside [1, 15] or equal to 8");
+    int ndev = 0;
+    hipError_t e = hipGetDeviceCount(&ndev);
+    if (e != hipSuccess) return fail_thread(GWTF_ERR_DEVICE, "hipGetDeviceCount", e);
+    if (device < 0 || device >= ndev) return fail_thread(GWTF_ERR_INVALID_ARG, "bad device ordinal");
+    if ((e = hipSetDevice(device)) != hipSuccess) return fail_thread(GWTF_ERR_DEVICE, "hipSetDevice", e);
+    int coop = 0, clock_khz = 0;
+    if ((e = hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, device)) != hipSuccess)
+        return fail_thread(GWTF_ERR_DEVICE, "hipDeviceGetAttribute", e);
+    if (!coop) return fail_thread(GWTF_ERR_DEVICE, "device has no cooperative launch");
+    if (hipDeviceGetAttribute(&clock_khz, hipDeviceAttributeWallClockRate, device) != hipSuccess) clock_khz = 0;
+    (void)hipGetLastError();
+    double out[3];
+    if ((e = run_handoff_calibration(static_cast<hipStream_t>(hip_stream), clock_khz, block_distance, out)) !=
+        hipSuccess)
+        return fail_thread(GWTF_ERR_DEVICE, "hand-off calibration", e);
+    for (int q = 0; q < 3; ++q) latency_ns[q] = out[q];
+    return GWTF_OK;
+}
+
 // Workspace of gwtf_mcf_solve_batch_noalloc: one array per device, held
 // until the process ends.  In host code this name is only a host-side
 // stand-in; the device address comes from hipGetSymbolAddress, once per

@@ -153,4 +153,10 @@ struct HeurParams {
 size_t heuristic_lds_bytes(int S, int n, int max_slots);
 hipError_t launch_heuristic(const HeurParams &p, hipStream_t stream);
 
+// Hand-off latency calibration (mcf_calibrate.hip): one-way latencies in
+// ns of an LDS hand-off between two waves, and of device-scope hand-offs
+// between workgroups 0 and `neighbour` and between workgroups 0 and 8 of one
+// cooperative launch; -1 where a bounded wait ran out.  Synchronises `s`.
+hipError_t run_handoff_calibration(hipStream_t s, int clock_khz, int neighbour, double out_ns[3]);
+
 } // namespace gwtf

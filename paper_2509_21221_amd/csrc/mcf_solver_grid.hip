@@ -347,8 +347,11 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
         }
     }
 
-    long long F = 0, cost = 0, rounds = 0, augs = 0, my_relax = 0, my_pulls = 0;
+    long long F = 0, cost = 0, rounds = 0, augs = 0, my_relax = 0, my_pulls = 0, searches = 0;
     int pit = 0;
+    // workgroup 0's phase clocks: label iterations; the potential update with
+    // the path walks and augmentations; the rest (label resets, barriers)
+    uint64_t tick = wall_clock64(), clk_iter = 0, clk_aug = 0, clk_other = 0;
 
     // Labels of a fresh shortest-path search: buffer 0 holds them as the
     // output of iteration 0; buffer 1 gets a tag no reader awaits before
@@ -389,6 +392,7 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
     if (!timed_out && status == 0 && supply > 0) {
         reset_labels();
         timed_out = !bar.sync(&sh_ok, &sh_flag);
+        clk_other += lap(tick);
         while (!timed_out) {
             // ---- (1) label-correcting iterations, pipelined over the stages ----
             // Iteration t of stage k relaxes from stage k-1's output of the
@@ -675,6 +679,8 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                 break;
             }
             rounds += ld(&ctrl[kCtlStop]);
+            searches++;
+            clk_iter += lap(tick);
             final_key = ld(final_key_w);
             if (final_key == ~0ull) break; // sink unreachable: the flow is maximum
 
@@ -982,6 +988,7 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                 break;
             }
             }
+            clk_aug += lap(tick);
             if (quit) break;
             pit = Dt;
             if (F >= supply) break;
@@ -991,6 +998,7 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                 timed_out = true;
                 break;
             }
+            clk_other += lap(tick);
             if (sh_flag) break;
         }
     }
@@ -1029,7 +1037,13 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
         stats[1] = rounds;
         stats[2] = int64_t(ld(reinterpret_cast<unsigned long long *>(ctrl + kCtlRelax)) / uint64_t(n));
         stats[3] = int64_t(ld(reinterpret_cast<unsigned long long *>(ctrl + kCtlPulls)));
-        for (int x = 4; x < kStatsPerInstance; ++x) stats[x] = 0;
+        const double ns_per_tick = 1e6 / double(p.clock_khz > 0 ? p.clock_khz : 100000);
+        stats[4] = int64_t(double(clk_iter) * ns_per_tick);
+        stats[5] = 0;
+        stats[6] = int64_t(double(clk_aug) * ns_per_tick);
+        stats[7] = int64_t(double(clk_other) * ns_per_tick);
+        stats[8] = searches;
+        stats[9] = 0;
     }
 }
 

@@ -161,6 +161,8 @@ def load_library(path: str = LIB_PATH):
                                                     ctypes.POINTER(gwtf_heur_config_t),
                                                     ctypes.POINTER(gwtf_heur_out_t)]
         lib.gwtf_mcf_simulate_heuristic.restype = ctypes.c_int
+        lib.gwtf_mcf_calibrate_handoff.argtypes = [i32, vp, i32, ctypes.POINTER(ctypes.c_double)]
+        lib.gwtf_mcf_calibrate_handoff.restype = ctypes.c_int
         lib.gwtf_mcf_destroy.argtypes = [vp]
         lib.gwtf_mcf_destroy.restype = None
         lib.gwtf_mcf_last_error.argtypes = [vp]
@@ -222,6 +224,16 @@ def gwtf_mcf_solve_located(handle, batch: int, num_locations: int, node_cap: int
                                  location or None, latency or None, src_cost or None, snk_cost or None,
                                  supply or None, flow_value or None, total_cost or None, status or None)
     _check(load_library().gwtf_mcf_solve_located(ctypes.c_void_p(handle), ctypes.byref(b)), handle)
+
+
+def gwtf_mcf_calibrate_handoff(device: int = 0, hip_stream: int = 0, block_distance: int = 4):
+    """One-way hand-off latencies in ns: LDS wave to wave, device scope
+    between workgroups 0 and ``block_distance``, and between workgroups 0
+    and 8 (-1 where a bounded wait ran out)."""
+    out = (ctypes.c_double * 3)()
+    _check(load_library().gwtf_mcf_calibrate_handoff(device, ctypes.c_void_p(hip_stream or None), block_distance,
+                                                     out))
+    return {"lds_wave_ns": out[0], "device_neighbour_ns": out[1], "device_same_xcd_ns": out[2]}
 
 
 def gwtf_mcf_get_flows(handle, first: int, count: int, node_flow: int = 0, arc_flow: int = 0,

@@ -58,6 +58,7 @@ def test_null_handle_calls_fail_cleanly():
     assert lib.gwtf_mcf_get_flows(None, 0, 1, None, None, None, None, None) == mcf.GWTF_ERR_INVALID_ARG
     assert lib.gwtf_mcf_get_stats(None, 0, 1, None) == mcf.GWTF_ERR_INVALID_ARG
     assert lib.gwtf_mcf_get_passes(None, 0, 1, None) == mcf.GWTF_ERR_INVALID_ARG
+    assert lib.gwtf_mcf_calibrate_handoff(0, None, 4, None) == mcf.GWTF_ERR_INVALID_ARG
     assert lib.gwtf_mcf_whatif_expand(None, None, None, 0, 1, None) == mcf.GWTF_ERR_INVALID_ARG
     assert lib.gwtf_mcf_whatif_best(None, 1, None, None, None, 0, 0, None) == mcf.GWTF_ERR_INVALID_ARG
     assert lib.gwtf_mcf_resolve_churn(None, None, None, None, None) == mcf.GWTF_ERR_INVALID_ARG
