@@ -100,6 +100,31 @@ __device__ __forceinline__ uint64_t wave_min_key(bool has, int label, int idx0)
     return (uint64_t(m) << 32) | uint32_t(idx0 + __builtin_ctzll(__ballot(v == m)));
 }
 
+// Minimum over the four lanes l, l ^ 16, l ^ 32, l ^ 48 (the same position in
+// the four 16-lane rows of the wave), by the lane swaps of gfx950: every lane
+// gets the result.  A swap returns {first operand, second operand} after the
+// exchange, so lane l's partner sits in the second half of the pair when the
+// row bit is clear and in the first when it is set.
+__device__ __forceinline__ uint64_t row_group_min(uint64_t x)
+{
+    const int lane = threadIdx.x & 63;
+    uint32_t lo = uint32_t(x), hi = uint32_t(x >> 32);
+    {
+        const auto pl = __builtin_amdgcn_permlane32_swap(lo, lo, false, false);
+        const auto ph = __builtin_amdgcn_permlane32_swap(hi, hi, false, false);
+        const uint64_t o = (uint64_t((lane & 32) ? ph[0] : ph[1]) << 32) | ((lane & 32) ? pl[0] : pl[1]);
+        x = min(x, o);
+    }
+    lo = uint32_t(x), hi = uint32_t(x >> 32);
+    {
+        const auto pl = __builtin_amdgcn_permlane16_swap(lo, lo, false, false);
+        const auto ph = __builtin_amdgcn_permlane16_swap(hi, hi, false, false);
+        const uint64_t o = (uint64_t((lane & 16) ? ph[0] : ph[1]) << 32) | ((lane & 16) ? pl[0] : pl[1]);
+        x = min(x, o);
+    }
+    return x;
+}
+
 // Device-coherent accesses for data shared between workgroups.
 template <typename T> __device__ __forceinline__ T ld(const T *p)
 {
@@ -161,7 +186,9 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
     const int g = blockIdx.x, k = g / gp.slices, s = g % gp.slices;
     const int j0 = s * kGridNB, nown = min(kGridNB, n - j0);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int col = tid % kGridNB, rgrp = tid / kGridNB;
+    // rows of the previous stage rounded up to whole groups of 16 (the link
+    // sweep reads four rows at a time in each of four lane groups)
+    const int npad = (n + 15) & ~15;
     const bool has_prev = k >= 1, has_next = k + 1 < S;
 
     extern __shared__ __align__(16) unsigned char smem[];
@@ -194,8 +221,8 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
     };
     int *exrow = reinterpret_cast<int *>(take(4 * size_t(n)));   // last seen exit labels of stage k-1
     int *enrow = reinterpret_cast<int *>(take(4 * size_t(n)));   // entry labels of stage k+1
-    int *rowlist = reinterpret_cast<int *>(take(4 * size_t(n))); // rows of stage k-1 that dropped
-    uint32_t *rowkey = reinterpret_cast<uint32_t *>(take(4 * size_t(n))); // packed key per row
+    int *rowlist = reinterpret_cast<int *>(take(4 * size_t(npad))); // rows of stage k-1 that dropped
+    uint32_t *rowkey = reinterpret_cast<uint32_t *>(take(4 * size_t(npad))); // packed key per row
     int *din = reinterpret_cast<int *>(take(4 * kGridNB));
     int *dout = reinterpret_cast<int *>(take(4 * kGridNB));
     int *pout = reinterpret_cast<int *>(take(4 * kGridNB));
@@ -298,16 +325,22 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                 if (((rowmask >> (e / L)) & 1u) && ((colmask >> (e % L)) & 1u)) mx = max(mx, latl[e]);
         }
     } else if (has_prev) {
+        // Row i of the block holds the links from exit i of stage k-1 to the
+        // owned entries, column c at c ^ (((i >> 2) & 3) << 4): the four lane
+        // groups of the link sweep read rows of four different residues of
+        // i >> 2, hence four different 32-byte segments (no bank conflict).
+        // Rows n .. npad-1 are missing links.
         const int32_t *layer = gac + size_t(k - 1) * n * n;
-        for (int e = tid; e < n * kGridNB; e += kGridThreads) {
+        for (int e = tid; e < npad * kGridNB; e += kGridThreads) {
             const int i = e / kGridNB, c = e % kGridNB;
-            const int a = c < nown ? layer[size_t(i) * n + j0 + c] : -1;
+            const int a = (i < n && c < nown) ? layer[size_t(i) * n + j0 + c] : -1;
             bad |= a < -1;
             wide |= a > 65534;
             mx = max(mx, a);
-            cost16[e] = (a < 0 || a > 65534) ? kNoArc16 : uint16_t(a);
+            cost16[i * kGridNB + (c ^ (((i >> 2) & 3) << 4))] = (a < 0 || a > 65534) ? kNoArc16 : uint16_t(a);
         }
     }
+    for (int i = n + tid; i < npad; i += kGridThreads) rowkey[i] = kNoRowKey;
     if (has_next) {
         int32_t *rows = gaf + size_t(k) * n * n + size_t(j0) * n;
         for (int e = tid; e < nown * n; e += kGridThreads) st(&rows[e], 0);
@@ -404,13 +437,8 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
             // before it, whose tag differs.
             uint64_t final_key = ~0ull;
             bool converged = false;
+            int ring_t = 0; // the iteration whose arrival this workgroup still owes
             for (int t = 1; t <= 4 * V + 8; ++t) {
-                // The sink's label so far bounds which changes matter: a vertex
-                // whose reduced label reaches the sink's cannot lie on a
-                // shortest path to it, and its label is only an upper bound,
-                // which the potential update ignores.  The value read is at
-                // least the final one, so the test only counts more changes.
-                const unsigned long long sbest = ld(sinkbest_w);
                 if (located && has_prev && tid < L) mkey[tid] = ~0ull;
                 const uint32_t *ex_f = gp.ex + size_t(t & 1) * SN + size_t(has_prev ? k - 1 : 0) * n;
                 const uint32_t *en_b = gp.en + size_t((t - 1) & 1) * SN + size_t(has_next ? k + 1 : 0) * n;
@@ -445,6 +473,39 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                 };
                 int s0 = ld(&ctrl[kCtlStop]);
                 uint32_t a0 = ld(&ex_f[wi]), c0 = ld(&en_b[wi]);
+                if (tid == 0 && ring_t) {
+                    // Count this workgroup into iteration ring_t (its atomic's
+                    // round trip overlaps the reads just issued).  The last one
+                    // in learns whether any label changed; if none did, the
+                    // labels are a fixed point and it publishes the sink's key
+                    // and stop.
+                    const int slot = ring_t % gp.ring_slots;
+                    if (sh_key != ~0ull) {
+                        atomicMin(&gp.ring_key[slot], sh_key);
+                        atomicMin(sinkbest_w, sh_key);
+                        drain();
+                    }
+                    const unsigned mine = sh_changed ? 0x10001u : 1u;
+                    const unsigned total = atomicAdd(&gp.ring[slot], mine) + mine;
+                    if ((total & 0xffffu) == gridDim.x) {
+                        if ((total >> 16) == 0) {
+                            st(final_key_w, ld(&gp.ring_key[slot]));
+                            drain();
+                            st(&ctrl[kCtlStop], ring_t);
+                        } else {
+                            st(&gp.ring[slot], 0u);
+                            st(&gp.ring_key[slot], ~0ull);
+                        }
+                    }
+                    sh_key = ~0ull;
+                    sh_changed = 0;
+                }
+                // The sink's label so far bounds which changes matter: a vertex
+                // whose reduced label reaches the sink's cannot lie on a
+                // shortest path to it, and its label is only an upper bound,
+                // which the potential update ignores.  The value read is at
+                // least the final one, so the test only counts more changes.
+                const unsigned long long sbest = ld(sinkbest_w);
                 for (int spins = 0;; spins += 2) {
                     __builtin_amdgcn_s_sleep(1);
                     const int s1 = ld(&ctrl[kCtlStop]);
@@ -501,105 +562,132 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                 // the compacted list (which then holds the packed keys).
                 const bool packed = uint32_t(maxd) < kPackLimit;
                 const bool dense = packed && 2 * nrows > n;
+                if (tid == 0)
+                    my_relax += located ? (nrows > 0 ? (long long)nrows + (long long)nown * L : 0)
+                                        : (long long)nrows * nown;
                 if (located) {
                     // fold the dropped rows into their location's best key
                     if (dropped) atomicMin(&mkey[rowloc[tid]], (unsigned long long)pack_key(dnew, tid));
-                } else if (dropped) {
+                } else if (dropped && !dense) {
                     rowlist[base + __popcll(m & ((1ull << lane) - 1ull))] = packed ? int(rowkey[tid]) : tid;
                 }
-                __syncthreads();
+                // A dense sweep reads the row keys written before the last
+                // barrier; the list (padded to whole groups of 16) and the
+                // location keys need one more.
+                const int nlist = (nrows + 15) & ~15;
+                if (located || !dense) {
+                    if (!located && tid >= nrows && tid < nlist) rowlist[tid] = int(kNoRowKey);
+                    __syncthreads();
+                }
 
-                // links into this block's entries, from the rows that dropped
+                // Links into this block's entries, from the rows that dropped.
+                // Wave w owns columns 16w .. 16w+15 (lane & 15) and its four
+                // 16-lane groups (lane >> 4) take rows, or list entries,
+                // 16e + 4g .. 16e + 4g + 3; the swizzled block puts the four
+                // groups' costs in different banks, and their four partial
+                // minima meet by lane swaps, so no barrier separates the sweep
+                // from the node step below.
+                const int cq = wave * 16 + (lane & 15), gq = lane >> 4;
+                auto cost_at = [&](int i) { return cost16[i * kGridNB + (cq ^ (((i >> 2) & 3) << 4))]; };
                 uint64_t key = ~0ull;
                 if (located) {
                     // one candidate per location: its best row plus the latency
-                    // to this column's location (a quarter of the locations each)
-                    if (col < nown && nrows > 0) {
-                        const int cl = colloc[col];
-                        const int chunk = (L + kGridRowGroups - 1) / kGridRowGroups;
-                        const int lo = min(L, rgrp * chunk), hi = min(L, lo + chunk);
-                        for (int a = lo; a < hi; ++a) {
+                    // to this column's location (every fourth location per group)
+                    if (cq < nown && nrows > 0) {
+                        const int cl = colloc[cq];
+                        for (int a = gq; a < L; a += kGridRowGroups) {
                             const unsigned long long mk = mkey[a];
                             if (mk != ~0ull) key = min(key, (uint64_t)mk + (uint64_t(uint32_t(latl[a * L + cl])) << 32));
                         }
                     }
-                } else if (col < nown && nrows > 0) {
-                    // this thread's share: a quarter of the rows (dense) or of the list
-                    const int span = dense ? n : nrows;
-                    const int chunk = (((span + kGridRowGroups - 1) / kGridRowGroups) + 3) & ~3;
-                    const int lo = min(span, rgrp * chunk), hi = min(span, lo + chunk);
+                } else if (cq < nown && nrows > 0) {
+                    // exact 64-bit keys over this group's rows or entries, in
+                    // increasing order (the first row of a tie wins)
                     auto exact = [&]() {
+                        const int span = dense ? n : nrows;
                         int best = kInf, arg = -1;
-                        for (int e = lo; e < hi; ++e) {
-                            int i;
-                            if (dense) {
-                                if (rowkey[e] == kNoRowKey) continue;
-                                i = e;
-                            } else {
-                                i = packed ? (rowlist[e] & 511) : rowlist[e];
+                        for (int e0 = 4 * gq; e0 < span; e0 += 16)
+                            for (int u = 0; u < 4; ++u) {
+                                const int e = e0 + u;
+                                if (e >= span) break;
+                                int i;
+                                if (dense) {
+                                    if (rowkey[e] == kNoRowKey) continue;
+                                    i = e;
+                                } else {
+                                    i = packed ? (rowlist[e] & 511) : rowlist[e];
+                                }
+                                const uint16_t c = cost_at(i);
+                                const int cand = exrow[i] + int(c);
+                                const bool take_it = (c != kNoArc16) & (cand < best);
+                                best = take_it ? cand : best;
+                                arg = take_it ? i : arg;
                             }
-                            const uint16_t c = cost16[i * kGridNB + col];
-                            const int cand = exrow[i] + int(c);
-                            const bool take_it = (c != kNoArc16) & (cand < best);
-                            best = take_it ? cand : best;
-                            arg = take_it ? i : arg;
-                        }
                         return best < kInf ? pack_key(best, arg) : ~0ull;
                     };
                     if (packed) {
                         uint32_t best = ~0u;
-                        const uint16_t *cc = cost16 + col;
                         if (dense) {
-                            int e = lo;
-#pragma unroll 4
-                            for (; e + 4 <= hi; e += 4) {
+                            // rows 16e + 4g + u all share the swizzle g
+                            const uint16_t *cc = cost16 + (cq ^ (gq << 4));
+#pragma unroll 2
+                            for (int e = 4 * gq; e < npad; e += 16) {
                                 const uint4 kq = *reinterpret_cast<const uint4 *>(&rowkey[e]);
                                 const uint32_t c0 = cc[(e + 0) * kGridNB], c1 = cc[(e + 1) * kGridNB];
                                 const uint32_t c2 = cc[(e + 2) * kGridNB], c3 = cc[(e + 3) * kGridNB];
                                 best = min(best, min((c0 << 9) + kq.x, (c1 << 9) + kq.y));
                                 best = min(best, min((c2 << 9) + kq.z, (c3 << 9) + kq.w));
                             }
-                            for (; e < hi; ++e) best = min(best, (uint32_t(cc[e * kGridNB]) << 9) + rowkey[e]);
                         } else {
                             const uint32_t *kl = reinterpret_cast<const uint32_t *>(rowlist);
-                            int e = lo;
-#pragma unroll 4
-                            for (; e + 4 <= hi; e += 4) {
+#pragma unroll 2
+                            for (int e = 4 * gq; e < nlist; e += 16) {
                                 const uint4 kq = *reinterpret_cast<const uint4 *>(&kl[e]);
-                                const uint32_t c0 = cc[(kq.x & 511u) * kGridNB], c1 = cc[(kq.y & 511u) * kGridNB];
-                                const uint32_t c2 = cc[(kq.z & 511u) * kGridNB], c3 = cc[(kq.w & 511u) * kGridNB];
+                                const uint32_t c0 = cost_at(int(kq.x & 511u)), c1 = cost_at(int(kq.y & 511u));
+                                const uint32_t c2 = cost_at(int(kq.z & 511u)), c3 = cost_at(int(kq.w & 511u));
                                 best = min(best, min((c0 << 9) + kq.x, (c1 << 9) + kq.y));
                                 best = min(best, min((c2 << 9) + kq.z, (c3 << 9) + kq.w));
                             }
-                            for (; e < hi; ++e) best = min(best, (uint32_t(cc[(kl[e] & 511u) * kGridNB]) << 9) + kl[e]);
                         }
                         if (best < kNoRowKey) {
                             const int row = int(best & 511u);
                             // a missing link reads as cost 65535; if one won, redo exactly
-                            key = cc[row * kGridNB] != kNoArc16 ? pack_key(int(best >> 9), row) : exact();
+                            key = cost_at(row) != kNoArc16 ? pack_key(int(best >> 9), row) : exact();
                         }
                     } else {
                         key = exact();
                     }
                 }
-                red[rgrp * kGridNB + col] = key;
-                __syncthreads();
+                key = row_group_min(key);
 
-                // compute arcs and reverse links of the owned nodes
-                uint64_t skey = ~0ull;
+                // Reverse links of the owned exits, only when an entry label of
+                // stage k+1 dropped since the last pull (the lists change only
+                // between searches): the column's four lanes take every fourth
+                // list entry; the smallest (label, entry) wins, i.e. the first
+                // entry of a tie.
+                const bool own = cq < nown;
+                uint64_t pk = ~0ull;
+                if (own && has_next && pull) {
+                    const int lo = loff[cq], hi = lo + llen[cq];
+                    for (int e = lo + gq; e < hi; e += kGridRowGroups) {
+                        const int dj = enrow[lpart[e]];
+                        if (dj < kInf) pk = min(pk, pack_key(dj - lcost[e], e));
+                    }
+                    if (gq == 0) my_pulls += hi - lo;
+                }
+                if (has_next && pull) pk = row_group_min(pk);
+
+                // compute arcs of the owned nodes (group 0 of each column)
                 bool sink_has = false;
                 int sink_label = 0;
-                if (tid < nown) {
-                    const int c = tid, q = k * n + j0 + c;
-                    uint64_t kb = red[c];
-#pragma unroll
-                    for (int r = 1; r < kGridRowGroups; ++r) kb = min(kb, (uint64_t)red[r * kGridNB + c]);
+                if (own && gq == 0) {
+                    const int c = cq, q = k * n + j0 + c;
                     int di = din[c], dq = dout[c], pi = prin[c], po = prout[c];
                     const int di0 = di, dq0 = dq;
                     const int fl = flow[c], cp = cap[c], nc = ncost[c];
-                    if (kb != ~0ull && key_label(kb) < di) {
-                        di = key_label(kb);
-                        pi = int(uint32_t(kb));
+                    if (key != ~0ull && key_label(key) < di) {
+                        di = key_label(key);
+                        pi = int(uint32_t(key));
                     }
                     if (fl > 0 && dq < kInf && dq - nc < di) {
                         di = dq - nc;
@@ -609,20 +697,9 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                         dq = di + nc;
                         po = kPredSplit;
                     }
-                    // reverse links: only when an entry label of stage k+1 dropped
-                    // since the last pull (the lists change only between searches)
-                    if (has_next && pull) {
-                        const int lo = loff[c], hi = lo + llen[c];
-#pragma unroll 4
-                        for (int e = lo; e < hi; ++e) {
-                            const int j = lpart[e];
-                            const int dj = enrow[j];
-                            if (dj < kInf && dj - lcost[e] < dq) {
-                                dq = dj - lcost[e];
-                                po = j;
-                            }
-                        }
-                        my_pulls += hi - lo;
+                    if (pk != ~0ull && key_label(pk) < dq) {
+                        dq = key_label(pk);
+                        po = lpart[int(uint32_t(pk))];
                     }
                     if (fl > 0 && dq < kInf && dq - nc < di) {
                         di = dq - nc;
@@ -638,40 +715,16 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                     if (((di != di0) & (di - pin[c] < bound)) | ((dq != dq0) & (dq - pout[c] < bound))) sh_changed = 1;
                     if (k == S - 1) sink_has = dq < kInf, sink_label = dq + snkc[c];
                 }
-                // the sink's best key: per wave first (the owner threads fill
-                // waves 0 and 1), then one LDS atomic per wave
-                if (k == S - 1 && tid < kGridNB) {
-                    skey = wave_min_key(sink_has, sink_label, j0 + wave * 64);
+                // the sink's best key: per wave first (its owners are lanes
+                // 0-15, node index j0 + 16w + lane), then one LDS atomic per wave
+                if (k == S - 1) {
+                    const uint64_t skey = wave_min_key(sink_has, sink_label, j0 + wave * 16);
                     if (lane == 0 && skey != ~0ull) atomicMin(&sh_key, (unsigned long long)skey);
                 }
                 __syncthreads();
-                // Count this workgroup into iteration t.  The last one in
-                // learns whether any label changed; if none did, the labels
-                // are a fixed point and it publishes the sink's key and stop.
-                if (tid == 0) {
-                    const int slot = t % gp.ring_slots;
-                    if (sh_key != ~0ull) {
-                        atomicMin(&gp.ring_key[slot], sh_key);
-                        atomicMin(sinkbest_w, sh_key);
-                        drain();
-                    }
-                    const unsigned mine = sh_changed ? 0x10001u : 1u;
-                    const unsigned total = atomicAdd(&gp.ring[slot], mine) + mine;
-                    if ((total & 0xffffu) == gridDim.x) {
-                        if ((total >> 16) == 0) {
-                            st(final_key_w, ld(&gp.ring_key[slot]));
-                            drain();
-                            st(&ctrl[kCtlStop], t);
-                        } else {
-                            st(&gp.ring[slot], 0u);
-                            st(&gp.ring_key[slot], ~0ull);
-                        }
-                    }
-                    sh_key = ~0ull;
-                    sh_changed = 0;
-                    my_relax += located ? (nrows > 0 ? (long long)nrows + (long long)nown * L : 0)
-                                        : (long long)nrows * nown;
-                }
+                // This workgroup's arrival for iteration t goes out at the start
+                // of the next iteration, behind its first reads.
+                ring_t = t;
             }
             if (timed_out) break;
             if (!converged) {
@@ -1055,7 +1108,7 @@ __global__ void grid_ctrl_reset_kernel(int32_t *ctrl)
 size_t lds_fixed(int S, int n)
 {
     size_t o = align16(grid_pass_big_bytes(S, n));
-    for (int a = 0; a < 4; ++a) o = align16(o + 4 * size_t(n));
+    for (int a = 0; a < 4; ++a) o = align16(o + 4 * size_t((n + 15) & ~15));
     for (int a = 0; a < 13; ++a) o = align16(o + 4 * size_t(kGridNB));
     o = align16(o + 8 * size_t(kGridRowGroups) * kGridNB);
     return o;
@@ -1063,7 +1116,10 @@ size_t lds_fixed(int S, int n)
 
 } // namespace
 
-size_t grid_pass_big_bytes(int S, int n) { return std::max(size_t(n) * kGridNB * 2, size_t(4) * S * n); }
+size_t grid_pass_big_bytes(int S, int n)
+{
+    return std::max(size_t((n + 15) & ~15) * kGridNB * 2, size_t(4) * S * n);
+}
 
 size_t grid_pass_lds_bytes(int S, int n, int64_t list_slots)
 {
