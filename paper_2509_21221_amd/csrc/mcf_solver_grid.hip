@@ -241,6 +241,10 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
     int *lamt = reinterpret_cast<int *>(take(4 * size_t(gp.list_slots)));
     int16_t *lpart = reinterpret_cast<int16_t *>(take(2 * size_t(gp.list_slots)));
     int *scanbuf = reinterpret_cast<int *>(red); // ingest only; red holds >= kGridThreads ints
+    // during the label iterations: byte offset of each list entry's row in
+    // the cost block, swizzle included (row i's column c sits at byte
+    // rowoff ^ 2c); the path walk reuses the space afterwards
+    uint32_t *rowoff = reinterpret_cast<uint32_t *>(red);
 
     int *ctrl = gp.ctrl;
     unsigned long long *final_key_w = reinterpret_cast<unsigned long long *>(ctrl + kCtlFinalKey);
@@ -561,7 +565,8 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                 // dropped is swept densely by row index, otherwise through
                 // the compacted list (which then holds the packed keys).
                 const bool packed = uint32_t(maxd) < kPackLimit;
-                const bool dense = packed && 2 * nrows > n;
+                // (a listed row costs about half again a dense one)
+                const bool dense = packed && 3 * nrows > 2 * n;
                 if (tid == 0)
                     my_relax += located ? (nrows > 0 ? (long long)nrows + (long long)nown * L : 0)
                                         : (long long)nrows * nown;
@@ -569,14 +574,19 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                     // fold the dropped rows into their location's best key
                     if (dropped) atomicMin(&mkey[rowloc[tid]], (unsigned long long)pack_key(dnew, tid));
                 } else if (dropped && !dense) {
-                    rowlist[base + __popcll(m & ((1ull << lane) - 1ull))] = packed ? int(rowkey[tid]) : tid;
+                    const int at = base + __popcll(m & ((1ull << lane) - 1ull));
+                    rowlist[at] = packed ? int(rowkey[tid]) : tid;
+                    rowoff[at] = uint32_t((tid << 7) | (((tid >> 2) & 3) << 4)) << 1;
                 }
                 // A dense sweep reads the row keys written before the last
                 // barrier; the list (padded to whole groups of 16) and the
                 // location keys need one more.
                 const int nlist = (nrows + 15) & ~15;
                 if (located || !dense) {
-                    if (!located && tid >= nrows && tid < nlist) rowlist[tid] = int(kNoRowKey);
+                    if (!located && tid >= nrows && tid < nlist) {
+                        rowlist[tid] = int(kNoRowKey);
+                        rowoff[tid] = 0;
+                    }
                     __syncthreads();
                 }
 
@@ -640,11 +650,14 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                             }
                         } else {
                             const uint32_t *kl = reinterpret_cast<const uint32_t *>(rowlist);
+                            const unsigned char *cb = reinterpret_cast<const unsigned char *>(cost16);
+                            const uint32_t cq2 = uint32_t(cq) << 1;
+                            auto at = [&](uint32_t off) { return uint32_t(*reinterpret_cast<const uint16_t *>(cb + (off ^ cq2))); };
 #pragma unroll 2
                             for (int e = 4 * gq; e < nlist; e += 16) {
                                 const uint4 kq = *reinterpret_cast<const uint4 *>(&kl[e]);
-                                const uint32_t c0 = cost_at(int(kq.x & 511u)), c1 = cost_at(int(kq.y & 511u));
-                                const uint32_t c2 = cost_at(int(kq.z & 511u)), c3 = cost_at(int(kq.w & 511u));
+                                const uint4 oq = *reinterpret_cast<const uint4 *>(&rowoff[e]);
+                                const uint32_t c0 = at(oq.x), c1 = at(oq.y), c2 = at(oq.z), c3 = at(oq.w);
                                 best = min(best, min((c0 << 9) + kq.x, (c1 << 9) + kq.y));
                                 best = min(best, min((c2 << 9) + kq.z, (c3 << 9) + kq.w));
                             }
