@@ -829,95 +829,100 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                         return -1;
                     };
                     int from = first ? predt : next_tie();
-                    int len = 0;
-                    bool okw = false;
+                    int len = 0, state = 2; // 0 walking, 1 reached the data node, 2 invalid, 3 blocked
                     while (from >= 0) {
                         int kk = S - 1, i = from;
-                        bool at_exit = true, blocked = false, done = false;
-                        okw = from < n;
+                        bool at_exit = true;
+                        state = from < n ? 0 : 2;
                         len = 0;
-                        auto record = [&](int code) {
-                            if (lane == 0) {
-                                if (len < kPathLds) lpath[len] = code;
-                                else st(&gp.path[len], code);
+                        // Step s's arc code goes to lane s & 63 of `rec`; every 64
+                        // steps the wave stores them with one write.
+                        uint32_t rec = 0;
+                        auto flush = [&](int upto) {
+                            const int at = (upto - 1) / 64 * 64 + lane;
+                            if (at < upto) {
+                                if (at < kPathLds) lpath[at] = int(rec);
+                                else st(&gp.path[at], int(rec));
                             }
-                            ++len;
+                        };
+                        auto record = [&](int code) {
+                            rec = lane == (len & 63) ? uint32_t(code) : rec;
+                            if ((++len & 63) == 0) flush(len);
                         };
                         // One read per node visited: a compute arc and the link arc
                         // after it come from the same word (entry predecessor in the
                         // low half, exit predecessor in the high half).  A compute
                         // arc followed by the opposite one would be a cycle.
-                        while (okw && !done) {
+                        while (state == 0) {
                             if (len > 2 * SN + 4) {
-                                okw = false;
+                                state = 2;
                                 break;
                             }
                             const uint32_t word = __builtin_amdgcn_readfirstlane(uint32_t(all_pred[kk * n + i]));
                             const int pen = int(word & 0x7fffu) - 3, pex = int((word >> 16) & 0x7fffu) - 3;
-                            const bool men = (word & 0x8000u) != 0, mex = (word >> 31) != 0;
-                            const bool ex_link = pex >= 0 && pex < n && kk + 1 < S;
-                            const bool en_link = pen >= 0 && pen < n && kk >= 1;
+                            bool via_split = false;
                             if (at_exit) {
-                                if (mex) {
-                                    blocked = true;
+                                if (word >> 31) {
+                                    state = 3;
                                     break;
                                 }
-                                if (pex == kPredSplit) {
-                                    record(path_code(kArcSplitFwd, kk, i, 0));
-                                    if (men) {
-                                        blocked = true;
+                                if (pex != kPredSplit) {
+                                    // entry (kk+1, pex) -> exit (kk, i), against a link's flow
+                                    if (unsigned(pex) >= unsigned(n) || kk + 1 >= S) {
+                                        state = 2;
                                         break;
                                     }
-                                    if (pen == kPredSrc) {
-                                        done = true;
-                                    } else if (en_link) {
-                                        record(path_code(kArcLinkFwd, kk - 1, pen, i)); // exit (kk-1, pen) -> entry (kk, i)
-                                        kk = kk - 1;
-                                        i = pen;
-                                    } else {
-                                        okw = false;
-                                    }
-                                } else if (ex_link) {
-                                    record(path_code(kArcLinkRev, kk, i, pex)); // entry (kk+1, pex) -> exit (kk, i)
-                                    kk = kk + 1;
+                                    record(path_code(kArcLinkRev, kk, i, pex));
+                                    kk += 1;
                                     i = pex;
                                     at_exit = false;
-                                } else {
-                                    okw = false;
+                                    continue;
                                 }
-                            } else {
-                                if (men) {
-                                    blocked = true;
+                                record(path_code(kArcSplitFwd, kk, i, 0));
+                                via_split = true;
+                            }
+                            // at the entry of node (kk, i)
+                            if (word & 0x8000u) {
+                                state = 3;
+                                break;
+                            }
+                            if (pen == kPredSrc) {
+                                state = 1;
+                                break;
+                            }
+                            if (pen == kPredSplit) {
+                                // exit (kk, i) -> entry (kk, i) against the node's flow,
+                                // then the exit's own predecessor: a reverse link
+                                if (via_split || (word >> 31)) {
+                                    state = via_split ? 2 : 3;
                                     break;
                                 }
-                                if (pen == kPredSrc) {
-                                    done = true;
-                                } else if (pen == kPredSplit) {
-                                    record(path_code(kArcSplitRev, kk, i, 0));
-                                    if (mex) {
-                                        blocked = true;
-                                        break;
-                                    }
-                                    if (ex_link) {
-                                        record(path_code(kArcLinkRev, kk, i, pex)); // entry (kk+1, pex) -> exit (kk, i)
-                                        kk = kk + 1;
-                                        i = pex;
-                                    } else {
-                                        okw = false;
-                                    }
-                                } else if (en_link) {
-                                    record(path_code(kArcLinkFwd, kk - 1, pen, i)); // exit (kk-1, pen) -> entry (kk, i)
-                                    kk = kk - 1;
-                                    i = pen;
-                                    at_exit = true;
-                                } else {
-                                    okw = false;
+                                record(path_code(kArcSplitRev, kk, i, 0));
+                                if (unsigned(pex) >= unsigned(n) || kk + 1 >= S) {
+                                    state = 2;
+                                    break;
                                 }
+                                record(path_code(kArcLinkRev, kk, i, pex));
+                                kk += 1;
+                                i = pex;
+                                continue;
                             }
+                            if (unsigned(pen) >= unsigned(n) || kk < 1) {
+                                state = 2;
+                                break;
+                            }
+                            record(path_code(kArcLinkFwd, kk - 1, pen, i)); // exit (kk-1, pen) -> entry (kk, i)
+                            kk -= 1;
+                            i = pen;
+                            at_exit = true;
                         }
-                        if (!blocked) break;
+                        if (state != 3) {
+                            if (state == 1 && (len & 63)) flush(len);
+                            break;
+                        }
                         from = next_tie();
                     }
+                    const bool okw = state == 1;
                     if (lane == 0) {
                         // length -2: no exit left to try
                         sh_len = from < 0 ? -2 : (okw ? len : -1);
