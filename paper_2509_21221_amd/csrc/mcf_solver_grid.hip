@@ -10,28 +10,31 @@
 //    column block of the link layer that feeds them (all n exits of stage k-1
 //    by its NB entries) as 16-bit costs in LDS.  The launch is cooperative,
 //    one workgroup per CU, so every workgroup is resident.
-//  * Shortest paths come from a Jacobi label-correcting iteration.  In one
-//    iteration each workgroup relaxes the links into its entries from the
-//    exit labels of stage k-1 published by the previous iteration (only the
-//    rows whose label dropped since it last saw them), applies its nodes'
-//    compute arcs in both directions, pulls its exits' reverse links from the
-//    previous iteration's entry labels of stage k+1, and publishes its labels
-//    into the other half of a double buffer.  One grid barrier separates
-//    iterations; the iteration stops when no label changed anywhere.
+//  * Shortest paths come from a label-correcting iteration pipelined over the
+//    stages, with no grid barrier: iteration t of stage k relaxes the links
+//    from stage k-1's exit labels of the same iteration (only the rows whose
+//    label dropped since it last saw them), applies its nodes' compute arcs in
+//    both directions, pulls its exits' reverse links from stage k+1's entry
+//    labels of iteration t-1, and publishes its labels.  Every published word
+//    carries an iteration tag, so a reader waits on the words themselves.
+//    Convergence is counted on a ring of per-iteration arrival counters; the
+//    last arrival of an iteration in which no label below the sink's changed
+//    publishes the sink's key and a stop word.
 //  * Workgroup 0 (stage 0, which holds no link costs) stages all
 //    predecessors in its LDS, walks the augmenting path and finds its
 //    bottleneck; each owner then applies the path to its nodes and lists.
+//    The last stage's other exits that reach the sink at the same label are
+//    tried next, without a new search, while their tree paths stay usable.
 //
 // Memory ordering.  The L2 cache is private to each XCD, so every value one
 // workgroup writes for another (labels, predecessors, path, flows, control
 // words) moves through device-scope atomic loads and stores, which bypass
 // the non-coherent cache state, and no cache-wide write-back or invalidate is
-// needed: before a workgroup arrives at the grid barrier, each of its threads
-// waits for its own stores to complete.  The barrier itself is one arrival
-// counter and one epoch word; it also ORs a one-bit flag over the grid (used
-// for "some label changed"), and its wait is bounded: a barrier that does not
-// complete within the bound ends the solve with the internal-error status
-// instead of hanging the device.
+// needed.  The grid barrier (between a search and its augmentations) is one
+// arrival counter and one epoch word; it also ORs a one-bit flag over the
+// grid (used to report a fault), and its wait is bounded: a barrier that does
+// not complete within the bound ends the solve with the internal-error status
+// instead of hanging the device.  Every other wait is bounded the same way.
 #include "mcf_device.h"
 #include "mcf_grid.h"
 
