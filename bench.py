@@ -52,6 +52,9 @@ BYTES_PER_RELAX = 12
 # its roofline is arithmetic: an add and a min per link relaxation.
 ALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12
 OPS_PER_RELAX = 2
+# VALU issue peak: each CU issues at most one wave64 vector instruction per
+# cycle (four SIMDs of 16 lanes, four cycles per wave64 instruction).
+VALU_ISSUE_PEAK = 256 * 2.4e9
 
 WORKLOADS = {
     1: "c1: 1024 instances, S=4 x n=4, random costs U[1,100], supply 16",
@@ -62,11 +65,10 @@ WORKLOADS = {
 }
 
 
-def measured_traffic(kernel: str, config: int, kernel_s: float):
-    """HBM bytes per launch from the committed rocprofv3 counter summary of
-    this kernel on this workload, as GB/s over the measured launch time; None
-    when there is no summary or the kernel's sources changed since it was
-    taken."""
+def counter_record(kernel: str, config):
+    """The committed rocprofv3 counter record of this kernel on this workload
+    (profiles/<kernel>_<workload>_traffic.json), or None when there is none or
+    the kernel's sources changed since it was taken."""
     import hashlib
 
     tag = config if isinstance(config, str) else f"c{config}"
@@ -80,9 +82,31 @@ def measured_traffic(kernel: str, config: int, kernel_s: float):
         if not os.path.exists(full):
             return None
         h.update(open(full, "rb").read())
-    if h.hexdigest() != rec["kernel_sources_sha256"]:
+    return rec if h.hexdigest() == rec["kernel_sources_sha256"] else None
+
+
+def measured_traffic(kernel: str, config, kernel_s: float):
+    """HBM bytes per launch from the committed counter record, as GB/s over
+    the measured launch time; None without a current record."""
+    rec = counter_record(kernel, config)
+    return None if rec is None else rec["traffic_bytes_per_launch"] / kernel_s / 1e9
+
+
+def valu_issue(kernel: str, config, kernel_s: float):
+    """VALU wave-instructions per launch from the committed counter record
+    over the measured launch time, against the issue peak (one wave64 vector
+    instruction per CU per cycle: four SIMDs of 16 lanes, four cycles each);
+    None without a current record with SQ counters."""
+    rec = counter_record(kernel, config)
+    if rec is None or "sq_counters_per_launch" not in rec:
         return None
-    return rec["traffic_bytes_per_launch"] / kernel_s / 1e9
+    sq = rec["sq_counters_per_launch"]
+    achieved = sq["SQ_INSTS_VALU"] / kernel_s
+    return {"achieved": achieved, "peak": VALU_ISSUE_PEAK, "unit": "VALU wave-instructions/s",
+            "frac": achieved / VALU_ISSUE_PEAK,
+            "lds_bank_conflict_cycles_per_lds_instruction": sq["SQ_LDS_BANK_CONFLICT"] / max(1.0, sq["SQ_INSTS_LDS"]),
+            "salu_per_cu_cycle": sq["SQ_INSTS_SALU"] / kernel_s / VALU_ISSUE_PEAK,
+            "waves": sq["SQ_WAVES"], "counters": f"profiles/{kernel}_{config if isinstance(config, str) else 'c%d' % config}_traffic.json"}
 
 
 KERNELS = {1: "solve_pipe_kernel", 2: "solve_kernel (LDS state)", 3: "solve_grid_kernel",
@@ -178,14 +202,24 @@ def cpu_baseline_single(batch, budget_s: float):
             "cpu_model": cpu_model(), "os_cpu_count": os.cpu_count()}
 
 
-def roofline_for(main_pass, relax, kernel_s, traffic, kernel):
-    """Integer-ALU roofline for the packed pass (costs in registers); HBM
-    roofline, 12 B per counted relaxation, for the passes that stream their
-    arcs.  The stage-pipelined passes use latency_roofline instead."""
+def roofline_for(main_pass, relax, kernel_s, traffic, kernel, issue=None):
+    """The packed pass keeps its link costs in registers and issues vector
+    instructions back to back: its roofline is the VALU issue rate from the
+    committed counters (`issue`), with the two useful integer operations per
+    link relaxation (add, min) beside it; without counters, those operations
+    against the integer lane peak.  HBM roofline, 12 B per counted
+    relaxation, for the passes that stream their arcs.  The stage-pipelined
+    passes use latency_roofline instead."""
     if main_pass == 5:
-        achieved = OPS_PER_RELAX * relax / kernel_s / 1e12
-        return {"bound": "alu", "achieved": achieved, "peak": ALU_PEAK_TOPS, "unit": "Tops/s",
-                "frac": achieved / ALU_PEAK_TOPS, "traffic": traffic, "traffic_unit": "GB/s",
+        useful = OPS_PER_RELAX * relax / kernel_s / 1e12
+        ops = {"achieved": useful, "peak": ALU_PEAK_TOPS, "unit": "Tops/s", "frac": useful / ALU_PEAK_TOPS,
+               "basis": "an add and a min per link relaxation"}
+        if issue is not None:
+            return {"bound": "alu", "achieved": issue["achieved"], "peak": issue["peak"], "unit": issue["unit"],
+                    "frac": issue["frac"], "traffic": traffic, "traffic_unit": "GB/s", "kernel": kernel,
+                    "kernel_ms": kernel_s * 1e3, "issue": issue, "useful_ops": ops}
+        return {"bound": "alu", "achieved": useful, "peak": ALU_PEAK_TOPS, "unit": "Tops/s",
+                "frac": useful / ALU_PEAK_TOPS, "traffic": traffic, "traffic_unit": "GB/s",
                 "kernel": kernel, "kernel_ms": kernel_s * 1e3}
     counted = BYTES_PER_RELAX * relax / kernel_s / 1e9
     return {"bound": "hbm", "achieved": counted, "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -235,11 +269,6 @@ def latency_roofline(main_pass, stats, S, kernel_s, handoff, traffic, kernel):
                       "hop_floor": "LDS wave-to-wave hand-off" if main_pass == 1
                       else "device-scope hand-off between neighbouring stages' workgroups",
                       "ns_per_hop": kernel_s * 1e9 / crit, "handoff_calibration_ns": handoff}}
-
-
-# VALU issue peak: each CU issues at most one wave64 vector instruction per
-# cycle (four SIMDs of 16 lanes, four cycles per wave64 instruction).
-VALU_ISSUE_PEAK = 256 * 2.4e9
 
 
 def heuristic_counters():
@@ -388,7 +417,8 @@ def run_whatif(args):
         "arc_relaxations_per_s": relax / solve_s,
         "roofline": roofline_for(main_pass, relax, solve_s,
                                  measured_traffic(KERNEL_SYMBOLS.get(main_pass, "?"), f"whatif{args.whatif}", solve_s),
-                                 KERNELS.get(main_pass, "?") + " (one launch per step)"),
+                                 KERNELS.get(main_pass, "?") + " (one launch per step)",
+                                 valu_issue(KERNEL_SYMBOLS.get(main_pass, "?"), f"whatif{args.whatif}", solve_s)),
     }
     if args.cpu_budget > 0:
         threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
@@ -692,6 +722,8 @@ def main():
         handoff = gwtf_mcf_calibrate_handoff(0, stream.cuda_stream, max(1, -(-batch.n // 128)) if main_pass == 3
                                              else 4)
         roof = latency_roofline(main_pass, stats, batch.S, kernel_s, handoff, traffic, kernel)
+        roof["issue"] = valu_issue(KERNEL_SYMBOLS.get(main_pass, "?"),
+                                   f"c{args.config}_located" if args.located else args.config, kernel_s)
         if not args.located:
             # The 12 B per residual arc of a sweep-based method, one sweep per
             # augmenting path, over the same time: what a CSR-streaming
@@ -704,7 +736,9 @@ def main():
                 "counted_work": {"achieved": counted, "frac": counted / HBM_PEAK_GBS, "unit": "GB/s",
                                  "basis": "12 B per relaxation performed; link costs stay on chip"}}
     else:
-        roof = roofline_for(main_pass, relax, kernel_s, traffic, kernel)
+        roof = roofline_for(main_pass, relax, kernel_s, traffic, kernel,
+                            valu_issue(KERNEL_SYMBOLS.get(main_pass, "?"),
+                                       f"c{args.config}_located" if args.located else args.config, kernel_s))
         # The same 12 B per residual arc at the floor of a sweep-based
         # method: one pass over every residual arc per augmenting path.
         roof["sweep_floor"] = {"achieved": floor_gbs, "frac": floor_gbs / HBM_PEAK_GBS,

@@ -397,8 +397,8 @@ gwtf_status_t gwtf_mcf_simulate_heuristic(gwtf_mcf_t *h, const gwtf_mcf_batch_t 
  * array latency_ns[3]:
  *   [0] one wave to another of the same workgroup through LDS (the register
  *       pass's mailboxes);
- *   [1] workgroup 0 to workgroup `block_distance` of one cooperative launch
- *       through device-scope atomic loads and stores (the grid pass's label
+ *   [1] workgroup 0 to workgroup `block_distance` of one launch of 16
+ *       one-wave workgroups through device-scope atomic loads and stores (the grid pass's label
  *       words; its neighbouring stages are `ceil(n/128)` workgroups apart);
  *   [2] workgroup 0 to workgroup 8 (on the same XCD when workgroups are
  *       dealt round robin over 8 XCDs).
@@ -406,8 +406,8 @@ gwtf_status_t gwtf_mcf_simulate_heuristic(gwtf_mcf_t *h, const gwtf_mcf_batch_t 
  * = the null stream), which it synchronises before returning; it allocates
  * and frees 1 KB of device memory.  Errors: GWTF_ERR_INVALID_ARG for a NULL
  * array, a bad device ordinal or block_distance outside [1, 15] or equal to
- * 8; GWTF_ERR_DEVICE if the device has no cooperative launch or a HIP call
- * fails (text in gwtf_mcf_last_error(NULL) of the calling thread). */
+ * 8; GWTF_ERR_DEVICE if a HIP call fails (text in gwtf_mcf_last_error(NULL)
+ * of the calling thread). */
 gwtf_status_t gwtf_mcf_calibrate_handoff(int32_t device, void *hip_stream, int32_t block_distance,
                                          double *latency_ns);
 

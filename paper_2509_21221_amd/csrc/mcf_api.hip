@@ -376,10 +376,7 @@ extern "C" gwtf_status_t gwtf_mcf_calibrate_handoff(int32_t device, void *hip_st
     if (e != hipSuccess) return fail_thread(GWTF_ERR_DEVICE, "hipGetDeviceCount", e);
     if (device < 0 || device >= ndev) return fail_thread(GWTF_ERR_INVALID_ARG, "bad device ordinal");
     if ((e = hipSetDevice(device)) != hipSuccess) return fail_thread(GWTF_ERR_DEVICE, "hipSetDevice", e);
-    int coop = 0, clock_khz = 0;
-    if ((e = hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, device)) != hipSuccess)
-        return fail_thread(GWTF_ERR_DEVICE, "hipDeviceGetAttribute", e);
-    if (!coop) return fail_thread(GWTF_ERR_DEVICE, "device has no cooperative launch");
+    int clock_khz = 0;
     if (hipDeviceGetAttribute(&clock_khz, hipDeviceAttributeWallClockRate, device) != hipSuccess) clock_khz = 0;
     (void)hipGetLastError();
     double out[3];

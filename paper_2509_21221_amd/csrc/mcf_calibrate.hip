@@ -10,12 +10,14 @@
 // times:
 //
 //  * LDS: wave 0 and wave 1 of one workgroup, one word each way;
-//  * device scope: two workgroups of one cooperative launch (all of them
-//    resident), relaxed agent-scope atomics as the grid pass uses, once for
-//    blocks 0 and kGridNeighbour (a stage and the next one in the grid pass,
-//    whose workgroup index differs by the stage's 4 slices of 128 nodes:
-//    workgroups are dealt round robin to the 8 XCDs, so they sit on
-//    different XCDs) and once for blocks 0 and 8 (the same XCD).
+//  * device scope: two workgroups of one launch of 16 one-wave workgroups
+//    (far fewer than the device's CUs, so all are placed at once; should one
+//    not be, the other's bounded wait runs out), relaxed agent-scope atomics
+//    as the grid pass uses, once for workgroups 0 and `neighbour` (a stage
+//    and the next one in the grid pass, whose workgroup indices differ by
+//    the stage's slices of 128 nodes: 4 at n = 512; workgroups are dealt
+//    round robin to the 8 XCDs, so these sit on different XCDs) and once for
+//    workgroups 0 and 8 (the same XCD).
 //
 // Every wait is bounded; a wait that runs out marks the result invalid
 // instead of hanging.  Times come from the constant-rate wall clock.
@@ -112,11 +114,9 @@ hipError_t run_handoff_calibration(hipStream_t s, int clock_khz, int neighbour, 
         hipLaunchKernelGGL(clear_flags_kernel, dim3(1), dim3(128), 0, s, flags, 128);
         e = hipGetLastError();
         if (e != hipSuccess) break;
-        long long *slot = res + 2 * (q + 1);
-        int a = pairs[q][0], b = pairs[q][1];
-        void *args[] = {&flags, &slot, &a, &b};
-        e = hipLaunchCooperativeKernel(reinterpret_cast<const void *>(device_handoff_kernel), dim3(kDeviceBlocks),
-                                       dim3(64), args, 0, s);
+        hipLaunchKernelGGL(device_handoff_kernel, dim3(kDeviceBlocks), dim3(64), 0, s, flags, res + 2 * (q + 1),
+                           pairs[q][0], pairs[q][1]);
+        e = hipGetLastError();
     }
     if (e == hipSuccess) e = hipMemcpyAsync(host, res, sizeof host, hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
