@@ -182,7 +182,9 @@ def cpu_baseline_single(batch, budget_s: float):
     import numpy as np
 
     import oracle
+    import oracle.located
 
+    solve = oracle.located.solve if hasattr(batch, "location") else oracle.solve
     full = json.load(open(os.path.join(ROOT, "tests", "golden", "c5_oracle.json")))
     paths = int(full["augmentations"][0])
     # about 0.25-0.35 s per augmenting path on one core of the test hosts
@@ -190,7 +192,7 @@ def cpu_baseline_single(batch, budget_s: float):
     sub = batch.subset([0])
     sub.supply = np.full_like(sub.supply, units)
     t0 = time.perf_counter()
-    r = oracle.solve(sub, nthreads=1, flows=False, potentials=False)
+    r = solve(sub, nthreads=1, flows=False, potentials=False)
     t_used = time.perf_counter() - t0
     got = int(r["F"][0])
     est_s = t_used / max(1, got) * paths
