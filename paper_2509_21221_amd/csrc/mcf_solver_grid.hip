@@ -445,6 +445,38 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
             uint64_t final_key = ~0ull;
             bool converged = false;
             int ring_t = 0; // the iteration whose arrival this workgroup still owes
+            // Wave w owns columns 16w .. 16w+15 (lane & 15), lane group gq =
+            // lane >> 4.  During the search a column's node state lives in
+            // registers of its lanes (group 0 updates it; it goes back to LDS
+            // after the search), and the first 16 entries of its exit's flow
+            // list, fixed within a search, four per lane.
+            const int cq = wave * 16 + (lane & 15), gq = lane >> 4;
+            const bool own = cq < nown;
+            int r_di = 0, r_dq = 0, r_pi = 0, r_po = 0, r_fl = 0, r_cp = 0, r_nc = 0, r_pin = 0, r_pout = 0, r_snk = 0;
+            int r_lo = 0, r_len = 0, lp[4], lc[4];
+            if (own) {
+                r_di = din[cq];
+                r_dq = dout[cq];
+                r_pi = prin[cq];
+                r_po = prout[cq];
+                r_fl = flow[cq];
+                r_cp = cap[cq];
+                r_nc = ncost[cq];
+                r_pin = pin[cq];
+                r_pout = pout[cq];
+                r_snk = snkc[cq];
+                if (has_next) {
+                    r_lo = loff[cq];
+                    r_len = llen[cq];
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int e = r_lo + gq + 4 * u;
+                const bool in_list = gq + 4 * u < r_len;
+                lp[u] = in_list ? int(lpart[e]) : -1;
+                lc[u] = in_list ? lcost[e] : 0;
+            }
             for (int t = 1; t <= 4 * V + 8; ++t) {
                 if (located && has_prev && tid < L) mkey[tid] = ~0ull;
                 const uint32_t *ex_f = gp.ex + size_t(t & 1) * SN + size_t(has_prev ? k - 1 : 0) * n;
@@ -594,13 +626,11 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                 }
 
                 // Links into this block's entries, from the rows that dropped.
-                // Wave w owns columns 16w .. 16w+15 (lane & 15) and its four
-                // 16-lane groups (lane >> 4) take rows, or list entries,
+                // The four lane groups of a column take rows, or list entries,
                 // 16e + 4g .. 16e + 4g + 3; the swizzled block puts the four
                 // groups' costs in different banks, and their four partial
                 // minima meet by lane swaps, so no barrier separates the sweep
                 // from the node step below.
-                const int cq = wave * 16 + (lane & 15), gq = lane >> 4;
                 auto cost_at = [&](int i) { return cost16[i * kGridNB + (cq ^ (((i >> 2) & 3) << 4))]; };
                 uint64_t key = ~0ull;
                 if (located) {
@@ -681,15 +711,18 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                 // between searches): the column's four lanes take every fourth
                 // list entry; the smallest (label, entry) wins, i.e. the first
                 // entry of a tie.
-                const bool own = cq < nown;
                 uint64_t pk = ~0ull;
                 if (own && has_next && pull) {
-                    const int lo = loff[cq], hi = lo + llen[cq];
-                    for (int e = lo + gq; e < hi; e += kGridRowGroups) {
+#pragma unroll
+                    for (int u = 0; u < 4; ++u) {
+                        const int dj = lp[u] >= 0 ? enrow[lp[u]] : kInf;
+                        if (dj < kInf) pk = min(pk, pack_key(dj - lc[u], r_lo + gq + 4 * u));
+                    }
+                    for (int e = r_lo + 16 + gq; e < r_lo + r_len; e += kGridRowGroups) {
                         const int dj = enrow[lpart[e]];
                         if (dj < kInf) pk = min(pk, pack_key(dj - lcost[e], e));
                     }
-                    if (gq == 0) my_pulls += hi - lo;
+                    if (gq == 0) my_pulls += r_len;
                 }
                 if (has_next && pull) pk = row_group_min(pk);
 
@@ -697,10 +730,10 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                 bool sink_has = false;
                 int sink_label = 0;
                 if (own && gq == 0) {
-                    const int c = cq, q = k * n + j0 + c;
-                    int di = din[c], dq = dout[c], pi = prin[c], po = prout[c];
+                    const int q = k * n + j0 + cq;
+                    int di = r_di, dq = r_dq, pi = r_pi, po = r_po;
                     const int di0 = di, dq0 = dq;
-                    const int fl = flow[c], cp = cap[c], nc = ncost[c];
+                    const int fl = r_fl, cp = r_cp, nc = r_nc;
                     if (key != ~0ull && key_label(key) < di) {
                         di = key_label(key);
                         pi = int(uint32_t(key));
@@ -721,15 +754,15 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                         di = dq - nc;
                         pi = kPredSplit;
                     }
-                    din[c] = di;
-                    dout[c] = dq;
-                    prin[c] = pi;
-                    prout[c] = po;
+                    r_di = di;
+                    r_dq = dq;
+                    r_pi = pi;
+                    r_po = po;
                     st(&ex_out[q], (uint32_t(dq) << 2) | tag_f);
                     st(&en_out[q], (uint32_t(di) << 2) | tag_f);
                     const int bound = sbest == ~0ull ? kInf : key_label(sbest) - pit;
-                    if (((di != di0) & (di - pin[c] < bound)) | ((dq != dq0) & (dq - pout[c] < bound))) sh_changed = 1;
-                    if (k == S - 1) sink_has = dq < kInf, sink_label = dq + snkc[c];
+                    if (((di != di0) & (di - r_pin < bound)) | ((dq != dq0) & (dq - r_pout < bound))) sh_changed = 1;
+                    if (k == S - 1) sink_has = dq < kInf, sink_label = dq + r_snk;
                 }
                 // the sink's best key: per wave first (its owners are lanes
                 // 0-15, node index j0 + 16w + lane), then one LDS atomic per wave
@@ -742,6 +775,13 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                 // of the next iteration, behind its first reads.
                 ring_t = t;
             }
+            if (own && gq == 0) {
+                din[cq] = r_di;
+                dout[cq] = r_dq;
+                prin[cq] = r_pi;
+                prout[cq] = r_po;
+            }
+            __syncthreads();
             if (timed_out) break;
             if (!converged) {
                 if (tid == 0) sh_fault = 1;
