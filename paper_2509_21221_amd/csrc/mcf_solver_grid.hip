@@ -195,9 +195,12 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
     const bool has_prev = k >= 1, has_next = k + 1 < S;
 
     extern __shared__ __align__(16) unsigned char smem[];
-    __shared__ int sh_ok, sh_flag, sh_bad, sh_maxc, sh_changed, sh_len, sh_delta, sh_fault, sh_why[2];
+    __shared__ int sh_ok, sh_flag, sh_bad, sh_maxc, sh_changed, sh_len, sh_delta, sh_fault;
     __shared__ unsigned long long sh_key;
-    __shared__ int wcnt[kGridWaves], wmaxd[kGridWaves], wendrop[kGridWaves];
+    // one word per wave and label iteration: rows that dropped (bits 0-6),
+    // an entry label of stage k+1 dropped (bit 7), a dropped label too wide
+    // for packed keys (bit 8), the stop seen (bit 9), a wait ran out (bit 10)
+    __shared__ __align__(16) uint32_t wword[kGridWaves];
     __shared__ uint32_t sh_ties[kGridMaxNodes / 32];
     __shared__ int sh_esat;
 
@@ -270,7 +273,6 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
         sh_maxc = 0;
         sh_fault = 0;
         sh_changed = 0;
-        sh_why[0] = sh_why[1] = 0;
         sh_key = ~0ull;
     }
     __syncthreads();
@@ -426,7 +428,6 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                 st(sinkbest_w, ~0ull);
             }
         }
-        if (tid == 0) sh_why[0] = sh_why[1] = 0;
     };
 
     if (!timed_out && status == 0 && supply > 0) {
@@ -556,7 +557,6 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                     c0 = ld(&en_b[wi]);
                     if (take(a1, c1, s1, spins + 1)) break;
                 }
-                if (why) atomicOr(&sh_why[t & 1], why);
                 int dropped = 0, dnew = 0;
                 bool en_drop = false;
                 if (tid < n) {
@@ -573,33 +573,33 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                     }
                 }
                 const uint64_t m = __ballot(dropped);
-                const int en_any = __any(en_drop) ? 1 : 0;
-                const int wmax = int(wave_reduce_u32<true>(dropped ? uint32_t(dnew) : 0u));
-                if (lane == 0) {
-                    wcnt[wave] = __popcll(m);
-                    wmaxd[wave] = wmax;
-                    wendrop[wave] = en_any;
-                }
+                const bool en_any = __any(en_drop), wide_any = __any(dropped && uint32_t(dnew) >= kPackLimit);
+                const bool stop_any = __any(why == 1), late_any = __any(why == 2);
+                if (lane == 0)
+                    wword[wave] = uint32_t(__popcll(m)) | (uint32_t(en_any) << 7) | (uint32_t(wide_any) << 8) |
+                                  (uint32_t(stop_any) << 9) | (uint32_t(late_any) << 10);
                 __syncthreads();
-                const int whyb = sh_why[t & 1];
-                if (whyb) { // a stop seen by any thread wins over a wait that ran out
-                    if (whyb & 1) converged = true;
+                const uint4 wa = *reinterpret_cast<const uint4 *>(&wword[0]);
+                const uint4 wb = *reinterpret_cast<const uint4 *>(&wword[4]);
+                const uint32_t ww[kGridWaves] = {wa.x, wa.y, wa.z, wa.w, wb.x, wb.y, wb.z, wb.w};
+                const uint32_t wor = (wa.x | wa.y | wa.z | wa.w) | (wb.x | wb.y | wb.z | wb.w);
+                if (wor & (3u << 9)) { // a stop seen by any thread wins over a wait that ran out
+                    if (wor & (1u << 9)) converged = true;
                     else timed_out = true;
                     break;
                 }
-                if (tid == 0) sh_why[(t + 1) & 1] = 0;
-                int base = 0, nrows = 0, maxd = 0, pull = 0;
+                int base = 0, nrows = 0;
+#pragma unroll
                 for (int w = 0; w < kGridWaves; ++w) {
-                    const int cnt = wcnt[w];
+                    const int cnt = int(ww[w] & 127u);
                     base += w < wave ? cnt : 0;
                     nrows += cnt;
-                    maxd = max(maxd, wmaxd[w]);
-                    pull |= wendrop[w];
                 }
+                const int pull = (wor >> 7) & 1;
                 // Packed keys while labels allow; a stage where most rows
                 // dropped is swept densely by row index, otherwise through
                 // the compacted list (which then holds the packed keys).
-                const bool packed = uint32_t(maxd) < kPackLimit;
+                const bool packed = !(wor & (1u << 8));
                 // (a listed row costs about half again a dense one)
                 const bool dense = packed && 3 * nrows > 2 * n;
                 if (tid == 0)
