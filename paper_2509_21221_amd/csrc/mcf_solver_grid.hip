@@ -46,7 +46,8 @@ using namespace dev;
 constexpr int kGridThreads = 512;
 constexpr int kGridWaves = kGridThreads / 64;
 constexpr int kGridNB = 128;                           // nodes per workgroup
-constexpr int kGridRowGroups = kGridThreads / kGridNB; // rows split over 4 groups
+constexpr int kGridRowGroups = kGridThreads / kGridNB; // lanes per column for pulls and locations
+constexpr int kSweepGroups = 8;                        // lane groups of the link sweep (two columns a lane)
 constexpr uint16_t kNoArc16 = 0xffff;
 constexpr int kBias = 1 << 30;
 constexpr int kSpinLimit = 1 << 20;
@@ -128,6 +129,62 @@ __device__ __forceinline__ uint64_t row_group_min(uint64_t x)
     return x;
 }
 
+// A 16-bit half of w (low or high) times m, plus k: one v_mad_u32_u16,
+// whose operand select picks the half.
+__device__ __forceinline__ uint32_t mad_lo16(uint32_t w, uint32_t m, uint32_t k)
+{
+    uint32_t r;
+    asm("v_mad_u32_u16 %0, %1, %2, %3" : "=v"(r) : "v"(w), "s"(m), "v"(k));
+    return r;
+}
+__device__ __forceinline__ uint32_t mad_hi16(uint32_t w, uint32_t m, uint32_t k)
+{
+    uint32_t r;
+    asm("v_mad_u32_u16 %0, %1, %2, %3 op_sel:[1,0,0,0]" : "=v"(r) : "v"(w), "s"(m), "v"(k));
+    return r;
+}
+
+// Minimum over the eight lanes l ^ 8j (the link sweep's row groups): a
+// rotation by 8 within each 16-lane row, then the two lane swaps.
+__device__ __forceinline__ uint32_t sweep_group_min(uint32_t x)
+{
+    const int lane = threadIdx.x & 63;
+    x = min(x, dpp_mov<0x128, 0xf>(x)); // row_ror:8
+    const auto p16 = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+    x = min(x, (lane & 16) ? p16[0] : p16[1]);
+    const auto p32 = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+    return min(x, (lane & 32) ? p32[0] : p32[1]);
+}
+__device__ __forceinline__ uint64_t sweep_group_min64(uint64_t x)
+{
+    const int lane = threadIdx.x & 63;
+    {
+        const uint32_t lo = dpp_mov<0x128, 0xf>(uint32_t(x)), hi = dpp_mov<0x128, 0xf>(uint32_t(x >> 32));
+        x = min(x, (uint64_t(hi) << 32) | lo);
+    }
+    {
+        const auto pl = __builtin_amdgcn_permlane16_swap(uint32_t(x), uint32_t(x), false, false);
+        const auto ph = __builtin_amdgcn_permlane16_swap(uint32_t(x >> 32), uint32_t(x >> 32), false, false);
+        x = min(x, (uint64_t((lane & 16) ? ph[0] : ph[1]) << 32) | ((lane & 16) ? pl[0] : pl[1]));
+    }
+    {
+        const auto pl = __builtin_amdgcn_permlane32_swap(uint32_t(x), uint32_t(x), false, false);
+        const auto ph = __builtin_amdgcn_permlane32_swap(uint32_t(x >> 32), uint32_t(x >> 32), false, false);
+        x = min(x, (uint64_t((lane & 32) ? ph[0] : ph[1]) << 32) | ((lane & 32) ? pl[0] : pl[1]));
+    }
+    return x;
+}
+
+// The smallest (label, index) key over the lanes that have one, the lowest
+// index among equal labels; ~0 when no lane has one.
+__device__ __forceinline__ uint64_t wave_min_key_idx(bool has, int label, int idx)
+{
+    const uint32_t v = has ? uint32_t(label + kBias) : ~0u;
+    const uint32_t m = wave_reduce_u32<false>(v);
+    if (m == ~0u) return ~0ull;
+    return (uint64_t(m) << 32) | wave_reduce_u32<false>(v == m ? uint32_t(idx) : ~0u);
+}
+
 // Device-coherent accesses for data shared between workgroups.
 template <typename T> __device__ __forceinline__ T ld(const T *p)
 {
@@ -189,9 +246,9 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
     const int g = blockIdx.x, k = g / gp.slices, s = g % gp.slices;
     const int j0 = s * kGridNB, nown = min(kGridNB, n - j0);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    // rows of the previous stage rounded up to whole groups of 16 (the link
-    // sweep reads four rows at a time in each of four lane groups)
-    const int npad = (n + 15) & ~15;
+    // rows of the previous stage rounded up to whole groups of 32 (the link
+    // sweep reads four rows at a time in each of eight lane groups)
+    const int npad = (n + 31) & ~31;
     const bool has_prev = k >= 1, has_next = k + 1 < S;
 
     extern __shared__ __align__(16) unsigned char smem[];
@@ -335,10 +392,12 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
         }
     } else if (has_prev) {
         // Row i of the block holds the links from exit i of stage k-1 to the
-        // owned entries, column c at c ^ (((i >> 2) & 3) << 4): the four lane
-        // groups of the link sweep read rows of four different residues of
-        // i >> 2, hence four different 32-byte segments (no bank conflict).
-        // Rows n .. npad-1 are missing links.
+        // owned entries, column c at c ^ (((i >> 2) & 7) << 4): the eight lane
+        // groups of the link sweep read rows of eight different residues of
+        // i >> 2, hence eight different 32-byte segments of a 256-byte row
+        // (two accesses per bank, the least a 64-lane read can take), and a
+        // lane's two columns 2p, 2p + 1 stay adjacent.  Rows n .. npad-1 are
+        // missing links.
         const int32_t *layer = gac + size_t(k - 1) * n * n;
         for (int e = tid; e < npad * kGridNB; e += kGridThreads) {
             const int i = e / kGridNB, c = e % kGridNB;
@@ -346,7 +405,7 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
             bad |= a < -1;
             wide |= a > 65534;
             mx = max(mx, a);
-            cost16[i * kGridNB + (c ^ (((i >> 2) & 3) << 4))] = (a < 0 || a > 65534) ? kNoArc16 : uint16_t(a);
+            cost16[i * kGridNB + (c ^ (((i >> 2) & 7) << 4))] = (a < 0 || a > 65534) ? kNoArc16 : uint16_t(a);
         }
     }
     for (int i = n + tid; i < npad; i += kGridThreads) rowkey[i] = kNoRowKey;
@@ -446,12 +505,15 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
             uint64_t final_key = ~0ull;
             bool converged = false;
             int ring_t = 0; // the iteration whose arrival this workgroup still owes
-            // Wave w owns columns 16w .. 16w+15 (lane & 15), lane group gq =
-            // lane >> 4.  During the search a column's node state lives in
-            // registers of its lanes (group 0 updates it; it goes back to LDS
-            // after the search), and the first 16 entries of its exit's flow
-            // list, fixed within a search, four per lane.
-            const int cq = wave * 16 + (lane & 15), gq = lane >> 4;
+            // Wave w owns columns 16w .. 16w+15.  Lane l serves column
+            // 16w + 2 (l & 7) + ((l >> 3) & 1) (the link sweep gives lane l the
+            // column pair 16w + 2 (l & 7) + {0, 1}, and l picks one of the two),
+            // with lane group gq = l >> 4 for the reverse pulls and locations.
+            // During the search a column's node state lives in registers of its
+            // lanes (group 0 updates it; it goes back to LDS after the search),
+            // and the first 16 entries of its exit's flow list, fixed within a
+            // search, four per lane.
+            const int cq = wave * 16 + 2 * (lane & 7) + ((lane >> 3) & 1), gq = lane >> 4;
             const bool own = cq < nown;
             int r_di = 0, r_dq = 0, r_pi = 0, r_po = 0, r_fl = 0, r_cp = 0, r_nc = 0, r_pin = 0, r_pout = 0, r_snk = 0;
             int r_lo = 0, r_len = 0, lp[4], lc[4];
@@ -611,12 +673,12 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                 } else if (dropped && !dense) {
                     const int at = base + __popcll(m & ((1ull << lane) - 1ull));
                     rowlist[at] = packed ? int(rowkey[tid]) : tid;
-                    rowoff[at] = uint32_t((tid << 7) | (((tid >> 2) & 3) << 4)) << 1;
+                    rowoff[at] = uint32_t((tid << 7) | (((tid >> 2) & 7) << 4)) << 1;
                 }
                 // A dense sweep reads the row keys written before the last
-                // barrier; the list (padded to whole groups of 16) and the
+                // barrier; the list (padded to whole groups of 32) and the
                 // location keys need one more.
-                const int nlist = (nrows + 15) & ~15;
+                const int nlist = (nrows + 31) & ~31;
                 if (located || !dense) {
                     if (!located && tid >= nrows && tid < nlist) {
                         rowlist[tid] = int(kNoRowKey);
@@ -626,12 +688,15 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                 }
 
                 // Links into this block's entries, from the rows that dropped.
-                // The four lane groups of a column take rows, or list entries,
-                // 16e + 4g .. 16e + 4g + 3; the swizzled block puts the four
-                // groups' costs in different banks, and their four partial
-                // minima meet by lane swaps, so no barrier separates the sweep
-                // from the node step below.
-                auto cost_at = [&](int i) { return cost16[i * kGridNB + (cq ^ (((i >> 2) & 3) << 4))]; };
+                // Lane l takes the column pair 16w + 2p, 16w + 2p + 1 (p = l & 7)
+                // over rows, or list entries, 32e + 4g .. 32e + 4g + 3 of its
+                // group g = l >> 3: one 4-byte read gives both costs, and the
+                // eight groups' partial minima meet by lane moves, so no barrier
+                // separates the sweep from the node step below.
+                auto cost_at = [&](int i, int c) { return cost16[i * kGridNB + (c ^ (((i >> 2) & 7) << 4))]; };
+                const int sp = lane & 7, sg = lane >> 3, pc0 = wave * 16 + 2 * sp;
+                const bool odd = (lane >> 3) & 1;
+                const bool sweep = !located && nrows > 0 && wave * 16 < nown; // the same in the whole wave
                 uint64_t key = ~0ull;
                 if (located) {
                     // one candidate per location: its best row plus the latency
@@ -643,68 +708,97 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                             if (mk != ~0ull) key = min(key, (uint64_t)mk + (uint64_t(uint32_t(latl[a * L + cl])) << 32));
                         }
                     }
-                } else if (cq < nown && nrows > 0) {
-                    // exact 64-bit keys over this group's rows or entries, in
-                    // increasing order (the first row of a tie wins)
-                    auto exact = [&]() {
-                        const int span = dense ? n : nrows;
-                        int best = kInf, arg = -1;
-                        for (int e0 = 4 * gq; e0 < span; e0 += 16)
-                            for (int u = 0; u < 4; ++u) {
-                                const int e = e0 + u;
-                                if (e >= span) break;
-                                int i;
-                                if (dense) {
-                                    if (rowkey[e] == kNoRowKey) continue;
-                                    i = e;
-                                } else {
-                                    i = packed ? (rowlist[e] & 511) : rowlist[e];
-                                }
-                                const uint16_t c = cost_at(i);
-                                const int cand = exrow[i] + int(c);
-                                const bool take_it = (c != kNoArc16) & (cand < best);
-                                best = take_it ? cand : best;
-                                arg = take_it ? i : arg;
+                    key = row_group_min(key);
+                }
+                // exact 64-bit keys of the pair over this group's rows or
+                // entries, in increasing order (the first row of a tie wins),
+                // then over the eight groups
+                auto exact = [&](uint64_t &k0, uint64_t &k1) {
+                    const int span = dense ? n : nrows;
+                    int b0 = kInf, a0 = -1, b1 = kInf, a1 = -1;
+                    for (int e0 = 4 * sg; e0 < span; e0 += 4 * kSweepGroups)
+                        for (int u = 0; u < 4; ++u) {
+                            const int e = e0 + u;
+                            if (e >= span) break;
+                            int i;
+                            if (dense) {
+                                if (rowkey[e] == kNoRowKey) continue;
+                                i = e;
+                            } else {
+                                i = packed ? (rowlist[e] & 511) : rowlist[e];
                             }
-                        return best < kInf ? pack_key(best, arg) : ~0ull;
-                    };
-                    if (packed) {
-                        uint32_t best = ~0u;
-                        if (dense) {
-                            // rows 16e + 4g + u all share the swizzle g
-                            const uint16_t *cc = cost16 + (cq ^ (gq << 4));
-#pragma unroll 2
-                            for (int e = 4 * gq; e < npad; e += 16) {
-                                const uint4 kq = *reinterpret_cast<const uint4 *>(&rowkey[e]);
-                                const uint32_t c0 = cc[(e + 0) * kGridNB], c1 = cc[(e + 1) * kGridNB];
-                                const uint32_t c2 = cc[(e + 2) * kGridNB], c3 = cc[(e + 3) * kGridNB];
-                                best = min(best, min((c0 << 9) + kq.x, (c1 << 9) + kq.y));
-                                best = min(best, min((c2 << 9) + kq.z, (c3 << 9) + kq.w));
-                            }
-                        } else {
-                            const uint32_t *kl = reinterpret_cast<const uint32_t *>(rowlist);
-                            const unsigned char *cb = reinterpret_cast<const unsigned char *>(cost16);
-                            const uint32_t cq2 = uint32_t(cq) << 1;
-                            auto at = [&](uint32_t off) { return uint32_t(*reinterpret_cast<const uint16_t *>(cb + (off ^ cq2))); };
-#pragma unroll 2
-                            for (int e = 4 * gq; e < nlist; e += 16) {
-                                const uint4 kq = *reinterpret_cast<const uint4 *>(&kl[e]);
-                                const uint4 oq = *reinterpret_cast<const uint4 *>(&rowoff[e]);
-                                const uint32_t c0 = at(oq.x), c1 = at(oq.y), c2 = at(oq.z), c3 = at(oq.w);
-                                best = min(best, min((c0 << 9) + kq.x, (c1 << 9) + kq.y));
-                                best = min(best, min((c2 << 9) + kq.z, (c3 << 9) + kq.w));
-                            }
+                            const int d = exrow[i];
+                            const uint16_t x0 = cost_at(i, pc0), x1 = cost_at(i, pc0 + 1);
+                            const bool t0 = (x0 != kNoArc16) & (d + int(x0) < b0);
+                            const bool t1 = (x1 != kNoArc16) & (d + int(x1) < b1);
+                            b0 = t0 ? d + int(x0) : b0;
+                            a0 = t0 ? i : a0;
+                            b1 = t1 ? d + int(x1) : b1;
+                            a1 = t1 ? i : a1;
                         }
-                        if (best < kNoRowKey) {
-                            const int row = int(best & 511u);
-                            // a missing link reads as cost 65535; if one won, redo exactly
-                            key = cost_at(row) != kNoArc16 ? pack_key(int(best >> 9), row) : exact();
+                    k0 = sweep_group_min64(b0 < kInf ? pack_key(b0, a0) : ~0ull);
+                    k1 = sweep_group_min64(b1 < kInf ? pack_key(b1, a1) : ~0ull);
+                };
+                if (sweep && packed) {
+                    // packed keys (label + cost) << 9 | row; a 16-bit cost times
+                    // 512 plus the key is one multiply-add
+                    uint32_t best0 = ~0u, best1 = ~0u;
+                    const uint32_t k512 = 512u;
+                    const unsigned char *cb = reinterpret_cast<const unsigned char *>(cost16);
+                    if (dense) {
+                        // rows 32e + 4g + u all share the swizzle g
+                        const unsigned char *cc = cb + ((pc0 ^ (sg << 4)) << 1);
+                        const int trips = npad / (4 * kSweepGroups); // the same in every lane
+#pragma clang loop unroll_count(2)
+                        for (int m = 0; m < trips; ++m) {
+                            const int e = 4 * kSweepGroups * m + 4 * sg;
+                            const uint4 kq = *reinterpret_cast<const uint4 *>(&rowkey[e]);
+                            const uint32_t w0 = *reinterpret_cast<const uint32_t *>(cc + (e + 0) * (2 * kGridNB));
+                            const uint32_t w1 = *reinterpret_cast<const uint32_t *>(cc + (e + 1) * (2 * kGridNB));
+                            const uint32_t w2 = *reinterpret_cast<const uint32_t *>(cc + (e + 2) * (2 * kGridNB));
+                            const uint32_t w3 = *reinterpret_cast<const uint32_t *>(cc + (e + 3) * (2 * kGridNB));
+                            best0 = min(min(best0, mad_lo16(w0, k512, kq.x)), mad_lo16(w1, k512, kq.y));
+                            best0 = min(min(best0, mad_lo16(w2, k512, kq.z)), mad_lo16(w3, k512, kq.w));
+                            best1 = min(min(best1, mad_hi16(w0, k512, kq.x)), mad_hi16(w1, k512, kq.y));
+                            best1 = min(min(best1, mad_hi16(w2, k512, kq.z)), mad_hi16(w3, k512, kq.w));
                         }
                     } else {
-                        key = exact();
+                        const uint32_t *kl = reinterpret_cast<const uint32_t *>(rowlist);
+                        const uint32_t c02 = uint32_t(pc0) << 1;
+                        auto at = [&](uint32_t off) { return *reinterpret_cast<const uint32_t *>(cb + (off ^ c02)); };
+                        const int trips = nlist / (4 * kSweepGroups); // the same in every lane
+#pragma clang loop unroll_count(2)
+                        for (int m = 0; m < trips; ++m) {
+                            const int e = 4 * kSweepGroups * m + 4 * sg;
+                            const uint4 kq = *reinterpret_cast<const uint4 *>(&kl[e]);
+                            const uint4 oq = *reinterpret_cast<const uint4 *>(&rowoff[e]);
+                            const uint32_t w0 = at(oq.x), w1 = at(oq.y), w2 = at(oq.z), w3 = at(oq.w);
+                            best0 = min(min(best0, mad_lo16(w0, k512, kq.x)), mad_lo16(w1, k512, kq.y));
+                            best0 = min(min(best0, mad_lo16(w2, k512, kq.z)), mad_lo16(w3, k512, kq.w));
+                            best1 = min(min(best1, mad_hi16(w0, k512, kq.x)), mad_hi16(w1, k512, kq.y));
+                            best1 = min(min(best1, mad_hi16(w2, k512, kq.z)), mad_hi16(w3, k512, kq.w));
+                        }
                     }
+                    best0 = sweep_group_min(best0);
+                    best1 = sweep_group_min(best1);
+                    const uint32_t best = odd ? best1 : best0;
+                    // a missing link reads as cost 65535; if one won, redo exactly
+                    bool redo = false;
+                    if (cq < nown && best < kNoRowKey) {
+                        const int row = int(best & 511u);
+                        if (cost_at(row, cq) != kNoArc16) key = pack_key(int(best >> 9), row);
+                        else redo = true;
+                    }
+                    if (__any(redo)) {
+                        uint64_t k0, k1;
+                        exact(k0, k1);
+                        if (redo) key = odd ? k1 : k0;
+                    }
+                } else if (sweep) {
+                    uint64_t k0, k1;
+                    exact(k0, k1);
+                    if (cq < nown) key = odd ? k1 : k0;
                 }
-                key = row_group_min(key);
 
                 // Reverse links of the owned exits, only when an entry label of
                 // stage k+1 dropped since the last pull (the lists change only
@@ -765,9 +859,9 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                     if (k == S - 1) sink_has = dq < kInf, sink_label = dq + r_snk;
                 }
                 // the sink's best key: per wave first (its owners are lanes
-                // 0-15, node index j0 + 16w + lane), then one LDS atomic per wave
+                // 0-15, node index j0 + cq), then one LDS atomic per wave
                 if (k == S - 1) {
-                    const uint64_t skey = wave_min_key(sink_has, sink_label, j0 + wave * 16);
+                    const uint64_t skey = wave_min_key_idx(sink_has, sink_label, j0 + cq);
                     if (lane == 0 && skey != ~0ull) atomicMin(&sh_key, (unsigned long long)skey);
                 }
                 __syncthreads();
@@ -1169,7 +1263,7 @@ __global__ void grid_ctrl_reset_kernel(int32_t *ctrl)
 size_t lds_fixed(int S, int n)
 {
     size_t o = align16(grid_pass_big_bytes(S, n));
-    for (int a = 0; a < 4; ++a) o = align16(o + 4 * size_t((n + 15) & ~15));
+    for (int a = 0; a < 4; ++a) o = align16(o + 4 * size_t((n + 31) & ~31));
     for (int a = 0; a < 13; ++a) o = align16(o + 4 * size_t(kGridNB));
     o = align16(o + 8 * size_t(kGridRowGroups) * kGridNB);
     return o;
@@ -1179,7 +1273,7 @@ size_t lds_fixed(int S, int n)
 
 size_t grid_pass_big_bytes(int S, int n)
 {
-    return std::max(size_t((n + 15) & ~15) * kGridNB * 2, size_t(4) * S * n);
+    return std::max(size_t((n + 31) & ~31) * kGridNB * 2, size_t(4) * S * n);
 }
 
 size_t grid_pass_lds_bytes(int S, int n, int64_t list_slots)

@@ -150,6 +150,21 @@ def test_grid_pass_tied_exits(S, n, cost_hi):
     assert (g["passes"] == mcf.GWTF_PASS_GRID).all()
 
 
+def test_grid_pass_wide_labels():
+    """Every cost between 55,000 and 65,000 on a 48-stage chain: shortest
+    path labels pass 2^22 - 2^16, where the grid pass's packed 32-bit keys
+    (label << 9 | row) stop, so its link sweep takes the exact 64-bit keys."""
+    batch = W.random_small(2, 48, 80, seed=41, cap_hi=3, cost_hi=10000, supply_hi=40)
+    for a in (batch.node_cost, batch.arc_cost, batch.src_cost, batch.snk_cost):
+        a[a >= 0] += 55000
+    say("grid pass wide labels")
+    g = gpu_solve(batch)
+    ref = oracle.solve(batch)
+    compare(batch, g, ref)
+    assert (g["passes"] == mcf.GWTF_PASS_GRID).all()
+    assert (ref["F"] > 0).all() and (ref["cost"] // ref["F"] > (1 << 22)).all()
+
+
 def test_grid_pass_routing_and_status():
     """At n = 512 a workgroup's LDS holds about 1400 flow-list slots: an
     instance with capacities of 64 reserves 128 * 64 and moves to the global
