@@ -662,8 +662,10 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                 // dropped is swept densely by row index, otherwise through
                 // the compacted list (which then holds the packed keys).
                 const bool packed = !(wor & (1u << 8));
-                // (a listed row costs about half again a dense one)
-                const bool dense = packed && 3 * nrows > 2 * n;
+                // (a listed row costs about twice a dense one: its key and
+                // offset are read as well; on the 64 x 512 instance the dense
+                // sweep pays from half the rows on)
+                const bool dense = packed && 2 * nrows > n;
                 if (tid == 0)
                     my_relax += located ? (nrows > 0 ? (long long)nrows + (long long)nown * L : 0)
                                         : (long long)nrows * nown;
@@ -749,8 +751,7 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                         // rows 32e + 4g + u all share the swizzle g
                         const unsigned char *cc = cb + ((pc0 ^ (sg << 4)) << 1);
                         const int trips = npad / (4 * kSweepGroups); // the same in every lane
-#pragma clang loop unroll_count(2)
-                        for (int m = 0; m < trips; ++m) {
+                        auto step = [&](int m) {
                             const int e = 4 * kSweepGroups * m + 4 * sg;
                             const uint4 kq = *reinterpret_cast<const uint4 *>(&rowkey[e]);
                             const uint32_t w0 = *reinterpret_cast<const uint32_t *>(cc + (e + 0) * (2 * kGridNB));
@@ -761,14 +762,19 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                             best0 = min(min(best0, mad_lo16(w2, k512, kq.z)), mad_lo16(w3, k512, kq.w));
                             best1 = min(min(best1, mad_hi16(w0, k512, kq.x)), mad_hi16(w1, k512, kq.y));
                             best1 = min(min(best1, mad_hi16(w2, k512, kq.z)), mad_hi16(w3, k512, kq.w));
+                        };
+                        int m = 0;
+                        for (; m + 2 <= trips; m += 2) {
+                            step(m);
+                            step(m + 1);
                         }
+                        if (m < trips) step(m);
                     } else {
                         const uint32_t *kl = reinterpret_cast<const uint32_t *>(rowlist);
                         const uint32_t c02 = uint32_t(pc0) << 1;
                         auto at = [&](uint32_t off) { return *reinterpret_cast<const uint32_t *>(cb + (off ^ c02)); };
                         const int trips = nlist / (4 * kSweepGroups); // the same in every lane
-#pragma clang loop unroll_count(2)
-                        for (int m = 0; m < trips; ++m) {
+                        auto step = [&](int m) {
                             const int e = 4 * kSweepGroups * m + 4 * sg;
                             const uint4 kq = *reinterpret_cast<const uint4 *>(&kl[e]);
                             const uint4 oq = *reinterpret_cast<const uint4 *>(&rowoff[e]);
@@ -777,7 +783,13 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                             best0 = min(min(best0, mad_lo16(w2, k512, kq.z)), mad_lo16(w3, k512, kq.w));
                             best1 = min(min(best1, mad_hi16(w0, k512, kq.x)), mad_hi16(w1, k512, kq.y));
                             best1 = min(min(best1, mad_hi16(w2, k512, kq.z)), mad_hi16(w3, k512, kq.w));
+                        };
+                        int m = 0;
+                        for (; m + 2 <= trips; m += 2) {
+                            step(m);
+                            step(m + 1);
                         }
+                        if (m < trips) step(m);
                     }
                     best0 = sweep_group_min(best0);
                     best1 = sweep_group_min(best1);
