@@ -573,35 +573,28 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                     else if ((need_ex | need_en) && spins > kSpinLimit) why = 2;
                     return why != 0 || !(need_ex | need_en);
                 };
-                int s0 = ld(&ctrl[kCtlStop]);
-                uint32_t a0 = ld(&ex_f[wi]), c0 = ld(&en_b[wi]);
+                // Count this workgroup into iteration ring_t.  The atomic goes
+                // out before this iteration's first reads and its result is
+                // looked at only once the wait below is over, so its round
+                // trip overlaps the wait.  The last one in learns whether any
+                // label changed; if none did, the labels are a fixed point and
+                // it publishes the sink's key and stop.
+                int ring_slot = -1;
+                unsigned ring_mine = 0, ring_old = 0;
                 if (tid == 0 && ring_t) {
-                    // Count this workgroup into iteration ring_t (its atomic's
-                    // round trip overlaps the reads just issued).  The last one
-                    // in learns whether any label changed; if none did, the
-                    // labels are a fixed point and it publishes the sink's key
-                    // and stop.
-                    const int slot = ring_t % gp.ring_slots;
+                    ring_slot = ring_t % gp.ring_slots;
                     if (sh_key != ~0ull) {
-                        atomicMin(&gp.ring_key[slot], sh_key);
+                        atomicMin(&gp.ring_key[ring_slot], sh_key);
                         atomicMin(sinkbest_w, sh_key);
                         drain();
                     }
-                    const unsigned mine = sh_changed ? 0x10001u : 1u;
-                    const unsigned total = atomicAdd(&gp.ring[slot], mine) + mine;
-                    if ((total & 0xffffu) == gridDim.x) {
-                        if ((total >> 16) == 0) {
-                            st(final_key_w, ld(&gp.ring_key[slot]));
-                            drain();
-                            st(&ctrl[kCtlStop], ring_t);
-                        } else {
-                            st(&gp.ring[slot], 0u);
-                            st(&gp.ring_key[slot], ~0ull);
-                        }
-                    }
+                    ring_mine = sh_changed ? 0x10001u : 1u;
+                    ring_old = atomicAdd(&gp.ring[ring_slot], ring_mine);
                     sh_key = ~0ull;
                     sh_changed = 0;
                 }
+                int s0 = ld(&ctrl[kCtlStop]);
+                uint32_t a0 = ld(&ex_f[wi]), c0 = ld(&en_b[wi]);
                 // The sink's label so far bounds which changes matter: a vertex
                 // whose reduced label reaches the sink's cannot lie on a
                 // shortest path to it, and its label is only an upper bound,
@@ -618,6 +611,19 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                     a0 = ld(&ex_f[wi]);
                     c0 = ld(&en_b[wi]);
                     if (take(a1, c1, s1, spins + 1)) break;
+                }
+                if (ring_slot >= 0) {
+                    const unsigned total = ring_old + ring_mine;
+                    if ((total & 0xffffu) == gridDim.x) {
+                        if ((total >> 16) == 0) {
+                            st(final_key_w, ld(&gp.ring_key[ring_slot]));
+                            drain();
+                            st(&ctrl[kCtlStop], ring_t);
+                        } else {
+                            st(&gp.ring[ring_slot], 0u);
+                            st(&gp.ring_key[ring_slot], ~0ull);
+                        }
+                    }
                 }
                 int dropped = 0, dnew = 0;
                 bool en_drop = false;
