@@ -185,6 +185,16 @@ __device__ __forceinline__ uint64_t wave_min_key_idx(bool has, int label, int id
     return (uint64_t(m) << 32) | wave_reduce_u32<false>(v == m ? uint32_t(idx) : ~0u);
 }
 
+// Workgroup barrier for data in LDS only: each wave waits for its own LDS
+// accesses, not for its global ones, so polling reads still in flight (and
+// label stores not yet acknowledged) do not hold the workgroup up.
+__device__ __forceinline__ void lds_barrier()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // Device-coherent accesses for data shared between workgroups.
 template <typename T> __device__ __forceinline__ T ld(const T *p)
 {
@@ -646,7 +656,7 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                 if (lane == 0)
                     wword[wave] = uint32_t(__popcll(m)) | (uint32_t(en_any) << 7) | (uint32_t(wide_any) << 8) |
                                   (uint32_t(stop_any) << 9) | (uint32_t(late_any) << 10);
-                __syncthreads();
+                lds_barrier();
                 const uint4 wa = *reinterpret_cast<const uint4 *>(&wword[0]);
                 const uint4 wb = *reinterpret_cast<const uint4 *>(&wword[4]);
                 const uint32_t ww[kGridWaves] = {wa.x, wa.y, wa.z, wa.w, wb.x, wb.y, wb.z, wb.w};
@@ -692,7 +702,7 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                         rowlist[tid] = int(kNoRowKey);
                         rowoff[tid] = 0;
                     }
-                    __syncthreads();
+                    lds_barrier();
                 }
 
                 // Links into this block's entries, from the rows that dropped.
@@ -882,9 +892,9 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                     const uint64_t skey = wave_min_key_idx(sink_has, sink_label, j0 + cq);
                     if (lane == 0 && skey != ~0ull) atomicMin(&sh_key, (unsigned long long)skey);
                 }
-                __syncthreads();
+                lds_barrier();
                 // This workgroup's arrival for iteration t goes out at the start
-                // of the next iteration, behind its first reads.
+                // of the next iteration, ahead of its first reads.
                 ring_t = t;
             }
             if (own && gq == 0) {
