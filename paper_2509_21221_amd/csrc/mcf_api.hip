@@ -82,7 +82,8 @@ void plan_workspace(Workspace &w, int S, int n, const DeviceInfo &d)
         if (slots >= 64) {
             const size_t lds = grid_pass_lds_bytes(S, n, slots);
             const int per_cu = grid_pass_blocks_per_cu(lds);
-            if (per_cu >= 1 && int64_t(S) * grid_pass_slices(n) <= int64_t(per_cu) * d.cus) {
+            const int64_t blocks = int64_t(S) * grid_pass_slices(n);
+            if (per_cu >= 1 && blocks <= int64_t(per_cu) * d.cus && blocks <= kGridMaxBlocks) {
                 w.grid = true;
                 w.grid_slots = slots;
                 w.grid_lds = lds;
@@ -109,8 +110,8 @@ void for_each_buffer(Workspace &w, int S, int n, int B, Fn f)
     f((void **)&w.g_pred, sizeof(int32_t) * gsn);
     f((void **)&w.g_path, w.grid ? sizeof(int32_t) * (2 * gsn + 8) : 0);
     f((void **)&w.g_ctrl, w.grid ? sizeof(int32_t) * kGridCtrlInts : 0);
-    f((void **)&w.g_ring, w.grid ? sizeof(uint32_t) * grid_ring_slots(S) : 0);
-    f((void **)&w.g_ring_key, w.grid ? sizeof(unsigned long long) * grid_ring_slots(S) : 0);
+    f((void **)&w.g_ring, w.grid ? sizeof(uint32_t) * kRingStride * grid_ring_slots(S) : 0);
+    f((void **)&w.g_ring_key, w.grid ? sizeof(unsigned long long) * kRingKeyStride * grid_ring_slots(S) : 0);
 }
 
 } // namespace

@@ -7,7 +7,11 @@
 
 namespace gwtf {
 
-constexpr int kGridCtrlInts = 48;      // control block: flags, barrier, per-iteration words, tied exits
+constexpr int kGridCtrlInts = 1280;    // control block: flags, barrier, per-iteration words, tied exits
+constexpr int kGridMaxBlocks = 512;    // workgroups of one grid launch (the barrier's group counters)
+// Ring slots and their sink keys sit 128 bytes apart: every workgroup adds
+// its arrival to a slot each iteration, and atomics on one line serialize.
+constexpr int kRingStride = 32, kRingKeyStride = 16;
 constexpr int kGridMaxNodes = 512;     // a stage's labels are staged with one thread per node
 constexpr size_t kGridStaticLds = 512; // static LDS of the grid kernel (upper bound)
 struct GridParams {
@@ -17,8 +21,8 @@ struct GridParams {
     int64_t list_slots; // flow-list capacity of one workgroup
     size_t big_bytes;   // leading LDS area: link-cost block or staged predecessors
     uint32_t *ex, *en;  // [2][S*n] exit / entry labels << 2 | iteration tag, by iteration parity
-    uint32_t *ring;     // [ring_slots] per-iteration arrivals (low 16 bits) and changed count
-    unsigned long long *ring_key; // [ring_slots] per-iteration minimum sink key
+    uint32_t *ring;     // [ring_slots * kRingStride] per-iteration arrivals (low 16 bits) and changed count
+    unsigned long long *ring_key; // [ring_slots * kRingKeyStride] per-iteration minimum sink key
     int32_t ring_slots; // > S + 2: iterations in flight at once across the stages
     int32_t *pred;      // [S*n] entry predecessor (low 16 bits) and exit predecessor (high)
     int32_t *path;      // [2*S*n + 8] arc codes of the augmenting path

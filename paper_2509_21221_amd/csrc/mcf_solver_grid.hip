@@ -72,20 +72,29 @@ enum : int { kFlagBad = 1, kFlagWide = 2, kFlagLists = 4, kFlagFault = 8 };
 enum : int {
     kCtlFlags = 0,
     kCtlMaxCost = 1,
-    kCtlBarCount = 2, // arrivals in the low 16 bits, raised flags above
-    kCtlBarWord = 3,  // epoch << 1 | OR of the last barrier's flags
-    kCtlSinkBest = 4, // uint64: the smallest sink key of the current search so far
     kCtlDelta = 16,
     kCtlLen = 17,
-    kCtlStop = 18,     // iteration at which the search converged, 0 while it runs
     kCtlMore = 19,     // tied exits are left to try after this path
     kCtlRelax = 20,    // uint64
     kCtlPulls = 22,    // uint64
     kCtlFinalKey = 24, // uint64: sink label and exit of the converged search
     kCtlTies = 32,     // [kGridMaxNodes / 32] exits of the last stage that reach the sink at its label
+    // Words that many workgroups poll or update get a 128-byte line each.
+    kCtlStop = 64,       // iteration at which the search converged, 0 while it runs
+    kCtlSinkBest = 96,   // uint64: the smallest sink key of the current search so far
+    kCtlBarCount = 128,  // barrier: groups arrived, over all barriers so far
+    kCtlBarWord = 160,   // barrier: epoch << 1 | OR of the last barrier's flags
+    kCtlBarFlags = 192,  // barrier: OR of the flags raised at the current barrier
+    kCtlBarGroups = 224, // barrier: per group of kBarGroup workgroups, arrivals so far
 };
-static_assert(kCtlTies + kGridMaxNodes / 32 <= kGridCtrlInts, "control block too small");
-static_assert(kCtlFinalKey + 2 <= kGridCtrlInts, "control block too small");
+// Grid barrier arrivals are counted per group of 16 workgroups, then per
+// group: atomics on one word are performed one after another, so 256
+// arrivals on one counter take several microseconds.
+constexpr int kBarGroup = 16, kBarLine = 32;
+static_assert(kCtlTies + kGridMaxNodes / 32 <= kCtlStop, "control words overlap");
+static_assert(kCtlFinalKey + 2 <= kCtlTies, "control words overlap");
+static_assert(kCtlBarGroups + kBarLine * ((kGridMaxBlocks + kBarGroup - 1) / kBarGroup) <= kGridCtrlInts,
+              "control block too small");
 
 __device__ __forceinline__ uint64_t pack_key(int label, int idx)
 {
@@ -209,9 +218,13 @@ __device__ __forceinline__ void drain() { asm volatile("s_waitcnt vmcnt(0)" ::: 
 
 // Grid barrier.  sync() returns false if the barrier did not complete within
 // the spin bound; *flag_lds receives the OR of the flags the workgroups
-// passed.  Both are the same in every thread of a workgroup.
+// passed.  Both are the same in every thread of a workgroup.  Arrivals go to
+// the workgroup's group counter; the group's last arrival counts the group
+// in; the last group's releases the barrier by advancing the epoch word.  The
+// counters only grow (barrier e is complete at (e + 1) times the number of
+// members), so no reset can race with the next barrier's arrivals.
 struct GridBarrier {
-    unsigned *count, *word;
+    unsigned *count, *word, *flags, *groups;
     unsigned nblocks, epoch;
 
     __device__ bool sync(bool raise, int *ok_lds, int *flag_lds)
@@ -219,14 +232,21 @@ struct GridBarrier {
         drain();
         __syncthreads();
         if (threadIdx.x == 0) {
-            const unsigned mine = raise ? 0x10001u : 1u;
-            const unsigned total = atomicAdd(count, mine) + mine;
-            bool good = true;
-            unsigned w;
-            if ((total & 0xffffu) == nblocks) {
-                st(count, 0u);
+            if (raise) {
+                atomicOr(flags, 1u);
                 drain();
-                w = ((epoch + 1u) << 1) | unsigned((total >> 16) != 0);
+            }
+            const unsigned grp = blockIdx.x / kBarGroup, ngroups = (nblocks + kBarGroup - 1) / kBarGroup;
+            const unsigned gsize = min(unsigned(kBarGroup), nblocks - grp * kBarGroup);
+            bool good = true, last = false;
+            unsigned w = 0;
+            if (atomicAdd(groups + grp * kBarLine, 1u) + 1u == gsize * (epoch + 1u))
+                last = atomicAdd(count, 1u) + 1u == ngroups * (epoch + 1u);
+            if (last) {
+                const unsigned f = ld(flags);
+                if (f) st(flags, 0u);
+                drain();
+                w = ((epoch + 1u) << 1) | unsigned(f != 0);
                 st(word, w);
             } else {
                 int spins = 0;
@@ -323,6 +343,7 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
     unsigned long long *final_key_w = reinterpret_cast<unsigned long long *>(ctrl + kCtlFinalKey);
     unsigned long long *sinkbest_w = reinterpret_cast<unsigned long long *>(ctrl + kCtlSinkBest);
     GridBarrier bar{reinterpret_cast<unsigned *>(ctrl + kCtlBarCount), reinterpret_cast<unsigned *>(ctrl + kCtlBarWord),
+                    reinterpret_cast<unsigned *>(ctrl + kCtlBarFlags), reinterpret_cast<unsigned *>(ctrl + kCtlBarGroups),
                     gridDim.x, 0u};
     if (tid == 0) bar.epoch = ld(bar.word) >> 1;
 
@@ -488,8 +509,8 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
         }
         if (g == 0) {
             for (int r = tid; r < gp.ring_slots; r += kGridThreads) {
-                st(&gp.ring[r], 0u);
-                st(&gp.ring_key[r], ~0ull);
+                st(&gp.ring[r * kRingStride], 0u);
+                st(&gp.ring_key[r * kRingKeyStride], ~0ull);
             }
             if (tid == 0) {
                 st(&ctrl[kCtlStop], 0);
@@ -594,12 +615,12 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                 if (tid == 0 && ring_t) {
                     ring_slot = ring_t % gp.ring_slots;
                     if (sh_key != ~0ull) {
-                        atomicMin(&gp.ring_key[ring_slot], sh_key);
+                        atomicMin(&gp.ring_key[ring_slot * kRingKeyStride], sh_key);
                         atomicMin(sinkbest_w, sh_key);
                         drain();
                     }
                     ring_mine = sh_changed ? 0x10001u : 1u;
-                    ring_old = atomicAdd(&gp.ring[ring_slot], ring_mine);
+                    ring_old = atomicAdd(&gp.ring[ring_slot * kRingStride], ring_mine);
                     sh_key = ~0ull;
                     sh_changed = 0;
                 }
@@ -626,12 +647,12 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                     const unsigned total = ring_old + ring_mine;
                     if ((total & 0xffffu) == gridDim.x) {
                         if ((total >> 16) == 0) {
-                            st(final_key_w, ld(&gp.ring_key[ring_slot]));
+                            st(final_key_w, ld(&gp.ring_key[ring_slot * kRingKeyStride]));
                             drain();
                             st(&ctrl[kCtlStop], ring_t);
                         } else {
-                            st(&gp.ring[ring_slot], 0u);
-                            st(&gp.ring_key[ring_slot], ~0ull);
+                            st(&gp.ring[ring_slot * kRingStride], 0u);
+                            st(&gp.ring_key[ring_slot * kRingKeyStride], ~0ull);
                         }
                     }
                 }
@@ -1285,7 +1306,7 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
 
 __global__ void grid_ctrl_reset_kernel(int32_t *ctrl)
 {
-    if (threadIdx.x < kGridCtrlInts) ctrl[threadIdx.x] = 0;
+    for (int i = threadIdx.x; i < kGridCtrlInts; i += blockDim.x) ctrl[i] = 0;
 }
 
 size_t lds_fixed(int S, int n)
@@ -1344,7 +1365,7 @@ int grid_pass_blocks_per_cu(size_t lds_bytes)
 
 hipError_t launch_grid_pass(const GridParams &gp, size_t lds_bytes, hipStream_t s)
 {
-    hipLaunchKernelGGL(grid_ctrl_reset_kernel, dim3(1), dim3(kGridCtrlInts), 0, s, gp.ctrl);
+    hipLaunchKernelGGL(grid_ctrl_reset_kernel, dim3(1), dim3(256), 0, s, gp.ctrl);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     GridParams arg = gp;
