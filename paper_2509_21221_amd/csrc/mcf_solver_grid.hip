@@ -1040,6 +1040,20 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                         // low half, exit predecessor in the high half).  A compute
                         // arc followed by the opposite one would be a cycle.
                         while (state == 0) {
+                            // Most nodes are reached at their exit by the compute
+                            // arc and at their entry by a forward link: two arcs
+                            // and one stage down per word, taken here with the
+                            // fewest tests; anything else goes to the full step.
+                            if (at_exit)
+                                for (;;) {
+                                    const uint32_t fw = __builtin_amdgcn_readfirstlane(uint32_t(all_pred[kk * n + i]));
+                                    const int fen = int(fw & 0x7fffu) - 3, fex = int((fw >> 16) & 0x7fffu) - 3;
+                                    if ((fw & 0x80008000u) | (fex != kPredSplit) | (unsigned(fen) >= unsigned(n)) | (kk < 1)) break;
+                                    record(path_code(kArcSplitFwd, kk, i, 0));
+                                    record(path_code(kArcLinkFwd, kk - 1, fen, i));
+                                    kk -= 1;
+                                    i = fen;
+                                }
                             if (len > 2 * SN + 4) {
                                 state = 2;
                                 break;
