@@ -1021,19 +1021,14 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                         bool at_exit = true;
                         state = from < n ? 0 : 2;
                         len = 0;
-                        // Step s's arc code goes to lane s & 63 of `rec`; every 64
-                        // steps the wave stores them with one write.
-                        uint32_t rec = 0;
-                        auto flush = [&](int upto) {
-                            const int at = (upto - 1) / 64 * 64 + lane;
-                            if (at < upto) {
-                                if (at < kPathLds) lpath[at] = int(rec);
-                                else st(&gp.path[at], int(rec));
-                            }
-                        };
+                        // Lane 0 stores step s's arc code (the first kPathLds in
+                        // LDS, the rest in memory).
                         auto record = [&](int code) {
-                            rec = lane == (len & 63) ? uint32_t(code) : rec;
-                            if ((++len & 63) == 0) flush(len);
+                            if (lane == 0) {
+                                if (len < kPathLds) lpath[len] = code;
+                                else st(&gp.path[len], code);
+                            }
+                            ++len;
                         };
                         // One read per node visited: a compute arc and the link arc
                         // after it come from the same word (entry predecessor in the
@@ -1047,10 +1042,20 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                             if (at_exit)
                                 for (;;) {
                                     const uint32_t fw = __builtin_amdgcn_readfirstlane(uint32_t(all_pred[kk * n + i]));
-                                    const int fen = int(fw & 0x7fffu) - 3, fex = int((fw >> 16) & 0x7fffu) - 3;
-                                    if ((fw & 0x80008000u) | (fex != kPredSplit) | (unsigned(fen) >= unsigned(n)) | (kk < 1)) break;
-                                    record(path_code(kArcSplitFwd, kk, i, 0));
-                                    record(path_code(kArcLinkFwd, kk - 1, fen, i));
+                                    const int fen = int(fw & 0x7fffu) - 3;
+                                    // no mark, the exit's predecessor is the compute arc,
+                                    // the entry's a node of stage kk - 1, and both arcs
+                                    // fit in LDS (sign bits of differences: the tests
+                                    // stay in scalar registers)
+                                    const uint32_t off = (fw & 0x80008000u) | ((fw >> 16) ^ uint32_t(kPredSplit + 3)) |
+                                                         (uint32_t(fen) >> 31) | (uint32_t(n - 1 - fen) >> 31) |
+                                                         (uint32_t(kk - 1) >> 31) | (uint32_t(kPathLds - 2 - len) >> 31);
+                                    if (off) break;
+                                    if (lane == 0) {
+                                        lpath[len] = path_code(kArcSplitFwd, kk, i, 0);
+                                        lpath[len + 1] = path_code(kArcLinkFwd, kk - 1, fen, i);
+                                    }
+                                    len += 2;
                                     kk -= 1;
                                     i = fen;
                                 }
@@ -1117,7 +1122,6 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                             at_exit = true;
                         }
                         if (state != 3) {
-                            if (state == 1 && (len & 63)) flush(len);
                             break;
                         }
                         from = next_tie();
