@@ -91,6 +91,7 @@ enum : int {
 // group: atomics on one word are performed one after another, so 256
 // arrivals on one counter take several microseconds.
 constexpr int kBarGroup = 16, kBarLine = 32;
+static_assert(kGridMaxNodes <= kGridThreads, "one thread per row of the previous stage");
 static_assert(kCtlTies + kGridMaxNodes / 32 <= kCtlStop, "control words overlap");
 static_assert(kCtlFinalKey + 2 <= kCtlTies, "control words overlap");
 static_assert(kCtlBarGroups + kBarLine * ((kGridMaxBlocks + kBarGroup - 1) / kBarGroup) <= kGridCtrlInts,
@@ -488,6 +489,9 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
     // Labels of a fresh shortest-path search: buffer 0 holds them as the
     // output of iteration 0; buffer 1 gets a tag no reader awaits before
     // iteration 1 overwrites it.
+    // this thread's row of exrow / enrow (tid < n), also kept in registers so
+    // that the per-iteration update needs no LDS read
+    int my_ex = kInf, my_en = kInf;
     auto reset_labels = [&]() {
         if (tid < kGridNB) {
             const int c = tid, q = k * n + j0 + c;
@@ -507,6 +511,8 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
             exrow[i] = kInf;
             enrow[i] = kInf;
         }
+        my_ex = kInf;
+        my_en = kInf;
         if (g == 0) {
             for (int r = tid; r < gp.ring_slots; r += kGridThreads) {
                 st(&gp.ring[r * kRingStride], 0u);
@@ -661,14 +667,14 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                 if (tid < n) {
                     if (has_prev) {
                         dnew = int(wex >> 2);
-                        dropped = dnew < exrow[tid];
-                        if (dropped) exrow[tid] = dnew;
+                        dropped = dnew < my_ex;
+                        if (dropped) exrow[tid] = my_ex = dnew;
                         rowkey[tid] = dropped ? (uint32_t(dnew) << 9) | uint32_t(tid) : kNoRowKey;
                     }
                     if (has_next) {
                         const int y = int(wen >> 2);
-                        en_drop = y < enrow[tid];
-                        enrow[tid] = y;
+                        en_drop = y < my_en;
+                        enrow[tid] = my_en = y;
                     }
                 }
                 const uint64_t m = __ballot(dropped);
