@@ -365,7 +365,7 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
         sh_key = ~0ull;
     }
     __syncthreads();
-    int bad = 0, wide = 0, mx = 0;
+    int bad = 0, wide = 0, holes = 0, mx = 0;
     if (tid < kGridNB) {
         const int c = tid;
         const bool own = c < nown;
@@ -436,6 +436,7 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
             const int a = (i < n && c < nown) ? layer[size_t(i) * n + j0 + c] : -1;
             bad |= a < -1;
             wide |= a > 65534;
+            holes |= (i < n) & (c < nown) & (a < 0);
             mx = max(mx, a);
             cost16[i * kGridNB + (c ^ (((i >> 2) & 7) << 4))] = (a < 0 || a > 65534) ? kNoArc16 : uint16_t(a);
         }
@@ -448,6 +449,7 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
     if (g == 0 && tid < 3) gpot[tid] = 0;
     if (bad) atomicOr(&sh_bad, 1);
     if (wide) atomicOr(&sh_bad, 2);
+    if (holes) atomicOr(&sh_bad, 4);
     atomicMax(&sh_maxc, mx);
     // flow-list capacity of each owned exit: min(cap, n, supply)
     int mine = 0;
@@ -467,6 +469,9 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
         atomicMax(&ctrl[kCtlMaxCost], sh_maxc);
     }
     bool timed_out = !bar.sync(&sh_ok, &sh_flag);
+    // some owned column misses a link from some row: a packed winner may then
+    // be a missing link (cost 65535) and is checked
+    const bool block_holes = (sh_bad & 4) != 0;
     int status = 0;
     if (!timed_out) {
         const int fl0 = ld(&ctrl[kCtlFlags]), maxc = ld(&ctrl[kCtlMaxCost]);
@@ -841,7 +846,7 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                     bool redo = false;
                     if (cq < nown && best < kNoRowKey) {
                         const int row = int(best & 511u);
-                        if (cost_at(row, cq) != kNoArc16) key = pack_key(int(best >> 9), row);
+                        if (!block_holes || cost_at(row, cq) != kNoArc16) key = pack_key(int(best >> 9), row);
                         else redo = true;
                     }
                     if (__any(redo)) {
