@@ -610,6 +610,27 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
                     // Every lane writes the (uniform) path entries.
                     static_assert(kChainDone > kChainBad, "one compare finds both markers");
                     while (okw) {
+                        // Most nodes are reached at their exit by the compute arc
+                        // and at their entry by a link from an exit of the stage
+                        // before: two entries and one read per node, with the
+                        // tests in scalar arithmetic; anything else takes the
+                        // general step below.
+                        while (v & 1u) {
+                            const uint64_t fb = *reinterpret_cast<const uint64_t *>(&chain[v - 1u]);
+                            const uint32_t flo = __builtin_amdgcn_readfirstlane(uint32_t(fb));
+                            const uint32_t fhi = __builtin_amdgcn_readfirstlane(uint32_t(fb >> 32));
+                            const uint32_t fnx = flo & kChainMask;
+                            // exit word leads to the entry, the entry's to an exit
+                            // (odd, so no marker: both markers are 0x1ffe and up,
+                            // and 0x1fff = done), room for two entries
+                            if ((fhi & kChainMask) != v - 1u) break;
+                            if ((fnx & 1u) == 0u || fnx == kChainDone) break;
+                            if (len > 2 * SN + 2) break;
+                            path[len] = int(fhi >> 13);
+                            path[len + 1] = int(flo >> 13);
+                            len += 2;
+                            v = fnx;
+                        }
                         // both words of the node in one 8-byte read
                         const uint64_t both = *reinterpret_cast<const uint64_t *>(&chain[v & ~1u]);
                         const uint32_t lo = __builtin_amdgcn_readfirstlane(uint32_t(both));
