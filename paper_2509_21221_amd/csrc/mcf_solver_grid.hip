@@ -30,11 +30,13 @@
 // workgroup writes for another (labels, predecessors, path, flows, control
 // words) moves through device-scope atomic loads and stores, which bypass
 // the non-coherent cache state, and no cache-wide write-back or invalidate is
-// needed.  The grid barrier (between a search and its augmentations) is one
-// arrival counter and one epoch word; it also ORs a one-bit flag over the
-// grid (used to report a fault), and its wait is bounded: a barrier that does
-// not complete within the bound ends the solve with the internal-error status
-// instead of hanging the device.  Every other wait is bounded the same way.
+// needed.  The grid barrier (between a search and its augmentations) counts
+// arrivals in groups of 16 workgroups and then per group, and releases with
+// one epoch word; it also ORs a one-bit flag over the grid (used to report a
+// fault), and its wait is bounded: a barrier that does not complete within
+// the bound ends the solve with the internal-error status instead of hanging
+// the device.  Every other wait is bounded the same way.  Words that many
+// workgroups update or poll each have a 128-byte line of their own.
 #include "mcf_device.h"
 #include "mcf_grid.h"
 
