@@ -759,6 +759,7 @@ def main():
         "unit": "instances/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": wall / args.steps * 1e3,
+        "ms_per_step_median": float(np.median(ev_ms)),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "int32", "data": "synthetic (seeded generator, paper-shaped)",
         "config": {"workload": WORKLOADS[args.config] + (", located form (node locations + latency matrix)"
