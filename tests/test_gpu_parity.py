@@ -196,14 +196,28 @@ def test_grid_pass_routing_and_status():
     (8, 8, 37, 0.2, 0.1), (6, 7, 9, 0.0, 0.2), (4, 2, 13, 0.3, 0.0), (8, 5, 70, 0.1, 0.1),
 ])
 def test_packed_pass_shapes(S, n, B, holes, zero):
-    """Shapes served by the packed pass (S <= 8, n <= 16): four instances per
-    wave (eight when n <= 8), batches that leave a wave partly empty, missing
-    links, deleted nodes."""
+    """Shapes served by the packed pass (S <= 8, n <= 16) in small batches
+    (one instance per wave), missing links, deleted nodes."""
     batch = W.random_small(B, S, n, seed=31, cap_hi=9, cost_hi=400, supply_hi=4 * n + 8,
                            holes=holes, zero_cap=zero)
     say("packed", S, n, B)
     g = gpu_solve(batch)
     compare(batch, g, oracle.solve(batch))
+    assert (g["passes"] == mcf.GWTF_PASS_PACKED).all()
+
+
+@pytest.mark.parametrize("S,n,B", [
+    (4, 6, 512), (4, 6, 513), (4, 6, 1024), (4, 6, 1025), (4, 6, 2040), (4, 6, 2041), (3, 12, 1100),
+])
+def test_packed_pass_instances_per_wave(S, n, B):
+    """Every launch shape of the packed pass at its batch-size boundaries:
+    one instance per wave up to 512 instances, two up to 1,024, four above
+    (n > 8, or up to 2,040 instances), eight per wave from 2,041 (n <= 8),
+    with the last wave partly empty."""
+    batch = W.random_small(B, S, n, seed=43, cap_hi=9, cost_hi=400, supply_hi=4 * n + 8, holes=0.1, zero_cap=0.1)
+    say("packed per wave", S, n, B)
+    g = gpu_solve(batch)
+    compare(batch, g, oracle.solve(batch), certify=[0, 1, B // 2, B - 2, B - 1])
     assert (g["passes"] == mcf.GWTF_PASS_PACKED).all()
 
 
