@@ -110,7 +110,7 @@ def valu_issue(kernel: str, config, kernel_s: float):
 
 
 KERNELS = {1: "solve_pipe_kernel", 2: "solve_kernel (LDS state)", 3: "solve_grid_kernel",
-           4: "solve_kernel (global-memory state)", 5: "solve_small_kernel (four instances per wave)"}
+           4: "solve_kernel (global-memory state)", 5: "solve_small_kernel (one to eight instances per wave)"}
 PASS_LAUNCHES = {1: " (keyed launch per step; the unscaled launch after it has no instance and exits)",
                  3: " (one cooperative launch per instance)"}
 KERNEL_SYMBOLS = {1: "solve_pipe_kernel", 2: "solve_kernel_lds", 3: "solve_grid_kernel", 4: "solve_kernel_global",

@@ -59,7 +59,7 @@ enum {
     GWTF_PASS_LDS = 2,      /* one workgroup, instance state in LDS: n <= 64 */
     GWTF_PASS_GRID = 3,     /* one instance over S * ceil(n/128) co-resident workgroups: 64 < n <= 512 */
     GWTF_PASS_GLOBAL = 4,   /* one workgroup, instance state in device memory: any shape */
-    GWTF_PASS_PACKED = 5    /* 4 (n <= 16) or 8 (n <= 8) instances per wave: S <= 8, supply <= 255, costs <= 2047 */
+    GWTF_PASS_PACKED = 5    /* 1 to 8 instances per wave (8 only for n <= 8): S <= 8, supply <= 255, costs <= 2047 */
 };
 
 /* arc_cost entry meaning "these two nodes share no link". */

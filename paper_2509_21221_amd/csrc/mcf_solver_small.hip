@@ -1,11 +1,13 @@
-// Packed pass for small instances: four instances per wave, for at most 8
-// stages of at most 16 nodes (the node-addition batches of paper Sec. VI and
-// the 4 x 4 / 8 x 8 presets).
+// Packed pass for small instances: one to eight instances per wave, for at
+// most 8 stages of at most 16 nodes (the node-addition batches of paper
+// Sec. VI and the 4 x 4 / 8 x 8 presets).
 //
 // Same method as the other passes (successive shortest paths with Johnson
 // potentials on the node-split stage graph, paper Sec. V-A Eq. 2); what
 // differs is the mapping.  One wave = four 16-lane rows (the DPP row of
-// CDNA), one instance per row, lane j of a row = node j of every stage:
+// CDNA), one instance per row (or per half row when n <= 8), lane j of a row
+// = node j of every stage; a small batch leaves some rows of each wave empty
+// so that it spreads over more waves:
 //
 //  * Keys.  A vertex label is kept as key = label << 5 | code, where code
 //    names the predecessor arc: for an entry, 0..15 = the link from that
