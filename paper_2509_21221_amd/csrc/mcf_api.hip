@@ -35,6 +35,7 @@ struct Workspace {
     bool grid = false;
     int64_t grid_slots = 0;
     size_t grid_lds = 0;
+    int grid_conc = 0; // instances per grid launch (buffers for that many)
     uint32_t *g_ex = nullptr, *g_en = nullptr, *g_ring = nullptr;
     unsigned long long *g_ring_key = nullptr;
     int32_t *g_pred = nullptr, *g_path = nullptr, *g_ctrl = nullptr;
@@ -71,8 +72,9 @@ hipError_t query_device(int device, DeviceInfo &d)
 // fallback state for the worst case (every exit vertex may need
 // min(cap, n, supply) <= n flow-list entries), and the grid pass when its
 // S * ceil(n / 128) workgroups can all be resident at once (cooperative
-// launch, one per CU given their LDS).
-void plan_workspace(Workspace &w, int S, int n, const DeviceInfo &d)
+// launch, one per CU given their LDS), with buffers for as many instances
+// per launch as can be resident together (at most B).
+void plan_workspace(Workspace &w, int S, int n, int B, const DeviceInfo &d)
 {
     w.fallback_slots = int64_t(std::max(S - 1, 0)) * n * n;
     w.state_stride = align16(make_layout(S, n, w.fallback_slots, false).total);
@@ -87,6 +89,8 @@ void plan_workspace(Workspace &w, int S, int n, const DeviceInfo &d)
                 w.grid = true;
                 w.grid_slots = slots;
                 w.grid_lds = lds;
+                w.grid_conc = int(std::min<int64_t>({int64_t(per_cu) * d.cus / blocks, int64_t(std::max(B, 1)),
+                                                     int64_t(kGridMaxConcurrent)}));
             }
         }
     }
@@ -98,20 +102,20 @@ template <class Fn>
 void for_each_buffer(Workspace &w, int S, int n, int B, Fn f)
 {
     const size_t SN = size_t(S) * n, V = 2 * SN + 3, na = size_t(std::max(S - 1, 0)) * n * n;
-    const size_t gsn = w.grid ? SN : 0;
+    const size_t gsn = w.grid ? SN : 0, gc = w.grid ? size_t(w.grid_conc) : 0;
     f((void **)&w.route, sizeof(int32_t) * B);
     f((void **)&w.node_flow, sizeof(int32_t) * SN * B);
     f((void **)&w.arc_flow, sizeof(int32_t) * std::max<size_t>(na, 1) * B);
     f((void **)&w.pot, sizeof(int32_t) * V * B);
     f((void **)&w.stats, sizeof(int64_t) * kStatsPerInstance * B);
     f((void **)&w.state, w.state_stride * B);
-    f((void **)&w.g_ex, sizeof(uint32_t) * 2 * gsn);
-    f((void **)&w.g_en, sizeof(uint32_t) * 2 * gsn);
-    f((void **)&w.g_pred, sizeof(int32_t) * gsn);
-    f((void **)&w.g_path, w.grid ? sizeof(int32_t) * (2 * gsn + 8) : 0);
-    f((void **)&w.g_ctrl, w.grid ? sizeof(int32_t) * kGridCtrlInts : 0);
-    f((void **)&w.g_ring, w.grid ? sizeof(uint32_t) * kRingStride * grid_ring_slots(S) : 0);
-    f((void **)&w.g_ring_key, w.grid ? sizeof(unsigned long long) * kRingKeyStride * grid_ring_slots(S) : 0);
+    f((void **)&w.g_ex, sizeof(uint32_t) * 2 * gsn * gc);
+    f((void **)&w.g_en, sizeof(uint32_t) * 2 * gsn * gc);
+    f((void **)&w.g_pred, sizeof(int32_t) * gsn * gc);
+    f((void **)&w.g_path, sizeof(int32_t) * (2 * gsn + 8) * gc);
+    f((void **)&w.g_ctrl, sizeof(int32_t) * kGridCtrlInts * gc);
+    f((void **)&w.g_ring, sizeof(uint32_t) * kRingStride * grid_ring_slots(S) * gc);
+    f((void **)&w.g_ring_key, sizeof(unsigned long long) * kRingKeyStride * grid_ring_slots(S) * gc);
 }
 
 } // namespace
@@ -210,7 +214,7 @@ extern "C" gwtf_status_t gwtf_mcf_create(const gwtf_mcf_shape_t *shape, void *hi
         delete h;
         return fail_thread(GWTF_ERR_DEVICE, "hipDeviceGetAttribute", e);
     }
-    plan_workspace(h->ws, S, n, h->dev);
+    plan_workspace(h->ws, S, n, B, h->dev);
     hipError_t first = hipSuccess;
     for_each_buffer(h->ws, S, n, B, [&](void **p, size_t bytes) {
         if (bytes == 0 || first != hipSuccess) return;
@@ -265,9 +269,9 @@ PassResult run_passes(const Workspace &w, const DeviceInfo &d, int S, int n, hip
         if ((e = launch_small_pass(p, stream)) != hipSuccess) return {GWTF_ERR_DEVICE, "packed solver launch", e};
         need_fallback = true;
     } else if (w.grid) {
-        // One cooperative launch per instance; instances whose link costs
-        // need more than 16 bits or whose flow lists outgrow LDS go to the
-        // fallback pass.
+        // Cooperative launches of up to grid_conc instances each; instances
+        // whose link costs need more than 16 bits or whose flow lists outgrow
+        // LDS go to the fallback pass.
         GridParams gp{};
         gp.base = p;
         gp.base.list_slots = w.grid_slots;
@@ -286,8 +290,9 @@ PassResult run_passes(const Workspace &w, const DeviceInfo &d, int S, int n, hip
         gp.loc = loc;
         gp.lat = lat;
         gp.L = L;
-        for (int i = 0; i < p.B; ++i) {
+        for (int i = 0; i < p.B; i += w.grid_conc) {
             gp.instance = i;
+            gp.count = std::min(w.grid_conc, p.B - i);
             if ((e = launch_grid_pass(gp, w.grid_lds, stream)) != hipSuccess)
                 return {GWTF_ERR_DEVICE, "grid solver launch", e};
         }
@@ -450,7 +455,7 @@ extern "C" gwtf_status_t gwtf_mcf_solve_batch_noalloc(const gwtf_mcf_shape_t *sh
     // Lay the workspace of this batch out in the array (256-byte aligned
     // buffers), or refuse the batch if it does not fit.
     Workspace w;
-    plan_workspace(w, S, n, dev);
+    plan_workspace(w, S, n, b->batch, dev);
     size_t need = 0;
     for_each_buffer(w, S, n, b->batch, [&](void **, size_t bytes) {
         if (bytes) need = ((need + 255) & ~size_t(255)) + bytes;

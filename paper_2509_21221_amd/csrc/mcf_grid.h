@@ -1,6 +1,7 @@
 // Internal interface of the grid-cooperative pass (mcf_solver_grid.hip):
-// one instance at a time over S * ceil(n / 128) co-resident workgroups,
-// for 64 < n <= 512.  Not part of the public C ABI.
+// each instance over S * ceil(n / 128) co-resident workgroups, as many
+// instances per launch as fit at once, for 64 < n <= 512.  Not part of the
+// public C ABI.
 #pragma once
 
 #include "mcf_internal.h"
@@ -8,7 +9,8 @@
 namespace gwtf {
 
 constexpr int kGridCtrlInts = 1280;    // control block: flags, barrier, per-iteration words, tied exits
-constexpr int kGridMaxBlocks = 512;    // workgroups of one grid launch (the barrier's group counters)
+constexpr int kGridMaxBlocks = 512;    // workgroups of one instance (the barrier's group counters)
+constexpr int kGridMaxConcurrent = 64; // instances of one grid launch
 // Ring slots and their sink keys sit 128 bytes apart: every workgroup adds
 // its arrival to a slot each iteration, and atomics on one line serialize.
 constexpr int kRingStride = 32, kRingKeyStride = 16;
@@ -16,10 +18,12 @@ constexpr int kGridMaxNodes = 512;     // a stage's labels are staged with one t
 constexpr size_t kGridStaticLds = 512; // static LDS of the grid kernel (upper bound)
 struct GridParams {
     SolveParams base;
-    int32_t instance;   // instance solved by this launch
+    int32_t instance;   // first instance solved by this launch
+    int32_t count;      // instances solved by this launch, S * slices workgroups each
     int32_t slices;     // workgroups per stage
     int64_t list_slots; // flow-list capacity of one workgroup
     size_t big_bytes;   // leading LDS area: link-cost block or staged predecessors
+    // per instance of the launch, one after another:
     uint32_t *ex, *en;  // [2][S*n] exit / entry labels << 2 | iteration tag, by iteration parity
     uint32_t *ring;     // [ring_slots * kRingStride] per-iteration arrivals (low 16 bits) and changed count
     unsigned long long *ring_key; // [ring_slots * kRingKeyStride] per-iteration minimum sink key

@@ -1,8 +1,11 @@
-// Grid-cooperative solver pass for one large instance (64 < n <= 512).
+// Grid-cooperative solver pass for large instances (64 < n <= 512).
 //
 // Same objective and method as the other passes -- successive shortest paths
 // with Johnson potentials on the node-split stage graph (paper Sec. V-A,
-// Eq. 2) -- spread over the whole GPU instead of one workgroup:
+// Eq. 2) -- spread over many workgroups instead of one.  A launch solves as
+// many instances as can be resident together; its workgroups are numbered
+// instance by instance, S * slices per instance, and g below counts within
+// the instance:
 //
 //  * Workgroup g owns a block of NB = 128 nodes of one stage k (g = k *
 //    slices + s covers nodes s*NB ...): their entry/exit labels, predecessors,
@@ -20,7 +23,7 @@
 //    Convergence is counted on a ring of per-iteration arrival counters; the
 //    last arrival of an iteration in which no label below the sink's changed
 //    publishes the sink's key and a stop word.
-//  * Workgroup 0 (stage 0, which holds no link costs) stages all
+//  * The instance's workgroup 0 (stage 0, which holds no link costs) stages all
 //    predecessors in its LDS, walks the augmenting path and finds its
 //    bottleneck; each owner then applies the path to its nodes and lists.
 //    The last stage's other exits that reach the sink at the same label are
@@ -229,6 +232,7 @@ __device__ __forceinline__ void drain() { asm volatile("s_waitcnt vmcnt(0)" ::: 
 struct GridBarrier {
     unsigned *count, *word, *flags, *groups;
     unsigned nblocks, epoch;
+    unsigned me; // this workgroup among the instance's nblocks
 
     __device__ bool sync(bool raise, int *ok_lds, int *flag_lds)
     {
@@ -239,7 +243,7 @@ struct GridBarrier {
                 atomicOr(flags, 1u);
                 drain();
             }
-            const unsigned grp = blockIdx.x / kBarGroup, ngroups = (nblocks + kBarGroup - 1) / kBarGroup;
+            const unsigned grp = me / kBarGroup, ngroups = (nblocks + kBarGroup - 1) / kBarGroup;
             const unsigned gsize = min(unsigned(kBarGroup), nblocks - grp * kBarGroup);
             bool good = true, last = false;
             unsigned w = 0;
@@ -271,12 +275,28 @@ struct GridBarrier {
     __device__ bool sync(int *ok_lds, int *flag_lds) { return sync(false, ok_lds, flag_lds); }
 };
 
-template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams gp)
+template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solve_grid_kernel(GridParams all)
 {
+    // One launch solves all.count instances, S * slices workgroups each;
+    // each instance has its own run of the label, ring, predecessor, path
+    // and control buffers.
+    const int nbi = all.base.S * all.slices, li = int(blockIdx.x) / nbi;
+    GridParams gp = all;
+    {
+        const size_t sn = size_t(all.base.S) * all.base.n;
+        gp.instance += li;
+        gp.ex += size_t(li) * 2 * sn;
+        gp.en += size_t(li) * 2 * sn;
+        gp.pred += size_t(li) * sn;
+        gp.path += size_t(li) * (2 * sn + 8);
+        gp.ctrl += size_t(li) * kGridCtrlInts;
+        gp.ring += size_t(li) * kRingStride * all.ring_slots;
+        gp.ring_key += size_t(li) * kRingKeyStride * all.ring_slots;
+    }
     const SolveParams &p = gp.base;
     const int b = gp.instance;
     const int S = p.S, n = p.n, SN = S * n, V = 2 * SN + 3;
-    const int g = blockIdx.x, k = g / gp.slices, s = g % gp.slices;
+    const int g = int(blockIdx.x) - li * nbi, k = g / gp.slices, s = g % gp.slices;
     const int j0 = s * kGridNB, nown = min(kGridNB, n - j0);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     // rows of the previous stage rounded up to whole groups of 32 (the link
@@ -347,7 +367,7 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
     unsigned long long *sinkbest_w = reinterpret_cast<unsigned long long *>(ctrl + kCtlSinkBest);
     GridBarrier bar{reinterpret_cast<unsigned *>(ctrl + kCtlBarCount), reinterpret_cast<unsigned *>(ctrl + kCtlBarWord),
                     reinterpret_cast<unsigned *>(ctrl + kCtlBarFlags), reinterpret_cast<unsigned *>(ctrl + kCtlBarGroups),
-                    gridDim.x, 0u};
+                    unsigned(nbi), 0u, unsigned(g)};
     if (tid == 0) bar.epoch = ld(bar.word) >> 1;
 
     const int32_t *gcap = p.cap + size_t(b) * SN;
@@ -658,7 +678,7 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
                 }
                 if (ring_slot >= 0) {
                     const unsigned total = ring_old + ring_mine;
-                    if ((total & 0xffffu) == gridDim.x) {
+                    if ((total & 0xffffu) == unsigned(nbi)) {
                         if ((total >> 16) == 0) {
                             st(final_key_w, ld(&gp.ring_key[ring_slot * kRingKeyStride]));
                             drain();
@@ -1335,9 +1355,9 @@ template <bool kLocated> __global__ __launch_bounds__(kGridThreads, 1) void solv
     }
 }
 
-__global__ void grid_ctrl_reset_kernel(int32_t *ctrl)
+__global__ void grid_ctrl_reset_kernel(int32_t *ctrl, int count)
 {
-    for (int i = threadIdx.x; i < kGridCtrlInts; i += blockDim.x) ctrl[i] = 0;
+    for (int i = threadIdx.x; i < count * kGridCtrlInts; i += blockDim.x) ctrl[i] = 0;
 }
 
 size_t lds_fixed(int S, int n)
@@ -1396,14 +1416,14 @@ int grid_pass_blocks_per_cu(size_t lds_bytes)
 
 hipError_t launch_grid_pass(const GridParams &gp, size_t lds_bytes, hipStream_t s)
 {
-    hipLaunchKernelGGL(grid_ctrl_reset_kernel, dim3(1), dim3(256), 0, s, gp.ctrl);
+    hipLaunchKernelGGL(grid_ctrl_reset_kernel, dim3(1), dim3(256), 0, s, gp.ctrl, gp.count);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     GridParams arg = gp;
     void *args[] = {&arg};
     const void *f = gp.loc ? reinterpret_cast<const void *>(solve_grid_kernel<true>)
                            : reinterpret_cast<const void *>(solve_grid_kernel<false>);
-    return hipLaunchCooperativeKernel(f, dim3(unsigned(gp.base.S * gp.slices)), dim3(kGridThreads), args,
+    return hipLaunchCooperativeKernel(f, dim3(unsigned(gp.count * gp.base.S * gp.slices)), dim3(kGridThreads), args,
                                       unsigned(lds_bytes), s);
 }
 

@@ -135,6 +135,28 @@ def test_grid_pass_shapes(S, n, holes, zero):
     assert (g["passes"] == mcf.GWTF_PASS_GRID).all()
 
 
+@pytest.mark.parametrize("S,n,B", [(6, 90, 40), (4, 130, 70), (33, 100, 9), (1, 300, 300)])
+def test_grid_pass_batches(S, n, B):
+    """Batches on the grid pass: as many instances per cooperative launch as
+    can be resident together (each with its own labels, ring, predecessors,
+    path and control block), the batch split over several launches when it
+    holds more, every instance against the oracle."""
+    batch = W.random_small(B, S, n, seed=47, cap_hi=5, cost_hi=300, supply_hi=2 * n, holes=0.1, zero_cap=0.1)
+    say("grid batch", S, n, B)
+    g = gpu_solve(batch, stats=True)
+    compare(batch, g, oracle.solve(batch), certify=[0, B // 2, B - 1])
+    assert (g["passes"] == mcf.GWTF_PASS_GRID).all()
+    # Each instance's searches converge as they do when it is solved alone:
+    # the label iterations per instance (stats column 1) stay within a few
+    # percent (the pipelined iterations are not strictly deterministic), so a
+    # convergence count that mixed instances would show here.
+    for b in (0, B - 1):
+        one = gpu_solve(batch.subset([b]), flows=False, stats=True)
+        assert one["F"][0] == g["F"][b] and one["cost"][0] == g["cost"][b]
+        r_batch, r_one = int(g["stats"][b, 1]), int(one["stats"][0, 1])
+        assert abs(r_batch - r_one) <= max(8, r_one // 10), (b, r_batch, r_one)
+
+
 @pytest.mark.parametrize("S,n,cost_hi", [(3, 200, 0), (6, 130, 1), (12, 300, 2), (4, 512, 3)])
 def test_grid_pass_tied_exits(S, n, cost_hi):
     """Costs drawn from a handful of values make many exits of the last
