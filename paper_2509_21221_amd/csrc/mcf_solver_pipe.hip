@@ -563,18 +563,23 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
             // ---- (2) stage predecessors ----
             const int Dt = key_label(fk), predt = int(uint32_t(fk));
             const int dred = Dt - pit;
+            // The lane index, opaque here so that the per-lane addresses and
+            // words below are computed after each search rather than held in
+            // registers across the label iterations (which would spill them).
+            int ln = lane;
+            __asm__ volatile("" : "+v"(ln));
 #pragma unroll
             for (int s = 0; s < P; ++s) {
                 const int k = k0 + s;
                 if (k > klast) break;
-                const int q = k * 64 + lane, pi = pred_in(pp[s]), po = pred_out(pp[s]);
+                const int q = k * 64 + ln, pi = pred_in(pp[s]), po = pred_out(pp[s]);
                 uint32_t ein, eout;
                 if (pi == kPredSrc) ein = kChainDone;
-                else if (pi == kPredSplit) ein = chain_word(2 * q + 1, arc_code(kArcSplitRev, k, lane, 0));
-                else if (pi >= 0 && pi < n && k >= 1) ein = chain_word(2 * ((k - 1) * 64 + pi) + 1, arc_code(kArcLinkFwd, k - 1, pi, lane));
+                else if (pi == kPredSplit) ein = chain_word(2 * q + 1, arc_code(kArcSplitRev, k, ln, 0));
+                else if (pi >= 0 && pi < n && k >= 1) ein = chain_word(2 * ((k - 1) * 64 + pi) + 1, arc_code(kArcLinkFwd, k - 1, pi, ln));
                 else ein = kChainBad;
-                if (po == kPredSplit) eout = chain_word(2 * q, arc_code(kArcSplitFwd, k, lane, 0));
-                else if (po >= 0 && po < n && k + 1 < S) eout = chain_word(2 * ((k + 1) * 64 + po), arc_code(kArcLinkRev, k, lane, po));
+                if (po == kPredSplit) eout = chain_word(2 * q, arc_code(kArcSplitFwd, k, ln, 0));
+                else if (po >= 0 && po < n && k + 1 < S) eout = chain_word(2 * ((k + 1) * 64 + po), arc_code(kArcLinkRev, k, ln, po));
                 else eout = kChainBad;
                 chain[2 * q] = ein;
                 chain[2 * q + 1] = eout;
@@ -587,7 +592,7 @@ __global__ __launch_bounds__(64 * W, 1) void solve_pipe_kernel(SolveParams p)
                 for (int s = 0; s < P; ++s) {
                     const int k = k0 + s;
                     if (k <= klast && jv) {
-                        int32_t *pin = gpot + 3 + 2 * (k * n + lane);
+                        int32_t *pin = gpot + 3 + 2 * (k * n + ln);
                         const int a = pin[0], c = pin[1];
                         pin[0] = min(din[s], a + dred);
                         pin[1] = min(dout[s], c + dred);
