@@ -81,6 +81,17 @@ def test_random_located(S, n, L, B, expect_pass):
     assert (g["passes"] == expect_pass).all()
 
 
+def test_located_grid_batch_over_several_launches():
+    """A located batch on the factored grid pass that needs several
+    cooperative launches (40 workgroups per instance, six instances per
+    launch on 256 CUs): every instance against the located oracle."""
+    lb = W.random_located(14, 40, 70, 6, seed=29, supply_hi=60)
+    say("located grid batch", 40, 70, 14)
+    g = gpu_solve_located(lb, flows=False)
+    check(lb, g, OL.solve(lb, flows=False, potentials=False))
+    assert (g["passes"] == mcf.GWTF_PASS_GRID).all()
+
+
 @pytest.mark.parametrize("S,n", [(3, 5), (3, 90)])
 def test_invalid_locations_and_latencies(S, n):
     lb = W.random_located(5, S, n, 4, seed=8, supply_hi=20)
