@@ -199,7 +199,7 @@ __device__ bool find_cycle(Inst &I, Shared &sh, int L)
 __device__ int correct_labels(Inst &I, Shared &sh, bool from_source, int32_t bound, int L, int64_t &rounds,
                               int64_t phase_start)
 {
-    const int tid = threadIdx.x, nt = blockDim.x, V = I.V;
+    const int tid = threadIdx.x, nt = blockDim.x, V = I.V, Sn = I.S * I.n;
     for (int v = tid; v < V; v += nt) {
         I.d[v] = (!from_source || v == 0) ? 0 : kInf;
         I.pred[v] = -1;
@@ -209,7 +209,10 @@ __device__ int correct_labels(Inst &I, Shared &sh, bool from_source, int32_t bou
     for (int it = 0;; ++it) {
         if (tid == 0) sh.flag[(it + 1) % 3] = 0;
         int f = 0;
-        for (int v = tid; v < V; v += nt) {
+        // all entry vertices first, then all exits, then s and t, so that a
+        // wave pulls one kind of vertex at a time
+        for (int q = tid; q < V; q += nt) {
+            const int v = q < Sn ? 2 + 2 * q : (q < 2 * Sn ? 3 + 2 * (q - Sn) : q - 2 * Sn);
             int32_t best;
             int bp;
             pull(I, v, best, bp);
