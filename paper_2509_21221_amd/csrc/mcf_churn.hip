@@ -48,7 +48,13 @@ __device__ inline int vout(int nd) { return 3 + 2 * nd; }
 struct Inst {
     int32_t *ac, *af, *cap, *nc, *nf, *src, *snk, *sf, *tf, *d, *pred, *anc, *anc2;
     int S, n, V;
+    float inv_n; // 1 / n, for the stage of a node index without an integer division
 };
+
+// Stage of node nd: (nd + 1/2) / n is at least 1/(2n) >= 2^-10 away from
+// every integer, and the float product is within S * 2^-23 <= 2^-14 of it
+// (S * n <= kChurnMaxNodes), so truncation gives nd / n exactly.
+__device__ inline int stage_of(const Inst &I, int nd) { return int((float(nd) + 0.5f) * I.inv_n); }
 
 // Residual capacity of the residual arc u -> v (which must exist).
 __device__ int32_t residual(const Inst &I, int u, int v)
@@ -101,7 +107,7 @@ __device__ void pull(const Inst &I, int v, int32_t &best, int &bp)
     } else if (v == 1) {
         for (int i = 0; i < n; ++i) take(vout((S - 1) * n + i), I.snk[i]);
     } else {
-        const int nd = (v - 2) >> 1, k = nd / n, i = nd - k * n;
+        const int nd = (v - 2) >> 1, k = stage_of(I, nd), i = nd - k * n;
         if (((v - 2) & 1) == 0) {
             if (k == 0) {
                 take(0, I.src[i]);
@@ -244,6 +250,7 @@ __global__ void __launch_bounds__(kChurnThreads) churn_kernel(ChurnParams p)
     I.S = S;
     I.n = n;
     I.V = V;
+    I.inv_n = 1.0f / float(n);
     int32_t *q = lds;
     I.ac = q; q += links;
     I.af = q; q += links;
