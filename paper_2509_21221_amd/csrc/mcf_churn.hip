@@ -46,8 +46,12 @@ __device__ inline int vin(int nd) { return 2 + 2 * nd; }
 __device__ inline int vout(int nd) { return 3 + 2 * nd; }
 
 struct Inst {
+    // ac, af: link costs and flows, row r = k*n + i (exit i of stage k) at
+    // r * ld, column j = entry j of stage k+1; ld = n + 1 is odd, so the
+    // threads of a wave that read along rows or columns of different stages
+    // fall on different LDS banks
     int32_t *ac, *af, *cap, *nc, *nf, *src, *snk, *sf, *tf, *d, *pred, *anc, *anc2;
-    int S, n, V;
+    int S, n, V, ld;
     float inv_n; // 1 / n, for the stage of a node index without an integer division
 };
 
@@ -67,7 +71,7 @@ __device__ int32_t residual(const Inst &I, int u, int v)
     const bool uout = (u - 2) & 1;
     if (nu == nv) return uout ? I.nf[nu] : I.cap[nu] - I.nf[nu];
     if (uout) return kResInf;
-    return I.af[nv * I.n + nu % I.n];
+    return I.af[nv * I.ld + nu % I.n];
 }
 
 // Push delta along the residual arc u -> v.
@@ -81,8 +85,8 @@ __device__ void push(Inst &I, int u, int v, int32_t delta)
         const int nu = (u - 2) >> 1, nv = (v - 2) >> 1;
         const bool uout = (u - 2) & 1;
         if (nu == nv) I.nf[nu] += uout ? -delta : delta;
-        else if (uout) I.af[nu * I.n + nv % I.n] += delta;
-        else I.af[nv * I.n + nu % I.n] -= delta;
+        else if (uout) I.af[nu * I.ld + nv % I.n] += delta;
+        else I.af[nv * I.ld + nu % I.n] -= delta;
     }
 }
 
@@ -112,9 +116,9 @@ __device__ void pull(const Inst &I, int v, int32_t &best, int &bp)
             if (k == 0) {
                 take(0, I.src[i]);
             } else {
-                const int32_t *col = I.ac + (k - 1) * n * n + i;
+                const int32_t *col = I.ac + (k - 1) * n * I.ld + i;
                 for (int j = 0; j < n; ++j) {
-                    const int32_t a = col[j * n];
+                    const int32_t a = col[j * I.ld];
                     if (a >= 0) take(vout((k - 1) * n + j), a);
                 }
             }
@@ -122,7 +126,7 @@ __device__ void pull(const Inst &I, int v, int32_t &best, int &bp)
         } else {
             if (I.nf[nd] < I.cap[nd]) take(vin(nd), I.nc[nd]);
             if (k < S - 1) {
-                const int row = nd * n;
+                const int row = nd * I.ld;
                 for (int j = 0; j < n; ++j)
                     if (I.af[row + j] > 0) take(vin((k + 1) * n + j), -I.ac[row + j]);
             } else if (I.tf[i] > 0) {
@@ -145,24 +149,24 @@ __device__ int32_t strip_path(Inst &I, int k0, int i0, int k1, int i1, int32_t w
     P[k1] = i1;
     for (int k = k0; k > 0; --k) {
         int j = 0;
-        while (j < n && I.af[((k - 1) * n + j) * n + P[k]] <= 0) ++j;
+        while (j < n && I.af[((k - 1) * n + j) * I.ld + P[k]] <= 0) ++j;
         if (j == n) return 0;
         P[k - 1] = j;
     }
     for (int k = k1; k < S - 1; ++k) {
         int j = 0;
-        while (j < n && I.af[(k * n + P[k]) * n + j] <= 0) ++j;
+        while (j < n && I.af[(k * n + P[k]) * I.ld + j] <= 0) ++j;
         if (j == n) return 0;
         P[k + 1] = j;
     }
     int32_t delta = min(want, min(I.sf[P[0]], I.tf[P[S - 1]]));
     for (int k = 0; k < S; ++k) delta = min(delta, I.nf[k * n + P[k]]);
-    for (int k = 0; k + 1 < S; ++k) delta = min(delta, I.af[(k * n + P[k]) * n + P[k + 1]]);
+    for (int k = 0; k + 1 < S; ++k) delta = min(delta, I.af[(k * n + P[k]) * I.ld + P[k + 1]]);
     if (delta <= 0) return 0;
     I.sf[P[0]] -= delta;
     I.tf[P[S - 1]] -= delta;
     for (int k = 0; k < S; ++k) I.nf[k * n + P[k]] -= delta;
-    for (int k = 0; k + 1 < S; ++k) I.af[(k * n + P[k]) * n + P[k + 1]] -= delta;
+    for (int k = 0; k + 1 < S; ++k) I.af[(k * n + P[k]) * I.ld + P[k + 1]] -= delta;
     return delta;
 }
 
@@ -243,6 +247,7 @@ __global__ void __launch_bounds__(kChurnThreads) churn_kernel(ChurnParams p)
     extern __shared__ int32_t lds[];
     __shared__ Shared sh;
     const int S = p.S, n = p.n, Sn = S * n, V = 2 * Sn + 2, links = (S - 1) * n * n;
+    const int ld = n + 1, plinks = (S - 1) * n * ld; // padded rows in LDS
     const int tid = threadIdx.x, nt = blockDim.x;
     const int64_t b = blockIdx.x, s0 = p.start_per_instance ? b : 0;
 
@@ -250,10 +255,11 @@ __global__ void __launch_bounds__(kChurnThreads) churn_kernel(ChurnParams p)
     I.S = S;
     I.n = n;
     I.V = V;
+    I.ld = ld;
     I.inv_n = 1.0f / float(n);
     int32_t *q = lds;
-    I.ac = q; q += links;
-    I.af = q; q += links;
+    I.ac = q; q += plinks;
+    I.af = q; q += plinks;
     I.cap = q; q += Sn;
     I.nc = q; q += Sn;
     I.nf = q; q += Sn;
@@ -281,10 +287,15 @@ __global__ void __launch_bounds__(kChurnThreads) churn_kernel(ChurnParams p)
     int32_t mx = 0;
     for (int e = tid; e < links; e += nt) {
         const int32_t a = p.acost[b * links + e], f = p.af0[s0 * links + e];
-        I.ac[e] = a;
-        I.af[e] = f;
+        const int r = e / n, at = r * ld + (e - r * n);
+        I.ac[at] = a;
+        I.af[at] = f;
         bad |= (a < -1) | (f < 0) | (f >= kFlowMax);
         mx = max(mx, a);
+    }
+    for (int r = tid; r < (S - 1) * n; r += nt) {
+        I.ac[r * ld + n] = -1; // the padding column: no link, no flow
+        I.af[r * ld + n] = 0;
     }
     for (int e = tid; e < Sn; e += nt) {
         const int32_t c = p.cap[b * Sn + e], w = p.ncost[b * Sn + e], f = p.nf0[s0 * Sn + e];
@@ -313,9 +324,9 @@ __global__ void __launch_bounds__(kChurnThreads) churn_kernel(ChurnParams p)
         const int k = nd / n, i = nd - k * n;
         int64_t in = 0, out = 0;
         if (k == 0) in = I.sf[i];
-        else for (int j = 0; j < n; ++j) in += I.af[((k - 1) * n + j) * n + i];
+        else for (int j = 0; j < n; ++j) in += I.af[((k - 1) * n + j) * ld + i];
         if (k == S - 1) out = I.tf[i];
-        else for (int j = 0; j < n; ++j) out += I.af[nd * n + j];
+        else for (int j = 0; j < n; ++j) out += I.af[nd * ld + j];
         bad |= (in != I.nf[nd]) | (out != I.nf[nd]);
     }
     if (bad) atomicOr(&sh.bad, 1);
@@ -343,9 +354,9 @@ __global__ void __launch_bounds__(kChurnThreads) churn_kernel(ChurnParams p)
                 }
             }
             for (int e = 0; ok && e < links; ++e) {
-                const int k = e / (n * n), i = (e / n) % n, j = e % n;
-                while (ok && I.ac[e] < 0 && I.af[e] > 0) {
-                    const int32_t r = strip_path(I, k, i, k + 1, j, I.af[e]);
+                const int k = e / (n * n), i = (e / n) % n, j = e % n, at = (k * n + i) * ld + j;
+                while (ok && I.ac[at] < 0 && I.af[at] > 0) {
+                    const int32_t r = strip_path(I, k, i, k + 1, j, I.af[at]);
                     ok = r > 0;
                     F -= r;
                     ++removed;
@@ -407,7 +418,7 @@ __global__ void __launch_bounds__(kChurnThreads) churn_kernel(ChurnParams p)
         }
     }
     if (restart) {
-        for (int e = tid; e < links; e += nt) I.af[e] = 0;
+        for (int e = tid; e < plinks; e += nt) I.af[e] = 0;
         for (int e = tid; e < Sn; e += nt) I.nf[e] = 0;
         for (int i = tid; i < n; i += nt) I.sf[i] = I.tf[i] = 0;
         __syncthreads();
@@ -454,7 +465,7 @@ __global__ void __launch_bounds__(kChurnThreads) churn_kernel(ChurnParams p)
     const bool ok = status == GWTF_INST_OK;
     int64_t part = 0;
     if (ok) {
-        for (int e = tid; e < links; e += nt)
+        for (int e = tid; e < plinks; e += nt)
             if (I.af[e] > 0) part += int64_t(I.ac[e]) * I.af[e];
         for (int e = tid; e < Sn; e += nt) part += int64_t(I.nc[e]) * I.nf[e];
         for (int i = tid; i < n; i += nt) part += int64_t(I.src[i]) * I.sf[i] + int64_t(I.snk[i]) * I.tf[i];
@@ -473,7 +484,10 @@ __global__ void __launch_bounds__(kChurnThreads) churn_kernel(ChurnParams p)
         }
     }
     if (p.nf_out) {
-        for (int e = tid; e < links; e += nt) p.af_out[b * links + e] = ok ? I.af[e] : 0;
+        for (int e = tid; e < links; e += nt) {
+            const int r = e / n;
+            p.af_out[b * links + e] = ok ? I.af[r * ld + (e - r * n)] : 0;
+        }
         for (int e = tid; e < Sn; e += nt) p.nf_out[b * Sn + e] = ok ? I.nf[e] : 0;
         for (int i = tid; i < n; i += nt) {
             p.sf_out[b * n + i] = ok ? I.sf[i] : 0;
@@ -487,7 +501,7 @@ __global__ void __launch_bounds__(kChurnThreads) churn_kernel(ChurnParams p)
 size_t churn_lds_bytes(int S, int n)
 {
     const size_t Sn = size_t(S) * n, V = 2 * Sn + 2;
-    return sizeof(int32_t) * (2 * size_t(S - 1) * n * n + 3 * Sn + 4 * size_t(n) + 4 * V);
+    return sizeof(int32_t) * (2 * size_t(S - 1) * n * (n + 1) + 3 * Sn + 4 * size_t(n) + 4 * V);
 }
 
 hipError_t launch_churn_resolve(const ChurnParams &p, hipStream_t stream)
