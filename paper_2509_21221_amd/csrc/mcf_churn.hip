@@ -232,7 +232,9 @@ __device__ int correct_labels(Inst &I, Shared &sh, bool from_source, int32_t bou
                 f |= best < -bound ? 3 : 1;
             }
         }
-        if (f) atomicOr(&sh.flag[it % 3], f);
+        // one flag update per wave (the lanes' flags are ORed by ballot first)
+        const int wf = (__ballot(f & 1) ? 1 : 0) | (__ballot(f & 2) ? 2 : 0);
+        if (wf && (threadIdx.x & 63) == 0) atomicOr(&sh.flag[it % 3], wf);
         __syncthreads();
         const int fl = sh.flag[it % 3];
         ++rounds;
