@@ -193,10 +193,13 @@ __device__ bool find_cycle(Inst &I, Shared &sh, int L)
         a = a2;
         a2 = t;
     }
+    int low = V; // lowest vertex on a cycle among this thread's ancestors
     for (int v = tid; v < V; v += nt) {
         const int x = a[v];
-        if (I.pred[x] >= 0) atomicMin(&sh.found, x);
+        if (I.pred[x] >= 0) low = min(low, x);
     }
+    for (int off = 32; off > 0; off >>= 1) low = min(low, __shfl_xor(low, off, 64));
+    if (low < V && (tid & 63) == 0) atomicMin(&sh.found, low);
     __syncthreads();
     return sh.found < V;
 }
