@@ -57,7 +57,7 @@ enum {
 enum {
     GWTF_PASS_REGISTER = 1, /* one workgroup, link costs in registers: 16 < n <= 64, S <= 32 */
     GWTF_PASS_LDS = 2,      /* one workgroup, instance state in LDS: n <= 64 */
-    GWTF_PASS_GRID = 3,     /* one instance over S * ceil(n/128) co-resident workgroups: 64 < n <= 512 */
+    GWTF_PASS_GRID = 3,     /* each instance over S * ceil(n/128) co-resident workgroups: 64 < n <= 512, or 16 < n <= 64 with S > 32 in small batches */
     GWTF_PASS_GLOBAL = 4,   /* one workgroup, instance state in device memory: any shape */
     GWTF_PASS_PACKED = 5    /* 1 to 8 instances per wave (8 only for n <= 8): S <= 8, supply <= 255, costs <= 2047 */
 };

@@ -73,13 +73,15 @@ hipError_t query_device(int device, DeviceInfo &d)
 // min(cap, n, supply) <= n flow-list entries), and the grid pass when its
 // S * ceil(n / 128) workgroups can all be resident at once (cooperative
 // launch, one per CU given their LDS), with buffers for as many instances
-// per launch as can be resident together (at most B).
+// per launch as can be resident together (at most B).  The grid pass serves
+// 64 < n <= 512, and pipelines too long for the register pass with
+// 16 < n <= 64 when the batch is small (grid_preferred).
 void plan_workspace(Workspace &w, int S, int n, int B, const DeviceInfo &d)
 {
     w.fallback_slots = int64_t(std::max(S - 1, 0)) * n * n;
     w.state_stride = align16(make_layout(S, n, w.fallback_slots, false).total);
     w.grid = false;
-    if (n > 64 && n <= kGridMaxNodes && S <= 1024 && d.coop && d.cus > 0) {
+    if ((n > 64 || (n > 16 && !pipe_pass_fits(S, n))) && n <= kGridMaxNodes && S <= 1024 && d.coop && d.cus > 0) {
         const int64_t slots = grid_pass_list_slots(S, n, d.lds_max);
         if (slots >= 64) {
             const size_t lds = grid_pass_lds_bytes(S, n, slots);
@@ -94,6 +96,19 @@ void plan_workspace(Workspace &w, int S, int n, int B, const DeviceInfo &d)
             }
         }
     }
+}
+
+// Long pipelines of narrow stages (16 < n <= 64, more stages than the
+// register pass holds) run on the grid pass when the batch needs at most
+// kDeepGridLaunches launches of it, on the LDS pass otherwise: an instance
+// of 40 x 64 takes about 0.1 s on the grid pass (40 workgroups) and 1.9 s
+// on the LDS pass (one workgroup), but the LDS pass solves a whole large
+// batch at once (128 such instances: 1.85 s, against 2.13 s in 22 grid
+// launches of six).
+constexpr int kDeepGridLaunches = 8;
+bool grid_preferred(const Workspace &w, int n, int B)
+{
+    return n > 64 || (B + w.grid_conc - 1) / w.grid_conc <= kDeepGridLaunches;
 }
 
 // Calls f(&buffer_pointer, bytes) for every workspace buffer of B instances
@@ -268,7 +283,7 @@ PassResult run_passes(const Workspace &w, const DeviceInfo &d, int S, int n, hip
         p.route_all = 0;
         if ((e = launch_small_pass(p, stream)) != hipSuccess) return {GWTF_ERR_DEVICE, "packed solver launch", e};
         need_fallback = true;
-    } else if (w.grid) {
+    } else if (w.grid && grid_preferred(w, n, p.B)) {
         // Cooperative launches of up to grid_conc instances each; instances
         // whose link costs need more than 16 bits or whose flow lists outgrow
         // LDS go to the fallback pass.

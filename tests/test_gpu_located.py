@@ -71,6 +71,7 @@ def check(lb, g, ref, certify=None):
     (2, 130, 32, 3, mcf.GWTF_PASS_GRID),
     (5, 200, 10, 2, mcf.GWTF_PASS_GRID),
     (1, 100, 4, 3, mcf.GWTF_PASS_GRID),
+    (40, 48, 6, 3, mcf.GWTF_PASS_GRID),
     (2, 1, 1, 8, mcf.GWTF_PASS_PACKED),
 ])
 def test_random_located(S, n, L, B, expect_pass):

@@ -157,6 +157,19 @@ def test_grid_pass_batches(S, n, B):
         assert r_batch <= 2 * r_one + 16 and r_one <= 2 * r_batch + 16, (b, r_batch, r_one)
 
 
+@pytest.mark.parametrize("S,n,B,expect", [(40, 64, 5, mcf.GWTF_PASS_GRID), (33, 17, 2, mcf.GWTF_PASS_GRID),
+                                         (64, 40, 32, mcf.GWTF_PASS_GRID), (36, 32, 200, mcf.GWTF_PASS_LDS)])
+def test_long_narrow_pipelines(S, n, B, expect):
+    """More stages than the register pass holds, 16 < n <= 64: a batch that
+    needs at most eight grid launches runs on the grid pass (one workgroup
+    per stage), a larger one on the LDS pass (one workgroup per instance)."""
+    batch = W.random_small(B, S, n, seed=53, cap_hi=5, cost_hi=300, supply_hi=2 * n, holes=0.1, zero_cap=0.1)
+    say("long narrow", S, n, B)
+    g = gpu_solve(batch)
+    compare(batch, g, oracle.solve(batch), certify=[0, B - 1])
+    assert (g["passes"] == expect).all(), np.bincount(g["passes"])
+
+
 @pytest.mark.parametrize("S,n,cost_hi", [(3, 200, 0), (6, 130, 1), (12, 300, 2), (4, 512, 3)])
 def test_grid_pass_tied_exits(S, n, cost_hi):
     """Costs drawn from a handful of values make many exits of the last
